@@ -1,0 +1,275 @@
+/*
+ * hsap.h -- C ABI of libhsap: document-masked packed causal attention for one
+ * sequence-parallel shard, on AMD Instinct MI355X (gfx950).
+ *
+ * Method (HSAP, arxiv 2606.30460):
+ *   - Documents are packed into one sequence of N tokens and described by
+ *     their cumulative lengths (cu_seqlens); attention stays inside each
+ *     document and is causal there (sequence-packing section).
+ *   - Inter-group sequence parallelism cuts the sequence into P shards of
+ *     n = N / P tokens; a shard's queries meet every K/V chunk in ring order,
+ *     accumulating partial results online (inter-group SP section).
+ *   - SAP compiles, before any communication, which blocks of the packed
+ *     causal mask carry work so that empty blocks are neither sent nor
+ *     computed (compile step 1 of the SAP section); "computing" is the
+ *     attention of the Q block against the K/V block at hand (instruction
+ *     table of the SAP section).
+ *
+ * Conventions shared by every entry point:
+ *   - Positions are global token indices 0..N-1.  start(t) is the first
+ *     position of t's document.  Query i may attend key j iff
+ *     start(i) <= j <= i.
+ *   - Layout of the shards: CONTIGUOUS gives shard r positions r*n..r*n+n-1;
+ *     ZIGZAG cuts N into 2P pieces of m = N/(2P) and gives shard r piece r
+ *     followed by piece 2P-1-r.  A K/V chunk c has the layout of shard c.
+ *   - Ring order: at ring step s shard r holds chunk (r - s) mod P.
+ *   - Tensors are token-major: a row is one token, [heads, head_dim]
+ *     contiguous.  "Sharded order" [P, n, H, d] stores chunk c's n rows (in
+ *     that chunk's local order) at row offset c*n.
+ *   - Query head h reads K/V head h / (Hq / Hkv).
+ *   - bf16 is IEEE bfloat16 (1-8-7); LSE is the natural-log log-sum-exp of
+ *     the scaled scores, fp32, laid out [Hq, rows].
+ *   - Device pointers are caller-owned; the library allocates no device
+ *     memory and keeps no state between calls.  Kernels run asynchronously on
+ *     the given HIP stream (NULL = default stream).  HSAP_ERR_HIP reports a
+ *     launch failure only; a fault inside a kernel surfaces at the caller's
+ *     next synchronisation.
+ *   - Every argument is checked before anything is launched.  A failed check
+ *     returns an error, launches nothing and leaves outputs untouched;
+ *     hsap_last_error() then describes it.  No C++ exception crosses the ABI.
+ */
+#ifndef HSAP_H
+#define HSAP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HSAP_OK = 0,
+  HSAP_ERR_INVALID_ARG = 1,  /* malformed argument: nothing was done          */
+  HSAP_ERR_CAPACITY = 2,     /* output list too small: required size returned */
+  HSAP_ERR_UNSUPPORTED = 3,  /* valid, but no kernel for this shape           */
+  HSAP_ERR_HIP = 4           /* the HIP runtime refused a launch              */
+} hsap_status;
+
+typedef enum { HSAP_LAYOUT_CONTIGUOUS = 0, HSAP_LAYOUT_ZIGZAG = 1 } hsap_layout;
+
+/* A listed tile is FULL when all BM*BN of its (query, key) pairs are allowed
+ * (no mask is applied) and MASKED when only some are.  Tiles with no allowed
+ * pair are never listed. */
+typedef enum { HSAP_TILE_FULL = 0, HSAP_TILE_MASKED = 1 } hsap_tile_kind;
+
+/* Which tile index groups a run: HSAP_MAJOR_Q groups the tiles of one
+ * (chunk, q_tile) -- the forward's unit of work; HSAP_MAJOR_K groups the tiles
+ * of one (chunk, k_tile) -- the backward's. */
+typedef enum { HSAP_MAJOR_Q = 0, HSAP_MAJOR_K = 1 } hsap_major;
+
+/* One non-empty (q-tile, k-tile) block: 16-byte POD.  q_tile counts BM-row
+ * tiles of the shard's local rows, k_tile counts BN-row tiles of chunk
+ * `chunk`'s local rows. */
+typedef struct {
+  int32_t chunk;
+  int32_t q_tile;
+  int32_t k_tile;
+  int32_t kind;   /* hsap_tile_kind */
+} hsap_tile;
+
+/* A run of tiles that share (chunk, q_tile) [HSAP_MAJOR_Q] or
+ * (chunk, k_tile) [HSAP_MAJOR_K]: tiles[first .. first+count-1] of the list
+ * hsap_plan_runs returns.  `tile` is the shared q_tile or k_tile. */
+typedef struct {
+  int32_t chunk;
+  int32_t tile;
+  int32_t first;
+  int32_t count;
+} hsap_run;
+
+typedef struct {
+  int64_t total_tokens;  /* N                                               */
+  int32_t sp_degree;     /* P >= 1                                          */
+  int32_t layout;        /* hsap_layout                                     */
+  int32_t shard_id;      /* r in [0, P)                                     */
+  int32_t block_m;       /* BM: query rows per tile                         */
+  int32_t block_n;       /* BN: key rows per tile                           */
+} hsap_shard_desc;
+
+typedef struct {
+  hsap_shard_desc shard;
+  int32_t heads_q;       /* Hq                                              */
+  int32_t heads_kv;      /* Hkv, divides Hq                                 */
+  int32_t head_dim;      /* d: 64 or 128                                    */
+  float softmax_scale;   /* multiplies q.k; 1/sqrt(d) in the paper's formula */
+} hsap_attn_desc;
+
+/* Largest number of partials hsap_lse_merge combines in one call. */
+#define HSAP_MAX_MERGE_PARTS 64
+
+/* Human-readable name of a status code (static storage). */
+const char* hsap_status_string(hsap_status status);
+
+/* Description of the last error returned on the calling thread ("" if none). */
+const char* hsap_last_error(void);
+
+/*
+ * hsap_plan -- host planner: the non-empty tiles of one shard against every
+ * chunk, in canonical order.  Compile step 1 of the SAP section partitions
+ * the packed causal mask into per-rank blocks by their attention pattern;
+ * this does the same per (BM x BN) tile.
+ *
+ *   cu_seqlens   host int32 [num_docs + 1]: 0 = cu[0] <= cu[1] <= ... <=
+ *                cu[num_docs] = N.  Zero-length documents are allowed.
+ *   shard        N, P, layout, r, BM, BN.  Requires N % P == 0 (CONTIGUOUS)
+ *                or N % 2P == 0 (ZIGZAG), BM and BN dividing n (ZIGZAG: n/2)
+ *                and N < 2^31.
+ *   tiles        host [capacity] or NULL.  On success holds *num_tiles tiles
+ *                ordered by ring step, then q_tile, then k_tile.
+ *   num_tiles    out: number of non-empty tiles (also on HSAP_ERR_CAPACITY).
+ *   step_offsets host int64 [P + 1] or NULL: tiles of ring step s are
+ *                tiles[step_offsets[s] .. step_offsets[s+1]-1].
+ *   useful_pairs host int64 [P] or NULL: allowed (query, key) pairs per ring
+ *                step (per head).
+ * Returns HSAP_ERR_CAPACITY (with *num_tiles, step_offsets and useful_pairs
+ * filled) when tiles is NULL or capacity < *num_tiles: call again with room.
+ */
+hsap_status hsap_plan(const int32_t* cu_seqlens, int32_t num_docs, const hsap_shard_desc* shard,
+                      hsap_tile* tiles, int64_t capacity, int64_t* num_tiles,
+                      int64_t* step_offsets, int64_t* useful_pairs);
+
+/*
+ * hsap_plan_runs -- group a canonical tile list into runs of work for the
+ * kernels (host).  Not in the paper: it is this library's scheduling of the
+ * planner's list onto workgroups.
+ *
+ *   tiles, num_tiles  the list hsap_plan returned for `shard`.
+ *   major        HSAP_MAJOR_Q: one run per (chunk, q_tile) for every q_tile of
+ *                every chunk that has at least one tile -- q-tiles with none
+ *                get a run with count 0, so the forward writes LSE = -inf for
+ *                their rows.  sorted_tiles is the input order.
+ *                HSAP_MAJOR_K: one run per (chunk, k_tile) that has tiles;
+ *                sorted_tiles is ordered by ring step, k_tile, q_tile.
+ *   sorted_tiles host [num_tiles] out: the tiles the runs index.
+ *   runs         host [capacity] or NULL, out: ordered by count descending
+ *                (longest work first), ties by ring step then tile ascending.
+ *   num_runs     out: number of runs (also on HSAP_ERR_CAPACITY).
+ */
+hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles, int64_t num_tiles,
+                           int32_t major, hsap_tile* sorted_tiles, hsap_run* runs, int64_t capacity,
+                           int64_t* num_runs);
+
+/*
+ * hsap_doc_start -- device int32 [N]: start(t) for every position t.
+ *   cu_seqlens  device int32 [num_docs + 1] (same rules as hsap_plan; the
+ *               device copy is not re-validated).
+ */
+hsap_status hsap_doc_start(const int32_t* cu_seqlens, int32_t num_docs, int64_t total_tokens,
+                           int32_t* doc_start, void* hip_stream);
+
+/*
+ * hsap_shard_gather -- place a global-order tensor into sharded order (the
+ * in-memory stand-in for scattering a sequence over P ranks).
+ *   src  device [N rows] in global token order; dst device [P, n rows].
+ *   row_bytes  bytes per token row, a multiple of 16; src and dst 16-byte
+ *              aligned.  Uses shard->total_tokens, sp_degree and layout only.
+ */
+hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, void* dst,
+                              int64_t row_bytes, void* hip_stream);
+
+/*
+ * hsap_partial_attn_fwd -- "computing" for the forward: for every run (chunk
+ * c, q_tile t), the queries of q-tile t of shard r against the listed k-tiles
+ * of chunk c, producing c's partial output and log-sum-exp (attention
+ * equation of the inter-group SP section restricted to the packing mask).
+ *
+ *   desc       shard layout (N, P, layout, r, BM, BN) and heads / head_dim /
+ *              softmax scale.  Supported: d in {64, 128}; BM in {64, 128};
+ *              BN in {64, 128}; Hq % Hkv == 0.
+ *   q          device bf16 [n, Hq, d]: shard r's queries, local row order.
+ *   k, v       device bf16 [P, n, Hkv, d]: every chunk, sharded order.
+ *   doc_start  device int32 [N] from hsap_doc_start.
+ *   tiles      device hsap_tile [..]: sorted_tiles of hsap_plan_runs(MAJOR_Q).
+ *   runs       device hsap_run [num_runs] from hsap_plan_runs(MAJOR_Q); any
+ *              subset of them may be passed (e.g. one ring step's).
+ *   o_part     device fp32 [P, n, Hq, d]: for each run with count > 0, rows of
+ *              q-tile t in slot c receive the normalised partial output over
+ *              c's allowed keys (0 for a row with none).
+ *   lse_part   device fp32 [P, Hq, n]: rows of q-tile t in slot c receive the
+ *              partial LSE, -inf where the row has no allowed key in c
+ *              (always for a run with count 0).
+ *   Rows of o_part whose LSE is -inf are not written when count == 0 and
+ *   must not be read (hsap_lse_merge does not).  Rows outside every passed
+ *   run are untouched.
+ */
+hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, const void* k,
+                                  const void* v, const int32_t* doc_start, const hsap_tile* tiles,
+                                  const hsap_run* runs, int64_t num_runs, float* o_part,
+                                  float* lse_part, void* hip_stream);
+
+/*
+ * hsap_lse_merge -- online-softmax combination of partial results (the ring's
+ * online accumulation, after Milakov & Gimelshein, inter-group SP section):
+ *   L = m + ln sum_p exp(LSE_p - m),  m = max_p LSE_p;
+ *   O = sum_p exp(LSE_p - L) O_p, skipping parts whose LSE is -inf (their O
+ *   rows are never read); all -inf gives O = 0, L = -inf.
+ *
+ *   num_parts  1 .. HSAP_MAX_MERGE_PARTS.
+ *   o_parts    HOST array of num_parts device pointers, each fp32 [n, Hq, d].
+ *   lse_parts  HOST array of num_parts device pointers, each fp32 [Hq, n].
+ *   o_out      device bf16 [n, Hq, d] (round to nearest even).
+ *   lse_out    device fp32 [Hq, n].
+ *   Supported head_dim: 64, 128.  Output pointers 16-byte aligned.
+ */
+hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const float* const* lse_parts,
+                           int64_t n, int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out,
+                           void* hip_stream);
+
+/*
+ * hsap_attn_bwd_preprocess -- delta[h, i] = sum_d dO[i, h, d] * O[i, h, d]
+ * (fp32 accumulation), the per-row term of the softmax backward.
+ *   o, d_o  device bf16 [n, Hq, d];  delta device fp32 [Hq, n].
+ */
+hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, int32_t heads_q,
+                                     int32_t head_dim, float* delta, void* hip_stream);
+
+/*
+ * hsap_partial_attn_bwd -- "computing" for the backward: for every run
+ * (chunk c, k_tile u) and its listed q-tiles, recompute P = exp(s - LSE) from
+ * the final LSE and accumulate
+ *   dV_c += P^T dO,  dS = P o (dO V_c^T - delta),
+ *   dQ   += scale dS K_c,  dK_c += scale dS^T Q,
+ * with dK/dV summed over the query heads of each K/V head.
+ *
+ *   desc, q, k, v, doc_start  as for the forward.  Supported: d = 128 with
+ *              BN in {64, 128}, or d = 64 with BN = 64; BM a multiple of 64.
+ *   d_o        device bf16 [n, Hq, d] (shard r, local rows).
+ *   lse        device fp32 [Hq, n]: the merged forward LSE.
+ *   delta      device fp32 [Hq, n] from hsap_attn_bwd_preprocess.
+ *   tiles      device: sorted_tiles of hsap_plan_runs(MAJOR_K).
+ *   runs       device hsap_run [num_runs] from hsap_plan_runs(MAJOR_K).
+ *   dq_acc     device fp32 [n, Hq, d], accumulated with atomic adds (+=).
+ *   dk_acc, dv_acc  device fp32 [P, n, Hkv, d] sharded order (+=).  Each
+ *              (chunk, k_tile) row block is owned by one workgroup, so these
+ *              are plain read-modify-write.
+ *   The caller zeroes the accumulators once; concurrent calls on the same
+ *   accumulators race.
+ */
+hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, const void* k,
+                                  const void* v, const void* d_o, const float* lse,
+                                  const float* delta, const int32_t* doc_start,
+                                  const hsap_tile* tiles, const hsap_run* runs, int64_t num_runs,
+                                  float* dq_acc, float* dk_acc, float* dv_acc, void* hip_stream);
+
+/*
+ * hsap_convert_f32_bf16 -- dst[i] = bf16(src[i]), round to nearest even
+ * (finalising fp32 gradient accumulators).  count >= 0; pointers 16-byte
+ * aligned when count is a multiple of 8.
+ */
+hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HSAP_H */

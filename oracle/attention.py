@@ -252,7 +252,7 @@ def shard_backward(q, k, v, d_o, cu_seqlens, total_tokens: int, sp_degree: int, 
     probabilities of the backward come from that final LSE.  Returns
       ``dq``  [n, Hq, d] (shard-local row order),
       ``dk``/``dv`` [P, n, Hkv, d] indexed by chunk id, chunk-local row order,
-      ``o``/``lse``/``delta`` of the forward.
+      ``o``/``lse``/``delta`` of the forward, and ``fwd``, the forward's own dict.
     """
     fwd = shard_forward(q, k, v, cu_seqlens, total_tokens, sp_degree, layout, shard, scale)
     q_pos = fwd["q_pos"]
@@ -271,4 +271,4 @@ def shard_backward(q, k, v, d_o, cu_seqlens, total_tokens: int, sp_degree: int, 
         dq += dq_c
         dk[c] = dk_c
         dv[c] = dv_c
-    return {"dq": dq, "dk": dk, "dv": dv, "o": fwd["o"], "lse": fwd["lse"], "delta": delta}
+    return {"dq": dq, "dk": dk, "dv": dv, "o": fwd["o"], "lse": fwd["lse"], "delta": delta, "fwd": fwd}

@@ -1,0 +1,278 @@
+"""ctypes binding of libhsap (the C ABI declared in include/hsap.h).
+
+Argument marshalling only: every function here checks shapes and dtypes,
+passes raw pointers and sizes to the library and raises ``HsapError`` on a
+non-OK status.  Device buffers are torch tensors (torch supplies memory and
+the current HIP stream); host arrays are numpy arrays.  There is no fallback:
+if the library is not built, or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG_DIR, "libhsap.so")
+
+HSAP_OK = 0
+HSAP_ERR_INVALID_ARG = 1
+HSAP_ERR_CAPACITY = 2
+HSAP_ERR_UNSUPPORTED = 3
+HSAP_ERR_HIP = 4
+
+LAYOUT_CONTIGUOUS = 0
+LAYOUT_ZIGZAG = 1
+TILE_FULL = 0
+TILE_MASKED = 1
+MAJOR_Q = 0
+MAJOR_K = 1
+MAX_MERGE_PARTS = 64
+
+# Every symbol include/hsap.h declares.
+EXPORTED = (
+    "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_doc_start",
+    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
+    "hsap_partial_attn_bwd", "hsap_convert_f32_bf16",
+)
+
+
+class HsapError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("%s: %s" % (_status_name(status), message))
+        self.status = status
+
+
+class ShardDesc(ctypes.Structure):
+    _fields_ = [("total_tokens", ctypes.c_int64), ("sp_degree", ctypes.c_int32), ("layout", ctypes.c_int32),
+                ("shard_id", ctypes.c_int32), ("block_m", ctypes.c_int32), ("block_n", ctypes.c_int32)]
+
+
+class AttnDesc(ctypes.Structure):
+    _fields_ = [("shard", ShardDesc), ("heads_q", ctypes.c_int32), ("heads_kv", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_SIG = {
+    "hsap_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "hsap_last_error": (ctypes.c_char_p, []),
+    "hsap_plan": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _P, _P]),
+    "hsap_plan_runs": (ctypes.c_int, [_P, _P, _I64, _I32, _P, _P, _I64, _P]),
+    "hsap_doc_start": (ctypes.c_int, [_P, _I32, _I64, _P, _P]),
+    "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
+    "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
+    "hsap_lse_merge": (ctypes.c_int, [_I32, _P, _P, _I64, _I32, _I32, _P, _P, _P]),
+    "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
+    "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P, _P]),
+    "hsap_convert_f32_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libhsap.so is not built (%s); run __graft_entry__.build() or "
+                               "python -m paper_2606_30460_amd.build" % LIB_PATH)
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIG.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _status_name(status: int) -> str:
+    try:
+        return lib().hsap_status_string(status).decode()
+    except Exception:  # pragma: no cover
+        return "status %d" % status
+
+
+def _check(status: int) -> None:
+    if status != HSAP_OK:
+        raise HsapError(status, lib().hsap_last_error().decode())
+
+
+def layout_code(layout) -> int:
+    if isinstance(layout, str):
+        return {"contiguous": LAYOUT_CONTIGUOUS, "zigzag": LAYOUT_ZIGZAG}[layout]
+    return int(layout)
+
+
+def shard_desc(total_tokens: int, sp_degree: int, layout, shard_id: int, block_m: int, block_n: int) -> ShardDesc:
+    return ShardDesc(int(total_tokens), int(sp_degree), layout_code(layout), int(shard_id), int(block_m), int(block_n))
+
+
+def attn_desc(shard: ShardDesc, heads_q: int, heads_kv: int, head_dim: int, softmax_scale: float) -> AttnDesc:
+    return AttnDesc(shard, int(heads_q), int(heads_kv), int(head_dim), float(softmax_scale))
+
+
+def _ptr(a) -> int:
+    """Raw address of a numpy array or torch tensor (None -> NULL)."""
+    if a is None:
+        return 0
+    if isinstance(a, np.ndarray):
+        return a.ctypes.data
+    return int(a.data_ptr())
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)
+
+
+def _dev(t, dtype_name: str, what: str, numel: Optional[int] = None):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a device tensor" % what)
+    if str(t.dtype) != "torch." + dtype_name:
+        raise TypeError("%s must be %s, got %s" % (what, dtype_name, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % what)
+    if numel is not None and t.numel() != numel:
+        raise ValueError("%s has %d elements, expected %d" % (what, t.numel(), numel))
+    return t
+
+
+# ---------------------------------------------------------------------------
+# host planner
+# ---------------------------------------------------------------------------
+
+def plan(cu_seqlens, shard: ShardDesc) -> Dict[str, np.ndarray]:
+    """hsap_plan with the two-call pattern.  Returns tiles int32 [T, 4],
+    step_offsets int64 [P+1], useful_pairs int64 [P]."""
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    P = shard.sp_degree
+    num = ctypes.c_int64(0)
+    offs = np.zeros(max(P, 0) + 1, dtype=np.int64)
+    pairs = np.zeros(max(P, 1), dtype=np.int64)
+    st = lib().hsap_plan(_ptr(cu), len(cu) - 1, ctypes.byref(shard), None, 0, ctypes.byref(num),
+                         _ptr(offs), _ptr(pairs))
+    if st != HSAP_ERR_CAPACITY:
+        _check(st)
+    tiles = np.zeros((max(num.value, 1), 4), dtype=np.int32)
+    _check(lib().hsap_plan(_ptr(cu), len(cu) - 1, ctypes.byref(shard), _ptr(tiles), tiles.shape[0],
+                           ctypes.byref(num), _ptr(offs), _ptr(pairs)))
+    return {"tiles": tiles[: num.value], "step_offsets": offs, "useful_pairs": pairs[:P]}
+
+
+def plan_runs(shard: ShardDesc, tiles: np.ndarray, major: int) -> Tuple[np.ndarray, np.ndarray]:
+    """hsap_plan_runs.  Returns (sorted_tiles int32 [T, 4], runs int32 [R, 4])."""
+    tiles = np.ascontiguousarray(tiles, dtype=np.int32).reshape(-1, 4)
+    sorted_tiles = np.zeros((max(len(tiles), 1), 4), dtype=np.int32)
+    num = ctypes.c_int64(0)
+    st = lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), len(tiles), int(major), _ptr(sorted_tiles), None, 0,
+                              ctypes.byref(num))
+    if st != HSAP_ERR_CAPACITY:
+        _check(st)
+    runs = np.zeros((max(num.value, 1), 4), dtype=np.int32)
+    _check(lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), len(tiles), int(major), _ptr(sorted_tiles),
+                                _ptr(runs), runs.shape[0], ctypes.byref(num)))
+    return sorted_tiles[: len(tiles)], runs[: num.value]
+
+
+# ---------------------------------------------------------------------------
+# device entry points
+# ---------------------------------------------------------------------------
+
+def doc_start(cu_seqlens_dev, total_tokens: int, out, stream=None) -> None:
+    _dev(cu_seqlens_dev, "int32", "cu_seqlens")
+    _dev(out, "int32", "doc_start", total_tokens)
+    _check(lib().hsap_doc_start(_ptr(cu_seqlens_dev), cu_seqlens_dev.numel() - 1, int(total_tokens), _ptr(out),
+                                _stream(stream)))
+
+
+def shard_gather(shard: ShardDesc, src, dst, stream=None) -> None:
+    import torch
+    if src.shape != dst.shape or src.dtype != dst.dtype or not (src.is_cuda and dst.is_cuda):
+        raise ValueError("src and dst must be device tensors of one shape and dtype")
+    if not (src.is_contiguous() and dst.is_contiguous()) or src.shape[0] != shard.total_tokens:
+        raise ValueError("src and dst must be contiguous with total_tokens rows")
+    row_bytes = src[0].numel() * src.element_size() if src.shape[0] else 0
+    del torch
+    _check(lib().hsap_shard_gather(ctypes.byref(shard), _ptr(src), _ptr(dst), int(row_bytes), _stream(stream)))
+
+
+def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev, o_part, lse_part,
+                     stream=None) -> None:
+    s = desc.shard
+    n = s.total_tokens // s.sp_degree
+    hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
+    _dev(q, "bfloat16", "q", n * hq * d)
+    _dev(k, "bfloat16", "k", P * n * hkv * d)
+    _dev(v, "bfloat16", "v", P * n * hkv * d)
+    _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
+    _dev(tiles_dev, "int32", "tiles")
+    _dev(runs_dev, "int32", "runs")
+    _dev(o_part, "float32", "o_part", P * n * hq * d)
+    _dev(lse_part, "float32", "lse_part", P * hq * n)
+    _check(lib().hsap_partial_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(doc_start_dev),
+                                       _ptr(tiles_dev), _ptr(runs_dev), runs_dev.numel() // 4, _ptr(o_part),
+                                       _ptr(lse_part), _stream(stream)))
+
+
+def lse_merge(o_parts: Sequence, lse_parts: Sequence, n: int, heads_q: int, head_dim: int, o_out, lse_out,
+              stream=None) -> None:
+    if len(o_parts) != len(lse_parts) or not o_parts:
+        raise ValueError("need matching, non-empty part lists")
+    for i, (o, l) in enumerate(zip(o_parts, lse_parts)):
+        _dev(o, "float32", "o_parts[%d]" % i, n * heads_q * head_dim)
+        _dev(l, "float32", "lse_parts[%d]" % i, heads_q * n)
+    _dev(o_out, "bfloat16", "o_out", n * heads_q * head_dim)
+    _dev(lse_out, "float32", "lse_out", heads_q * n)
+    np_ = len(o_parts)
+    o_arr = (ctypes.c_void_p * np_)(*[_ptr(t) for t in o_parts])
+    l_arr = (ctypes.c_void_p * np_)(*[_ptr(t) for t in lse_parts])
+    _check(lib().hsap_lse_merge(np_, o_arr, l_arr, int(n), int(heads_q), int(head_dim), _ptr(o_out), _ptr(lse_out),
+                                _stream(stream)))
+
+
+def attn_bwd_preprocess(o, d_o, n: int, heads_q: int, head_dim: int, delta, stream=None) -> None:
+    _dev(o, "bfloat16", "o", n * heads_q * head_dim)
+    _dev(d_o, "bfloat16", "d_o", n * heads_q * head_dim)
+    _dev(delta, "float32", "delta", heads_q * n)
+    _check(lib().hsap_attn_bwd_preprocess(_ptr(o), _ptr(d_o), int(n), int(heads_q), int(head_dim), _ptr(delta),
+                                          _stream(stream)))
+
+
+def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_dev, runs_dev, dq_acc, dk_acc,
+                     dv_acc, stream=None) -> None:
+    s = desc.shard
+    n = s.total_tokens // s.sp_degree
+    hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
+    _dev(q, "bfloat16", "q", n * hq * d)
+    _dev(k, "bfloat16", "k", P * n * hkv * d)
+    _dev(v, "bfloat16", "v", P * n * hkv * d)
+    _dev(d_o, "bfloat16", "d_o", n * hq * d)
+    _dev(lse, "float32", "lse", hq * n)
+    _dev(delta, "float32", "delta", hq * n)
+    _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
+    _dev(tiles_dev, "int32", "tiles")
+    _dev(runs_dev, "int32", "runs")
+    _dev(dq_acc, "float32", "dq_acc", n * hq * d)
+    _dev(dk_acc, "float32", "dk_acc", P * n * hkv * d)
+    _dev(dv_acc, "float32", "dv_acc", P * n * hkv * d)
+    _check(lib().hsap_partial_attn_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(d_o), _ptr(lse),
+                                       _ptr(delta), _ptr(doc_start_dev), _ptr(tiles_dev), _ptr(runs_dev),
+                                       runs_dev.numel() // 4, _ptr(dq_acc), _ptr(dk_acc), _ptr(dv_acc),
+                                       _stream(stream)))
+
+
+def convert_f32_bf16(src, dst, stream=None) -> None:
+    _dev(src, "float32", "src")
+    _dev(dst, "bfloat16", "dst", src.numel())
+    _check(lib().hsap_convert_f32_bf16(_ptr(src), _ptr(dst), src.numel(), _stream(stream)))

@@ -1,0 +1,34 @@
+// CDNA4 (gfx950) matrix-core helpers shared by the attention kernels.
+//
+// v_mfma_f32_32x32x16_bf16 computes C[32x32] += A[32x16] * B[16x32] for one
+// 64-lane wave, fp32 accumulation.  Lane l (l32 = l % 32, hi = l / 32):
+//   A operand: row l32 of A, eight consecutive k values of half `hi`;
+//   B operand: column l32 of B, eight k values of half `hi` (same k order
+//              as A, so any fixed permutation of k applied to both operands
+//              leaves the product unchanged);
+//   C/D:       column l32 of C, rows 8*(j/4) + 4*hi + (j%4) in register j.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace hsap {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Row index (within a 32-row C block) held by register j of a lane in half hi.
+__device__ __forceinline__ constexpr int c_row(int j, int hi) { return 8 * (j >> 2) + 4 * hi + (j & 3); }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ bf16x8 cat4(const bf16x4& a, const bf16x4& b) {
+  return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+}  // namespace hsap

@@ -1,0 +1,246 @@
+// Memory-bound kernels of libhsap: the LSE merge of partial results, the
+// backward's row term delta = rowsum(dO * O), fp32 -> bf16 conversion, the
+// per-position document start, and the gather into sharded order.
+#include "hsap_internal.h"
+#include "mfma.h"
+
+namespace hsap {
+
+// ---------------------------------------------------------------------------
+// LSE merge (online-softmax combination of the ring's partial results)
+//
+// Thread layout: D/4 consecutive lanes own one (row, head) and 4 consecutive
+// d each, so a (row, head) of a partial is one contiguous 4*D-byte read.
+// Each lane reads the partials' LSE values itself (same address across the
+// D/4 lanes: one broadcast), and skips the O read of parts at -inf.
+// ---------------------------------------------------------------------------
+struct MergeArgs {
+  const float* o[HSAP_MAX_MERGE_PARTS];
+  const float* lse[HSAP_MAX_MERGE_PARTS];
+  int32_t num_parts;
+  int32_t hq;
+  int64_t n;
+  __bf16* o_out;
+  float* lse_out;
+};
+
+template <int D>
+__global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
+  constexpr int TPR = D / 4;
+  constexpr float NEG_INF = -__builtin_inff();
+  constexpr float LOG2E = 1.44269504088896340736f;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t rh = gid / TPR;  // rh = row * hq + head
+  const int part = (int)(gid % TPR);
+  if (rh >= a.n * a.hq) return;
+  const int64_t row = rh / a.hq;
+  const int h = (int)(rh - row * a.hq);
+  const int64_t li = (int64_t)h * a.n + row;
+  float mx = NEG_INF;
+  for (int p = 0; p < a.num_parts; ++p) mx = fmaxf(mx, a.lse[p][li]);
+  f32x4 acc{0.f, 0.f, 0.f, 0.f};
+  float L = NEG_INF;
+  if (mx != NEG_INF) {
+    float sum = 0.f;
+    for (int p = 0; p < a.num_parts; ++p) sum += fast_exp2((a.lse[p][li] - mx) * LOG2E);
+    L = mx + __logf(sum);
+    for (int p = 0; p < a.num_parts; ++p) {
+      const float lp = a.lse[p][li];
+      if (lp == NEG_INF) continue;
+      const float wgt = fast_exp2((lp - L) * LOG2E);
+      const f32x4 x = *(const f32x4*)(a.o[p] + rh * D + 4 * part);
+      acc += wgt * x;
+    }
+  }
+  const bf16x4 out{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+  *(bf16x4*)(a.o_out + rh * D + 4 * part) = out;
+  if (part == 0) a.lse_out[li] = L;
+}
+
+// ---------------------------------------------------------------------------
+// delta[h, i] = sum_d dO[i, h, d] * O[i, h, d]
+// D/8 lanes per (row, head), 8 bf16 each, reduced with lane shuffles.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void bwd_preprocess_kernel(const __bf16* o, const __bf16* d_o, int64_t n, int32_t hq,
+                                                             float* delta) {
+  constexpr int TPR = D / 8;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t rh = gid / TPR;
+  const int part = (int)(gid % TPR);
+  const bool live = rh < n * hq;
+  float acc = 0.f;
+  if (live) {
+    const bf16x8 x = *(const bf16x8*)(o + rh * D + 8 * part);
+    const bf16x8 y = *(const bf16x8*)(d_o + rh * D + 8 * part);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc += (float)x[e] * (float)y[e];
+  }
+#pragma unroll
+  for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (live && part == 0) {
+    const int64_t row = rh / hq;
+    const int h = (int)(rh - row * hq);
+    delta[(int64_t)h * n + row] = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 -> bf16 (round to nearest even), 8 elements per thread when aligned
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void convert_kernel(const float* src, __bf16* dst, int64_t count, int vec) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i * 8 < count; i += stride) {
+    if (vec && i * 8 + 8 <= count) {
+      const f32x4 a = *(const f32x4*)(src + i * 8);
+      const f32x4 b = *(const f32x4*)(src + i * 8 + 4);
+      const bf16x8 out{(__bf16)a[0], (__bf16)a[1], (__bf16)a[2], (__bf16)a[3],
+                       (__bf16)b[0], (__bf16)b[1], (__bf16)b[2], (__bf16)b[3]};
+      *(bf16x8*)(dst + i * 8) = out;
+    } else {
+      for (int64_t j = i * 8; j < i * 8 + 8 && j < count; ++j) dst[j] = (__bf16)src[j];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// doc_start[t] = cu[k] for the last k with cu[k] <= t (binary search)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void doc_start_kernel(const int32_t* cu, int32_t num_docs, int64_t total,
+                                                        int32_t* out) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += stride) {
+    int32_t lo = 0, hi = num_docs;  // invariant: cu[lo] <= t < cu[hi]
+    while (hi - lo > 1) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (cu[mid] <= t) lo = mid;
+      else hi = mid;
+    }
+    out[t] = cu[lo];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dst[c, l] = src[position of chunk c's local row l], 16 bytes per lane
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void gather_kernel(Geom g, const uint4* src, uint4* dst, int64_t words_per_row) {
+  const int64_t total = g.N * words_per_row;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += stride) {
+    const int64_t row = i / words_per_row, word = i - row * words_per_row;
+    const int32_t c = (int32_t)(row / g.n);
+    const int64_t local = row - (int64_t)c * g.n;
+    dst[i] = src[global_pos(g, c, local) * words_per_row + word];
+  }
+}
+
+static hsap_status check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
+  return HSAP_OK;
+}
+
+static unsigned grid_for(int64_t threads) {
+  const int64_t b = (threads + 255) / 256;
+  return (unsigned)(b < 1 ? 1 : (b > 65536 ? 65536 : b));
+}
+
+}  // namespace hsap
+
+using namespace hsap;
+
+extern "C" {
+
+hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const float* const* lse_parts, int64_t n,
+                           int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, void* hip_stream) {
+  clear_error();
+  if (num_parts < 1 || num_parts > HSAP_MAX_MERGE_PARTS)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_parts %d outside 1..%d", num_parts, HSAP_MAX_MERGE_PARTS);
+  if (!o_parts || !lse_parts || !o_out || !lse_out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (n < 0 || heads_q <= 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "bad n=%lld or heads_q=%d", (long long)n, heads_q);
+  if (head_dim != 64 && head_dim != 128) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "head_dim %d not supported", head_dim);
+  MergeArgs a;
+  for (int p = 0; p < num_parts; ++p) {
+    if (!o_parts[p] || !lse_parts[p]) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "part %d pointer is NULL", p);
+    if ((uintptr_t)o_parts[p] & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_parts[%d] not 16-byte aligned", p);
+    a.o[p] = o_parts[p];
+    a.lse[p] = lse_parts[p];
+  }
+  if ((uintptr_t)o_out & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_out not 16-byte aligned");
+  if (n == 0) return HSAP_OK;
+  a.num_parts = num_parts;
+  a.hq = heads_q;
+  a.n = n;
+  a.o_out = (__bf16*)o_out;
+  a.lse_out = lse_out;
+  const int64_t threads = n * heads_q * (head_dim / 4);
+  const int64_t blocks = (threads + 255) / 256;
+  if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "problem too large");
+  hipStream_t s = (hipStream_t)hip_stream;
+  if (head_dim == 128) hipLaunchKernelGGL(lse_merge_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(lse_merge_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  return check_launch("lse_merge");
+}
+
+hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, int32_t heads_q, int32_t head_dim,
+                                     float* delta, void* hip_stream) {
+  clear_error();
+  if (!o || !d_o || !delta) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (n < 0 || heads_q <= 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "bad n=%lld or heads_q=%d", (long long)n, heads_q);
+  if (head_dim != 64 && head_dim != 128) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "head_dim %d not supported", head_dim);
+  if (((uintptr_t)o | (uintptr_t)d_o) & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o and d_o must be 16-byte aligned");
+  if (n == 0) return HSAP_OK;
+  const int64_t threads = n * heads_q * (head_dim / 8);
+  const int64_t blocks = (threads + 255) / 256;
+  if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "problem too large");
+  hipStream_t s = (hipStream_t)hip_stream;
+  if (head_dim == 128)
+    hipLaunchKernelGGL(bwd_preprocess_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, s, (const __bf16*)o,
+                       (const __bf16*)d_o, n, heads_q, delta);
+  else
+    hipLaunchKernelGGL(bwd_preprocess_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, s, (const __bf16*)o,
+                       (const __bf16*)d_o, n, heads_q, delta);
+  return check_launch("bwd_preprocess");
+}
+
+hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, void* hip_stream) {
+  clear_error();
+  if (count < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "count < 0");
+  if (count == 0) return HSAP_OK;
+  if (!src || !dst) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  const int vec = (((uintptr_t)src | (uintptr_t)dst) & 15) == 0;
+  hipLaunchKernelGGL(convert_kernel, dim3(grid_for((count + 7) / 8)), dim3(256), 0, (hipStream_t)hip_stream, src,
+                     (__bf16*)dst, count, vec);
+  return check_launch("convert");
+}
+
+hsap_status hsap_doc_start(const int32_t* cu_seqlens, int32_t num_docs, int64_t total_tokens, int32_t* doc_start,
+                           void* hip_stream) {
+  clear_error();
+  if (!cu_seqlens || !doc_start) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (num_docs < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_docs %d < 1", num_docs);
+  if (total_tokens <= 0 || total_tokens > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "bad total_tokens");
+  hipLaunchKernelGGL(doc_start_kernel, dim3(grid_for(total_tokens)), dim3(256), 0, (hipStream_t)hip_stream,
+                     cu_seqlens, num_docs, total_tokens, doc_start);
+  return check_launch("doc_start");
+}
+
+hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, void* dst, int64_t row_bytes,
+                              void* hip_stream) {
+  clear_error();
+  if (!shard) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "shard descriptor is NULL");
+  hsap_shard_desc d = *shard;
+  d.shard_id = 0;  // only N, P and the layout matter here
+  d.block_m = d.block_n = 1;
+  Geom g;
+  hsap_status st = check_shard(&d, &g);
+  if (st != HSAP_OK) return st;
+  if (!src || !dst) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (row_bytes <= 0 || row_bytes % 16) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "row_bytes must be a positive multiple of 16");
+  if (((uintptr_t)src | (uintptr_t)dst) & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "src and dst must be 16-byte aligned");
+  hipLaunchKernelGGL(gather_kernel, dim3(grid_for(g.N * (row_bytes / 16))), dim3(256), 0, (hipStream_t)hip_stream, g,
+                     (const uint4*)src, (uint4*)dst, row_bytes / 16);
+  return check_launch("shard_gather");
+}
+
+}  // extern "C"

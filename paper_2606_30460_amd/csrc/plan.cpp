@@ -1,0 +1,287 @@
+// Host side of libhsap: argument checks, error strings and the tile planner.
+//
+// The planner follows compile step 1 of the SAP section: the packed causal
+// mask is cut into blocks that one rank computes against one K/V chunk and
+// each block is classified by its attention pattern, so blocks with nothing
+// to attend are neither transferred nor computed.  Here the blocks are
+// BM x BN tiles and the classes are EMPTY (dropped), FULL and MASKED.
+//
+// Counting is interval arithmetic, never pair by pair:
+//   * a q-tile covers consecutive global positions [qa, qb] (tiles never
+//     straddle two zigzag pieces), so the keys its rows may attend form the
+//     single window [start(qa), qb]; every k-tile meeting that window holds
+//     at least one allowed pair and every other k-tile holds none;
+//   * a tile is FULL iff start(qb) <= ka and kb <= qa (the latest document
+//     start among its rows is at or before its first key, and its last key is
+//     at or before its first query);
+//   * otherwise its pair count is summed per document segment of its rows as
+//     two arithmetic series (rows before the k-tile's end, rows after it).
+#include <algorithm>
+#include <cstdarg>
+#include <cstring>
+#include <numeric>
+#include <vector>
+
+#include "hsap_internal.h"
+
+namespace hsap {
+
+static thread_local std::string g_last_error;
+
+void set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+hsap_status check_shard(const hsap_shard_desc* d, Geom* g) {
+  if (!d) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "shard descriptor is NULL");
+  if (d->total_tokens <= 0 || d->total_tokens > INT32_MAX)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "total_tokens %lld outside 1..2^31-1", (long long)d->total_tokens);
+  if (d->sp_degree < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "sp_degree %d < 1", d->sp_degree);
+  if (d->shard_id < 0 || d->shard_id >= d->sp_degree)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "shard_id %d outside 0..%d", d->shard_id, d->sp_degree - 1);
+  if (d->layout != HSAP_LAYOUT_CONTIGUOUS && d->layout != HSAP_LAYOUT_ZIGZAG)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "unknown layout %d", d->layout);
+  const int64_t N = d->total_tokens, P = d->sp_degree;
+  const int64_t split = d->layout == HSAP_LAYOUT_ZIGZAG ? 2 * P : P;
+  if (N % split)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "total_tokens %lld not divisible by %lld", (long long)N, (long long)split);
+  const int64_t piece = N / split;
+  if (d->block_m <= 0 || d->block_n <= 0)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "tile sizes must be positive (BM=%d BN=%d)", d->block_m, d->block_n);
+  if (piece % d->block_m || piece % d->block_n)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "BM=%d and BN=%d must divide the %s length %lld", d->block_m, d->block_n,
+              d->layout == HSAP_LAYOUT_ZIGZAG ? "zigzag piece" : "shard", (long long)piece);
+  g->N = N;
+  g->n = N / P;
+  g->m = piece;
+  g->P = (int32_t)P;
+  g->layout = d->layout;
+  return HSAP_OK;
+}
+
+hsap_status check_attn(const hsap_attn_desc* d, Geom* g) {
+  if (!d) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "attention descriptor is NULL");
+  hsap_status st = check_shard(&d->shard, g);
+  if (st != HSAP_OK) return st;
+  if (d->heads_q <= 0 || d->heads_kv <= 0 || d->heads_q % d->heads_kv)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "heads_q=%d must be a positive multiple of heads_kv=%d", d->heads_q,
+              d->heads_kv);
+  if (!(d->softmax_scale > 0.f) || d->softmax_scale > 1e30f)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
+  if (d->head_dim != 64 && d->head_dim != 128)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d->head_dim);
+  return HSAP_OK;
+}
+
+namespace {
+
+// Positions of shard x's local rows, as (global start, local start, length) pieces.
+struct Piece {
+  int64_t global0, local0, len;
+};
+
+int shard_pieces(const Geom& g, int32_t x, Piece out[2]) {
+  if (g.layout == HSAP_LAYOUT_CONTIGUOUS) {
+    out[0] = {(int64_t)x * g.n, 0, g.n};
+    return 1;
+  }
+  out[0] = {(int64_t)x * g.m, 0, g.m};
+  out[1] = {(int64_t)(2 * g.P - 1 - x) * g.m, g.m, g.m};
+  return 2;
+}
+
+// Index of the document holding position t (the last k with cu[k] <= t).
+inline int64_t doc_of(const int32_t* cu, int32_t num_docs, int64_t t) {
+  const int32_t* it = std::upper_bound(cu, cu + num_docs + 1, (int32_t)t);
+  return (int64_t)(it - cu) - 1;
+}
+
+// Allowed pairs between query rows [qa, qb] (document of qa: dq) and keys [ka, kb].
+int64_t tile_pairs(const int32_t* cu, int64_t dq, int64_t qa, int64_t qb, int64_t ka, int64_t kb) {
+  int64_t total = 0;
+  for (int64_t d = dq;; ++d) {
+    const int64_t s = cu[d], e = cu[d + 1];  // document d covers [s, e)
+    if (e > s) {
+      const int64_t ra = std::max(qa, s), rb = std::min(qb, e - 1);
+      if (ra <= rb) {
+        const int64_t lo = std::max(s, ka);  // first key any row of this segment may use
+        // rows i <= kb contribute i - lo + 1 (when i >= lo)
+        const int64_t a1 = std::max(ra, lo), b1 = std::min(rb, kb);
+        if (a1 <= b1) total += ((a1 - lo + 1) + (b1 - lo + 1)) * (b1 - a1 + 1) / 2;
+        // rows i > kb contribute kb - lo + 1 (when kb >= lo)
+        const int64_t a2 = std::max(ra, kb + 1);
+        if (a2 <= rb && kb >= lo) total += (rb - a2 + 1) * (kb - lo + 1);
+      }
+    }
+    if (e - 1 >= qb) break;
+  }
+  return total;
+}
+
+}  // namespace
+}  // namespace hsap
+
+using namespace hsap;
+
+extern "C" {
+
+const char* hsap_status_string(hsap_status status) {
+  switch (status) {
+    case HSAP_OK: return "HSAP_OK";
+    case HSAP_ERR_INVALID_ARG: return "HSAP_ERR_INVALID_ARG";
+    case HSAP_ERR_CAPACITY: return "HSAP_ERR_CAPACITY";
+    case HSAP_ERR_UNSUPPORTED: return "HSAP_ERR_UNSUPPORTED";
+    case HSAP_ERR_HIP: return "HSAP_ERR_HIP";
+  }
+  return "HSAP_ERR_UNKNOWN";
+}
+
+const char* hsap_last_error(void) { return g_last_error.c_str(); }
+
+hsap_status hsap_plan(const int32_t* cu, int32_t num_docs, const hsap_shard_desc* shard, hsap_tile* tiles,
+                      int64_t capacity, int64_t* num_tiles, int64_t* step_offsets, int64_t* useful_pairs) {
+  clear_error();
+  Geom g;
+  hsap_status st = check_shard(shard, &g);
+  if (st != HSAP_OK) return st;
+  if (!cu) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if (!num_tiles) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_tiles is NULL");
+  if (num_docs < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_docs %d < 1", num_docs);
+  if (capacity < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "capacity < 0");
+  if (cu[0] != 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens[0] = %d, expected 0", cu[0]);
+  for (int32_t i = 0; i < num_docs; ++i)
+    if (cu[i + 1] < cu[i]) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens decreases at %d", i + 1);
+  if ((int64_t)cu[num_docs] != g.N)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens[%d] = %d, expected total_tokens %lld", num_docs, cu[num_docs],
+              (long long)g.N);
+
+  const int32_t P = g.P, r = shard->shard_id;
+  const int64_t BM = shard->block_m, BN = shard->block_n;
+  const int64_t full = BM * BN;
+  Piece qp[2], kp[2];
+  const int nq_pieces = shard_pieces(g, r, qp);
+  const bool store = tiles != nullptr;
+  int64_t count = 0;
+  if (step_offsets) step_offsets[0] = 0;
+  for (int32_t step = 0; step < P; ++step) {
+    const int32_t c = ((r - step) % P + P) % P;
+    const int nk_pieces = shard_pieces(g, c, kp);
+    int64_t step_pairs = 0;
+    for (int qi = 0; qi < nq_pieces; ++qi) {
+      for (int64_t l0 = 0; l0 < qp[qi].len; l0 += BM) {
+        const int64_t qa = qp[qi].global0 + l0, qb = qa + BM - 1;
+        const int64_t q_tile = (qp[qi].local0 + l0) / BM;
+        const int64_t dq = doc_of(cu, num_docs, qa);
+        const int64_t s_first = cu[dq];
+        const int64_t s_last = cu[doc_of(cu, num_docs, qb)];
+        for (int ki = 0; ki < nk_pieces; ++ki) {
+          const int64_t pa = kp[ki].global0, pb = pa + kp[ki].len - 1;
+          const int64_t x = std::max(s_first, pa), y = std::min(qb, pb);
+          if (x > y) continue;
+          const int64_t u0 = (kp[ki].local0 + (x - pa)) / BN, u1 = (kp[ki].local0 + (y - pa)) / BN;
+          for (int64_t u = u0; u <= u1; ++u) {
+            const int64_t ka = pa + (u * BN - kp[ki].local0), kb = ka + BN - 1;
+            const bool is_full = s_last <= ka && kb <= qa;
+            const int64_t pairs = is_full ? full : tile_pairs(cu, dq, qa, qb, ka, kb);
+            if (pairs == 0) continue;
+            if (store && count < capacity)
+              tiles[count] = hsap_tile{c, (int32_t)q_tile, (int32_t)u, pairs == full ? HSAP_TILE_FULL : HSAP_TILE_MASKED};
+            ++count;
+            step_pairs += pairs;
+          }
+        }
+      }
+    }
+    if (step_offsets) step_offsets[step + 1] = count;
+    if (useful_pairs) useful_pairs[step] = step_pairs;
+  }
+  *num_tiles = count;
+  if (!store || count > capacity)
+    HSAP_FAIL(HSAP_ERR_CAPACITY, "tile list needs %lld entries, capacity %lld", (long long)count, (long long)capacity);
+  return HSAP_OK;
+}
+
+hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles, int64_t num_tiles, int32_t major,
+                           hsap_tile* sorted_tiles, hsap_run* runs, int64_t capacity, int64_t* num_runs) {
+  clear_error();
+  Geom g;
+  hsap_status st = check_shard(shard, &g);
+  if (st != HSAP_OK) return st;
+  if (major != HSAP_MAJOR_Q && major != HSAP_MAJOR_K) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "unknown major %d", major);
+  if (num_tiles < 0 || (num_tiles > 0 && !tiles)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "tiles is NULL");
+  if (num_tiles > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many tiles");
+  if (!num_runs) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_runs is NULL");
+  if (num_tiles > 0 && !sorted_tiles) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "sorted_tiles is NULL");
+  if (capacity < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "capacity < 0");
+  const int32_t P = g.P, r = shard->shard_id;
+  const int64_t nq = g.n / shard->block_m, nk = g.n / shard->block_n;
+  auto step_of = [&](int32_t c) { return ((r - c) % P + P) % P; };
+  // the list must be canonical: ring step, q_tile, k_tile strictly increasing
+  for (int64_t i = 0; i < num_tiles; ++i) {
+    const hsap_tile& t = tiles[i];
+    if (t.chunk < 0 || t.chunk >= P || t.q_tile < 0 || t.q_tile >= nq || t.k_tile < 0 || t.k_tile >= nk ||
+        (t.kind != HSAP_TILE_FULL && t.kind != HSAP_TILE_MASKED))
+      HSAP_FAIL(HSAP_ERR_INVALID_ARG, "tile %lld out of range", (long long)i);
+    if (i > 0) {
+      const hsap_tile& p = tiles[i - 1];
+      const int64_t a = ((int64_t)step_of(p.chunk) * nq + p.q_tile) * nk + p.k_tile;
+      const int64_t b = ((int64_t)step_of(t.chunk) * nq + t.q_tile) * nk + t.k_tile;
+      if (b <= a) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "tile list not in canonical order at %lld", (long long)i);
+    }
+  }
+  std::vector<hsap_run> out;
+  if (major == HSAP_MAJOR_Q) {
+    if (num_tiles > 0) std::memcpy(sorted_tiles, tiles, sizeof(hsap_tile) * num_tiles);
+    int64_t i = 0;
+    while (i < num_tiles) {
+      const int32_t c = tiles[i].chunk;
+      // every q-tile of this chunk gets a run, empty or not
+      for (int32_t t = 0; t < nq; ++t) {
+        int64_t j = i;
+        while (j < num_tiles && tiles[j].chunk == c && tiles[j].q_tile == t) ++j;
+        out.push_back(hsap_run{c, t, (int32_t)i, (int32_t)(j - i)});
+        i = j;
+      }
+    }
+  } else {
+    std::vector<int64_t> order(num_tiles);
+    std::iota(order.begin(), order.end(), 0);
+    auto key = [&](int64_t i) {
+      const hsap_tile& t = tiles[i];
+      return ((int64_t)step_of(t.chunk) * nk + t.k_tile) * nq + t.q_tile;
+    };
+    std::sort(order.begin(), order.end(), [&](int64_t a, int64_t b) { return key(a) < key(b); });
+    for (int64_t i = 0; i < num_tiles; ++i) sorted_tiles[i] = tiles[order[i]];
+    int64_t i = 0;
+    while (i < num_tiles) {
+      int64_t j = i;
+      while (j < num_tiles && sorted_tiles[j].chunk == sorted_tiles[i].chunk &&
+             sorted_tiles[j].k_tile == sorted_tiles[i].k_tile)
+        ++j;
+      out.push_back(hsap_run{sorted_tiles[i].chunk, sorted_tiles[i].k_tile, (int32_t)i, (int32_t)(j - i)});
+      i = j;
+    }
+  }
+  // longest first; ties by ring step then tile, so the order is unique
+  std::stable_sort(out.begin(), out.end(), [&](const hsap_run& a, const hsap_run& b) {
+    if (a.count != b.count) return a.count > b.count;
+    const int32_t sa = step_of(a.chunk), sb = step_of(b.chunk);
+    if (sa != sb) return sa < sb;
+    return a.tile < b.tile;
+  });
+  *num_runs = (int64_t)out.size();
+  if (!runs || (int64_t)out.size() > capacity)
+    HSAP_FAIL(HSAP_ERR_CAPACITY, "run list needs %lld entries, capacity %lld", (long long)out.size(),
+              (long long)capacity);
+  std::copy(out.begin(), out.end(), runs);
+  return HSAP_OK;
+}
+
+}  // extern "C"
