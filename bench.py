@@ -1,0 +1,274 @@
+#!/usr/bin/env python3
+"""Useful document-masked attention TFLOP/s for one sequence-parallel shard on one MI355X.
+
+One step is one pass of the whole path for one packed batch, inputs resident
+in HBM:
+  host planner (tile list and runs, C++) -> async upload -> document starts
+  -> partial attention of the shard against every K/V chunk -> LSE merge
+  (and, for a forward+backward workload, the backward preprocess, partial
+  attention backward and gradient conversion).
+The planner of step i+1 runs on the host while the GPU executes step i.
+
+Default workload: 32768-token packed sequence, log-normal documents, 32
+heads of 128, sequence-parallel degree 8 (contiguous), shard 3, forward.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+  python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload c2]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "useful doc-masked attention TFLOP/s per shard; % of bf16 MFMA peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _critical_shard(L, w):
+    best, best_r = -1, 0
+    for r in range(w.sp_degree):
+        d = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, r, w.block_m, w.block_n)
+        pairs = int(L.plan(w.cu_seqlens, d)["useful_pairs"].sum())
+        if pairs > best:
+            best, best_r = pairs, r
+    return best_r
+
+
+def measure(name: str, steps: int, warmup: int, backward=None):
+    """Time `steps` pipelined steps of one workload; returns a result dict (GPU side only)."""
+    import torch
+    from paper_2606_30460_amd import _lib as L
+    from paper_2606_30460_amd.shard_attention import PlanPipeline, ShardAttention, to_sharded
+    from workloads import make_workload
+
+    w = make_workload(name)
+    bwd = w.backward if backward is None else backward
+    shard = w.shard if w.shard is not None else _critical_shard(L, w)
+    log("[bench] %s: generating inputs (shard %d)" % (w.name, shard))
+    t = w.tensors(backward=bwd)
+    dev = torch.device("cuda")
+    sa = ShardAttention(w.cu_seqlens, w.total_tokens, w.sp_degree, w.layout, shard, w.heads_q, w.heads_kv,
+                        w.head_dim, w.block_m, w.block_n)
+    q = to_sharded(sa.shard, t["q"].to(dev))[shard].contiguous()
+    k = to_sharded(sa.shard, t["k"].to(dev))
+    v = to_sharded(sa.shard, t["v"].to(dev))
+    d_o = to_sharded(sa.shard, t["do"].to(dev))[shard].contiguous() if bwd else None
+    del t
+    pipe = PlanPipeline(sa, backward=bwd)
+    fwd = sa.alloc_forward()
+    bb = sa.alloc_backward() if bwd else None
+    torch.cuda.synchronize()
+
+    events = []
+
+    def one_step():
+        pipe.step()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        e[0].record()
+        L.partial_attn_fwd(sa.desc, q, k, v, sa.doc_start, sa.tiles_q, sa.runs_q, fwd["o_part"], fwd["lse_part"])
+        e[1].record()
+        L.lse_merge([fwd["o_part"][c] for c in sa.present], [fwd["lse_part"][c] for c in sa.present], sa.n, sa.hq,
+                    sa.d, fwd["o"], fwd["lse"])
+        e[2].record()
+        if bwd:
+            for c in sa.present:
+                bb["dk_acc"][c].zero_()
+                bb["dv_acc"][c].zero_()
+            bb["dq_acc"].zero_()
+            L.attn_bwd_preprocess(fwd["o"], d_o, sa.n, sa.hq, sa.d, bb["delta"])
+            e[3].record()
+            L.partial_attn_bwd(sa.desc, q, k, v, d_o, fwd["lse"], bb["delta"], sa.doc_start, sa.tiles_k, sa.runs_k,
+                               bb["dq_acc"], bb["dk_acc"], bb["dv_acc"])
+            e[4].record()
+            L.convert_f32_bf16(bb["dq_acc"], bb["dq"])
+            for c in sa.present:
+                L.convert_f32_bf16(bb["dk_acc"][c], bb["dk"][c])
+                L.convert_f32_bf16(bb["dv_acc"][c], bb["dv"][c])
+        events.append(e)
+
+    for _ in range(warmup):
+        one_step()
+    torch.cuda.synchronize()
+    events.clear()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one_step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    fwd_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
+    merge_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
+    bwd_ms = np.array([e[3].elapsed_time(e[4]) for e in events]) if bwd else None
+
+    # planner host time (not overlapped), for reference
+    t1 = time.perf_counter()
+    reps = 20
+    for _ in range(reps):
+        L.plan(sa.cu_host, sa.shard)
+    plan_ms = (time.perf_counter() - t1) / reps * 1e3
+
+    pairs = sa.total_useful_pairs
+    tiles = int(sa.step_offsets[-1])
+    fwd_flops = 4.0 * w.head_dim * w.heads_q * pairs
+    bwd_flops = 10.0 * w.head_dim * w.heads_q * pairs if bwd else 0.0
+    # merge bytes actually required: every part's LSE row, the O row of parts whose LSE is finite, the outputs
+    lse_present = fwd["lse_part"][sa.present]
+    finite_rows = int(torch.isfinite(lse_present).sum().item())
+    merge_bytes = (len(sa.present) * sa.hq * sa.n * 4 + finite_rows * sa.d * 4 + sa.n * sa.hq * (2 * sa.d + 4))
+    ms_step = wall / steps * 1e3
+    res = {
+        "workload": w.name, "shard": shard, "tokens": w.total_tokens, "sp_degree": w.sp_degree,
+        "layout": w.layout, "heads_q": w.heads_q, "heads_kv": w.heads_kv, "head_dim": w.head_dim,
+        "block_m": w.block_m, "block_n": w.block_n, "backward": bool(bwd), "docs": w.num_docs,
+        "useful_pairs": pairs, "tiles": tiles, "full_tiles": int(np.sum(sa.tiles_q.view(-1, 4)[:, 3].cpu().numpy() == 0)),
+        "tile_efficiency": pairs / float(tiles * w.block_m * w.block_n),
+        "chunks_with_tiles": len(sa.present),
+        "useful_gflop_per_step": (fwd_flops + bwd_flops) / 1e9,
+        "ms_per_step": ms_step,
+        "tflops": (fwd_flops + bwd_flops) / (ms_step * 1e-3) / 1e12,
+        "fwd_kernel_ms_mean": float(fwd_ms.mean()), "fwd_kernel_ms_median": float(np.median(fwd_ms)),
+        "fwd_kernel_ms_min": float(fwd_ms.min()),
+        "fwd_kernel_tflops": fwd_flops / (fwd_ms.mean() * 1e-3) / 1e12,
+        "merge_kernel_ms_mean": float(merge_ms.mean()),
+        "merge_bytes": merge_bytes,
+        "merge_gbs": merge_bytes / (merge_ms.mean() * 1e-3) / 1e9,
+        "planner_host_ms": plan_ms,
+    }
+    if bwd:
+        res.update({"bwd_kernel_ms_mean": float(bwd_ms.mean()), "bwd_kernel_ms_median": float(np.median(bwd_ms)),
+                    "bwd_kernel_tflops": bwd_flops / (bwd_ms.mean() * 1e-3) / 1e12})
+    res["_fwd_flops"] = fwd_flops
+    log("[bench] %s: %.3f ms/step, %.1f TFLOP/s useful (fwd kernel %.3f ms = %.1f TFLOP/s)" % (
+        w.name, ms_step, res["tflops"], res["fwd_kernel_ms_mean"], res["fwd_kernel_tflops"]))
+    del q, k, v, fwd, bb, pipe, sa
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(name: str, budget_s: float):
+    """The fp64 oracle on a bounded sample of the workload's query rows, on the host cores."""
+    import oracle
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from workloads import make_workload
+    from paper_2606_30460_amd import _lib as L
+
+    w = make_workload(name)
+    shard = w.shard if w.shard is not None else _critical_shard(L, w)
+    t = w.tensors(backward=False)
+    q, k, v = (t[x].float().numpy() for x in ("q", "k", "v"))
+    cores = len(os.sched_getaffinity(0))
+    n = w.total_tokens // w.sp_degree
+    pos_all = oracle.shard_positions(w.total_tokens, w.sp_degree, w.layout, shard)
+    starts = oracle.doc_starts(w.cu_seqlens)
+    rng = np.random.default_rng(0)
+    with threadpool_limits(limits=cores):
+        used = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        # double the sample until one oracle run takes at least half the budget
+        count = 64
+        while True:
+            count = min(count, n)
+            rows = np.sort(rng.choice(n, size=count, replace=False))
+            t0 = time.perf_counter()
+            oracle.shard_forward(q, k, v, w.cu_seqlens, w.total_tokens, w.sp_degree, w.layout, shard, rows=rows)
+            el = time.perf_counter() - t0
+            log("[bench] oracle: %d rows in %.1f s" % (count, el))
+            if el >= 0.5 * budget_s or count == n:
+                break
+            count *= 2
+    pos = pos_all[rows]
+    pairs = int(np.sum(pos - starts[pos] + 1))
+    flops = 4.0 * w.head_dim * w.heads_q * pairs
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        cpu_model = platform.processor()
+    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(used), "kind": "oracle",
+            "sample": "%d of %d query rows of shard %d (all %d heads, all %d chunks, merge), fp64 numpy/BLAS, "
+                      "%.1f s, %.2f useful GFLOP" % (count, n, shard, w.heads_q, w.sp_degree, el, flops / 1e9),
+            "cpu": cpu_model, "affinity_cores": cores}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2")
+    ap.add_argument("--extra", default="c3,c4,c5", help="other workloads reported under 'extra' ('' for none)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle budget for the CPU baseline (0: skip)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the sequence-parallel split is simulated in memory on a single "
+              "MI355X; run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    from paper_2606_30460_amd import _lib as L
+    L.lib()
+
+    main_res = measure(args.workload, args.steps, args.warmup)
+    extra = {}
+    for name in [x for x in args.extra.split(",") if x and x != args.workload]:
+        r = measure(name, min(args.steps, 20), min(args.warmup, 3))
+        r.pop("_fwd_flops", None)
+        extra[name] = r
+    cpu = None
+    if args.cpu_seconds > 0:
+        log("[bench] CPU baseline (oracle) on %s, ~%.0f s" % (args.workload, args.cpu_seconds))
+        cpu = cpu_baseline(args.workload, args.cpu_seconds)
+
+    fwd_flops = main_res.pop("_fwd_flops")
+    achieved = fwd_flops / (main_res["fwd_kernel_ms_mean"] * 1e-3) / 1e12
+    line = {
+        "metric": METRIC,
+        "value": round(main_res["tflops"], 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(main_res["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": main_res["workload"], "tokens": main_res["tokens"], "sp_degree": main_res["sp_degree"],
+                   "layout": main_res["layout"], "shard": main_res["shard"], "heads_q": main_res["heads_q"],
+                   "heads_kv": main_res["heads_kv"], "head_dim": main_res["head_dim"],
+                   "block_m": main_res["block_m"], "block_n": main_res["block_n"], "pass": "forward"
+                   if not main_res["backward"] else "forward+backward"},
+        "pct_of_bf16_peak": round(100.0 * main_res["tflops"] / PEAK_BF16_TFLOPS, 3),
+        "roofline": {"bound": "mfma", "kernel": "attn_fwd_kernel", "achieved": round(achieved, 3),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
+                     "traffic": None},
+        "cpu_baseline": cpu,
+        "detail": main_res,
+        "extra": extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -185,6 +185,26 @@ def plan_runs(shard: ShardDesc, tiles: np.ndarray, major: int) -> Tuple[np.ndarr
     return sorted_tiles[: len(tiles)], runs[: num.value]
 
 
+def plan_into(cu_seqlens: np.ndarray, shard: ShardDesc, tiles_out: np.ndarray, step_offsets_out: np.ndarray,
+              useful_pairs_out: np.ndarray) -> int:
+    """hsap_plan into caller-provided host buffers (e.g. views of pinned memory).
+
+    ``tiles_out`` int32 [capacity, 4]; returns the tile count."""
+    num = ctypes.c_int64(0)
+    _check(lib().hsap_plan(_ptr(cu_seqlens), len(cu_seqlens) - 1, ctypes.byref(shard), _ptr(tiles_out),
+                           tiles_out.shape[0], ctypes.byref(num), _ptr(step_offsets_out), _ptr(useful_pairs_out)))
+    return num.value
+
+
+def plan_runs_into(shard: ShardDesc, tiles: np.ndarray, num_tiles: int, major: int, sorted_out: np.ndarray,
+                   runs_out: np.ndarray) -> int:
+    """hsap_plan_runs into caller-provided host buffers; returns the run count."""
+    num = ctypes.c_int64(0)
+    _check(lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), int(num_tiles), int(major), _ptr(sorted_out),
+                                _ptr(runs_out), runs_out.shape[0], ctypes.byref(num)))
+    return num.value
+
+
 # ---------------------------------------------------------------------------
 # device entry points
 # ---------------------------------------------------------------------------
