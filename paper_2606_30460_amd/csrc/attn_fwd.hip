@@ -4,18 +4,26 @@
 //
 // Work decomposition: one workgroup per (run, query head).  A run is one
 // (chunk, q-tile) with its listed k-tiles.  The workgroup has WAVES waves;
-// wave w owns 32 query rows, so BM = 32 * WAVES.
+// wave w owns 32 query rows, so BM = 32 * WAVES.  Every listed k-tile of BN
+// keys is consumed in steps of KB = 64 keys.
 //
-// Per k-tile: K rows are staged in LDS as [key][d] and V as its transpose
-// [d][key]; the wave computes the scores transposed, S^T = K Q^T, with Q held
-// in registers as the MFMA B operand.  In that orientation a lane holds one
-// query (its column) and 16 keys per 32-key block, so the row max and row sum
-// of the online softmax need only the lane itself and lane l ^ 32.  P (bf16)
-// then feeds O^T += V^T P^T as the B operand straight from registers: the
-// register order of the score block is the key order both MFMA operands use.
+// Per step the workgroup stages the step's K and V rows in LDS, both in their
+// natural [key][d] layout with 16-byte stores, and each wave computes the
+// scores transposed, S^T = K Q^T, with Q held in registers as the MFMA B
+// operand.  In that orientation a lane holds one query (its column) and 16
+// keys per 32-key block, so the row max and row sum of the online softmax
+// need only the lane and lane l ^ 32 (one permlane32 swap).  P (bf16) then
+// feeds O^T += V^T P^T as the B operand straight from registers; the V^T
+// operand is read from the [key][d] tile with the LDS transpose read, whose
+// per-lane key order matches the register order of the score block.
+//
+// Pipelining: two LDS buffers.  While a step computes on one buffer, the next
+// step's K/V rows are already loading into registers; they are written to the
+// other buffer after the compute, and one barrier per step orders the two.
 // Scores are scaled by softmax_scale * log2(e) so the exponentials are exp2.
 // FULL tiles skip all mask arithmetic; MASKED tiles compare each key position
-// with the query's document start and position.
+// with the query's document start and position.  O is rescaled only when
+// some row of the wave raised its running max.
 #include "hsap_internal.h"
 #include "mfma.h"
 
@@ -39,14 +47,18 @@ struct FwdArgs {
 };
 
 template <int D, int BN, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void attn_fwd_kernel(FwdArgs a) {
-  constexpr int BM = 32 * WAVES;
+__global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
+  constexpr int KB = 64;                     // keys per step
+  constexpr int SUBS = BN / KB;              // steps per listed k-tile
   constexpr int NT = 64 * WAVES;
-  constexpr int KS = D + 8;   // LDS row stride of K (bf16), padded against bank conflicts
-  constexpr int VS = BN + 8;  // LDS row stride of V^T
+  constexpr int KS = D + 8;                  // K row stride (bf16): 16-lane b128 reads hit distinct banks
+  constexpr int VS = D + 16;                 // V row stride (bf16): 4-row transpose reads hit distinct banks
+  constexpr int CHUNKS = KB * D / 8;         // 16-byte chunks per K (or V) step
+  constexpr int PER_T = CHUNKS / NT;         // chunks per thread
+  static_assert(CHUNKS % NT == 0, "step must split evenly over the threads");
   constexpr float NEG_INF = -__builtin_inff();
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[BN * KS];
-  __shared__ __attribute__((aligned(16))) __bf16 Vt[D * VS];
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[2][KB * KS];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[2][KB * VS];
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
@@ -56,116 +68,147 @@ __global__ __launch_bounds__(64 * WAVES) void attn_fwd_kernel(FwdArgs a) {
   const int c = run.chunk;
   const int g = h / a.group;
   const int64_t n = a.geom.n;
+  const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;  // this lane's query row (shard-local)
 
-  const int64_t qrow = (int64_t)run.tile * BM + 32 * w + l32;  // shard-local query row of this lane
+  if (run.count == 0) {  // no key of chunk c for this q-tile
+    if (hi == 0) a.lse_part[((int64_t)c * a.hq + h) * n + qrow] = NEG_INF;
+    return;
+  }
+
   const int64_t gq = global_pos(a.geom, a.shard, qrow);
+  const int64_t qstart = a.doc_start[gq];
+  bf16x8 qf[D / 16];
+  {
+    const __bf16* qp = a.q + (qrow * a.hq + h) * D + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
+  }
+  const int64_t rstride = (int64_t)a.hkv * D;
+  const __bf16* kbase = a.k + ((int64_t)c * n * a.hkv + g) * D;
+  const __bf16* vbase = a.v + ((int64_t)c * n * a.hkv + g) * D;
+  const int total = run.count * SUBS;
+
+  // staging: thread t moves chunks t, t + NT, ... of the step's [KB][D] tiles
+  bf16x8 kreg[PER_T], vreg[PER_T];
+  auto load_step = [&](int s) {
+    const hsap_tile tile = a.tiles[run.first + s / SUBS];
+    const int64_t row0 = (int64_t)tile.k_tile * BN + (s % SUBS) * KB;
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int idx = tid + i * NT, row = idx / (D / 8), cc = idx % (D / 8);
+      const int64_t off = (row0 + row) * rstride + cc * 8;
+      kreg[i] = *(const bf16x8*)(kbase + off);
+      vreg[i] = *(const bf16x8*)(vbase + off);
+    }
+  };
+  auto store_step = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      const int idx = tid + i * NT, row = idx / (D / 8), cc = idx % (D / 8);
+      *(bf16x8*)(&Ks[buf][row * KS + cc * 8]) = kreg[i];
+      *(bf16x8*)(&Vs[buf][row * VS + cc * 8]) = vreg[i];
+    }
+  };
+
+  // transpose-read geometry for the V^T operand (see mfma.h): lane j of each
+  // 16-lane group points at 4 consecutive d of key row (j / 4) of its group
+  const int tr_row = 4 * hi + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
   float m_run = NEG_INF, l_run = 0.f;
   f32x16 o[D / 32];
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
 
-  if (run.count > 0) {
-    bf16x8 qf[D / 16];
-    const __bf16* qp = a.q + (qrow * a.hq + h) * D + 8 * hi;
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
-    const int64_t qstart = a.doc_start[gq];
-    const int64_t rstride = (int64_t)a.hkv * D;
+  load_step(0);
+  store_step(0);
+  __syncthreads();
 
-    for (int it = 0; it < run.count; ++it) {
-      const hsap_tile tile = a.tiles[run.first + it];
-      const int64_t krow0 = (int64_t)tile.k_tile * BN;
-      const int64_t gk0 = global_pos(a.geom, c, krow0);
-      const int64_t off = (((int64_t)c * n + krow0) * a.hkv + g) * D;
-      const __bf16* kb = a.k + off;
-      const __bf16* vb = a.v + off;
+  for (int s = 0; s < total; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < total) load_step(s + 1);
+    const hsap_tile tile = a.tiles[run.first + s / SUBS];
+    const __bf16* K = Ks[buf];
+    const __bf16* V = Vs[buf];
 
-      __syncthreads();  // the previous tile's LDS reads are done
+    // S^T = K Q^T for 2 blocks of 32 keys
+    f32x16 sc[KB / 32];
 #pragma unroll
-      for (int i = tid; i < BN * D / 8; i += NT) {
-        const int row = i / (D / 8), cc = i % (D / 8);
-        const bf16x8 kv = *(const bf16x8*)(kb + row * rstride + cc * 8);
-        const bf16x8 vv = *(const bf16x8*)(vb + row * rstride + cc * 8);
-        *(bf16x8*)(Ks + row * KS + cc * 8) = kv;
+    for (int nb = 0; nb < KB / 32; ++nb) {
+      sc[nb] = f32x16{};
 #pragma unroll
-        for (int e = 0; e < 8; ++e) Vt[(cc * 8 + e) * VS + row] = vv[e];
+      for (int kk = 0; kk < D / 16; ++kk) {
+        const bf16x8 af = *(const bf16x8*)(K + (32 * nb + l32) * KS + 16 * kk + 8 * hi);
+        sc[nb] = mfma32(af, qf[kk], sc[nb]);
       }
-      __syncthreads();
-
-      // S^T = K Q^T, 32 keys per block
-      f32x16 s[BN / 32];
+    }
+    if (tile.kind == HSAP_TILE_MASKED) {
+      const int64_t gk0 = global_pos(a.geom, c, (int64_t)tile.k_tile * BN) + (s % SUBS) * KB;
 #pragma unroll
-      for (int nb = 0; nb < BN / 32; ++nb) {
-        s[nb] = f32x16{};
-#pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          const bf16x8 af = *(const bf16x8*)(Ks + (32 * nb + l32) * KS + 16 * kk + 8 * hi);
-          s[nb] = mfma32(af, qf[kk], s[nb]);
-        }
-      }
-      if (tile.kind == HSAP_TILE_MASKED) {
-#pragma unroll
-        for (int nb = 0; nb < BN / 32; ++nb)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int64_t gk = gk0 + 32 * nb + c_row(j, hi);
-            if (gk < qstart || gk > gq) s[nb][j] = NEG_INF;
-          }
-      }
-      // online softmax over this tile's keys (row = this lane's query)
-      float mx = NEG_INF;
-#pragma unroll
-      for (int nb = 0; nb < BN / 32; ++nb)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[nb][j]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx * a.scale_log2);
-      const float m_use = m_new == NEG_INF ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run - m_use);
-      float rs = 0.f;
-#pragma unroll
-      for (int nb = 0; nb < BN / 32; ++nb)
+      for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const float p = fast_exp2(s[nb][j] * a.scale_log2 - m_use);
-          s[nb][j] = p;
-          rs += p;
-        }
-      rs += __shfl_xor(rs, 32);
-      l_run = l_run * alpha + rs;
-      m_run = m_new;
-#pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
-
-      // O^T += V^T P^T: 16 keys per MFMA
-#pragma unroll
-      for (int nb = 0; nb < BN / 32; ++nb)
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          bf16x8 pb;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pb[e] = (__bf16)s[nb][8 * half + e];
-#pragma unroll
-          for (int mb = 0; mb < D / 32; ++mb) {
-            const __bf16* vr = Vt + (32 * mb + l32) * VS + 32 * nb + 16 * half + 4 * hi;
-            const bf16x8 av = cat4(*(const bf16x4*)vr, *(const bf16x4*)(vr + 8));
-            o[mb] = mfma32(av, pb, o[mb]);
-          }
+          const int64_t gk = gk0 + 32 * nb + c_row(j, hi);
+          if (gk < qstart || gk > gq) sc[nb][j] = NEG_INF;
         }
     }
-
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    float* op = a.o_part + (((int64_t)c * n + qrow) * a.hq + h) * D + 4 * hi;
+    // online softmax (this lane's row = its query)
+    float mx = sc[0][0];
 #pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb)
+    for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
-      for (int grp = 0; grp < 4; ++grp) {
-        const f32x4 val{o[mb][4 * grp] * inv, o[mb][4 * grp + 1] * inv, o[mb][4 * grp + 2] * inv,
-                        o[mb][4 * grp + 3] * inv};
-        *(f32x4*)(op + 32 * mb + 8 * grp) = val;
+      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
+    mx = pair_max(mx);
+    const float m_new = fmaxf(m_run, mx * a.scale_log2);
+    const float m_use = m_new == NEG_INF ? 0.f : m_new;
+    if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {  // some row's max moved: rescale
+      const float alpha = fast_exp2(m_run - m_use);
+      l_run *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+      m_run = m_new;
+    }
+    float rs = 0.f;
+    bf16x8 pb[KB / 32][2];
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const float p = fast_exp2(__builtin_fmaf(sc[nb][j], a.scale_log2, -m_use));
+        rs += p;
+        pb[nb][j >> 3][j & 7] = (__bf16)p;
       }
+    l_run += rs;  // the half-row sums of lanes l and l ^ 32 are combined once, at the end
+
+    // O^T += V^T P^T, 16 keys per MFMA
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int r0 = 32 * nb + 16 * half + tr_row;
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb) {
+          const __bf16* vp = V + r0 * VS + 32 * mb + tr_col;
+          const bf16x8 av = cat4(ds_read_tr16(vp), ds_read_tr16(vp + 8 * VS));
+          o[mb] = mfma32(av, pb[nb][half], o[mb]);
+        }
+      }
+
+    if (s + 1 < total) store_step(buf ^ 1);
+    __syncthreads();
   }
+
+  l_run = pair_sum(l_run);
+  const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+  float* op = a.o_part + (((int64_t)c * n + qrow) * a.hq + h) * D + 4 * hi;
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp) {
+      const f32x4 val{o[mb][4 * grp] * inv, o[mb][4 * grp + 1] * inv, o[mb][4 * grp + 2] * inv,
+                      o[mb][4 * grp + 3] * inv};
+      *(f32x4*)(op + 32 * mb + 8 * grp) = val;
+    }
   if (hi == 0)
     a.lse_part[((int64_t)c * a.hq + h) * n + qrow] =
         l_run > 0.f ? (m_run + __log2f(l_run)) * 0.69314718055994530942f : NEG_INF;

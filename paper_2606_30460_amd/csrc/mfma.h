@@ -31,4 +31,28 @@ __device__ __forceinline__ bf16x8 cat4(const bf16x4& a, const bf16x4& b) {
   return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }
 
+// v_permlane32_swap with both operands x: lane l < 32 receives (x[l], x[l+32]),
+// lane l >= 32 receives (x[l-32], x[l]).  So the pair holds x[l] and x[l ^ 32]
+// in every lane, without an LDS round trip.
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane j supplies the LDS
+// address of four consecutive 16-bit values c_j[0..3]; lane i receives
+// c_{i/4 + 4k}[i % 4] for k = 0..3.  If lane j points at row (j / 4) of a
+// 4-row block, columns 4 * (j % 4) .. +3, lane i gets column i of the four
+// rows: a 4 x 16 tile read transposed.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+__device__ __forceinline__ bf16x4 ds_read_tr16(const __bf16* lds_ptr) {
+  const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds_ptr));
+  return __builtin_bit_cast(bf16x4, r);
+}
+
 }  // namespace hsap
