@@ -23,7 +23,7 @@
 // Scores are scaled by softmax_scale * log2(e) so the exponentials are exp2.
 // FULL tiles skip all mask arithmetic; MASKED tiles compare each key position
 // with the query's document start and position.  O is rescaled only when
-// some row of the wave raised its running max.
+// some row of the wave raised its running max by more than a fixed slack.
 #include "hsap_internal.h"
 #include "mfma.h"
 
@@ -51,18 +51,19 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int KB = 64;                     // keys per step
   constexpr int SUBS = BN / KB;              // steps per listed k-tile
   constexpr int NT = 64 * WAVES;
-  constexpr int KS = D + 8;                  // K row stride (bf16): 16-lane b128 reads hit distinct banks
-  constexpr int VS = D + 16;                 // V row stride (bf16): 4-row transpose reads hit distinct banks
+  constexpr int KS = D + 8;                  // K row stride (bf16): 68 dwords, rows of a 16-lane b128 read hit distinct banks
+  constexpr int VS = D + 32;                 // V row stride (bf16): 16 (mod 64) dwords, 32 lanes of a transpose read hit distinct banks
   constexpr int CHUNKS = KB * D / 8;         // 16-byte chunks per K (or V) step
   constexpr int PER_T = CHUNKS / NT;         // chunks per thread
   static_assert(CHUNKS % NT == 0, "step must split evenly over the threads");
   constexpr float NEG_INF = -__builtin_inff();
+  constexpr float RESCALE_SLACK = 8.f;       // log2 units a row max may rise before O is rescaled
   __shared__ __attribute__((aligned(16))) __bf16 Ks[2][KB * KS];
   __shared__ __attribute__((aligned(16))) __bf16 Vs[2][KB * VS];
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
-  const int run_idx = blockIdx.x / a.hq;
+  const int run_idx = blockIdx.x / a.hq;  // runs are longest first: long work starts first
   const int h = blockIdx.x - run_idx * a.hq;
   const hsap_run run = a.runs[run_idx];
   const int c = run.chunk;
@@ -75,8 +76,9 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     return;
   }
 
-  const int64_t gq = global_pos(a.geom, a.shard, qrow);
-  const int64_t qstart = a.doc_start[gq];
+  const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
+  const int32_t qstart = a.doc_start[gq];
+  const uint32_t span = (uint32_t)(gq - qstart);  // key j is allowed iff 0 <= j - start <= span
   bf16x8 qf[D / 16];
   {
     const __bf16* qp = a.q + (qrow * a.hq + h) * D + 8 * hi;
@@ -89,26 +91,32 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   const int total = run.count * SUBS;
 
   // staging: thread t moves chunks t, t + NT, ... of the step's [KB][D] tiles
+  int32_t goff[PER_T], koff[PER_T], voff[PER_T];
+#pragma unroll
+  for (int i = 0; i < PER_T; ++i) {
+    const int idx = tid + i * NT, row = idx / (D / 8), cc = idx % (D / 8);
+    goff[i] = (int32_t)(row * rstride + cc * 8);
+    koff[i] = row * KS + cc * 8;
+    voff[i] = row * VS + cc * 8;
+  }
   bf16x8 kreg[PER_T], vreg[PER_T];
-  auto load_step = [&](int s) {
-    const hsap_tile tile = a.tiles[run.first + s / SUBS];
-    const int64_t row0 = (int64_t)tile.k_tile * BN + (s % SUBS) * KB;
+  auto load_step = [&](int64_t row0) {
+    const __bf16* kb = kbase + row0 * rstride;
+    const __bf16* vb = vbase + row0 * rstride;
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
-      const int idx = tid + i * NT, row = idx / (D / 8), cc = idx % (D / 8);
-      const int64_t off = (row0 + row) * rstride + cc * 8;
-      kreg[i] = *(const bf16x8*)(kbase + off);
-      vreg[i] = *(const bf16x8*)(vbase + off);
+      kreg[i] = *(const bf16x8*)(kb + goff[i]);
+      vreg[i] = *(const bf16x8*)(vb + goff[i]);
     }
   };
   auto store_step = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
-      const int idx = tid + i * NT, row = idx / (D / 8), cc = idx % (D / 8);
-      *(bf16x8*)(&Ks[buf][row * KS + cc * 8]) = kreg[i];
-      *(bf16x8*)(&Vs[buf][row * VS + cc * 8]) = vreg[i];
+      *(bf16x8*)(&Ks[buf][koff[i]]) = kreg[i];
+      *(bf16x8*)(&Vs[buf][voff[i]]) = vreg[i];
     }
   };
+  auto step_row0 = [&](const hsap_tile& t, int s) { return (int64_t)t.k_tile * BN + (s % SUBS) * KB; };
 
   // transpose-read geometry for the V^T operand (see mfma.h): lane j of each
   // 16-lane group points at 4 consecutive d of key row (j / 4) of its group
@@ -120,14 +128,24 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
 
-  load_step(0);
+  hsap_tile cur = a.tiles[run.first];
+  load_step(step_row0(cur, 0));
   store_step(0);
+  hsap_tile nxt = cur;
+  if (run.count > 1) nxt = a.tiles[run.first + 1];
   __syncthreads();
 
   for (int s = 0; s < total; ++s) {
     const int buf = s & 1;
-    if (s + 1 < total) load_step(s + 1);
-    const hsap_tile tile = a.tiles[run.first + s / SUBS];
+    const hsap_tile tile = cur;
+    if (s + 1 < total) {
+      // descriptor of step s + 1, then of the tile after it (loaded a step ahead)
+      if ((s + 1) % SUBS == 0) {
+        cur = nxt;
+        if ((s + 1) / SUBS + 1 < run.count) nxt = a.tiles[run.first + (s + 1) / SUBS + 1];
+      }
+      load_step(step_row0(cur, s + 1));
+    }
     const __bf16* K = Ks[buf];
     const __bf16* V = Vs[buf];
 
@@ -135,39 +153,39 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     f32x16 sc[KB / 32];
 #pragma unroll
     for (int nb = 0; nb < KB / 32; ++nb) {
+      bf16x8 kf[D / 16];
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(K + (32 * nb + l32) * KS + 16 * kk + 8 * hi);
       sc[nb] = f32x16{};
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 af = *(const bf16x8*)(K + (32 * nb + l32) * KS + 16 * kk + 8 * hi);
-        sc[nb] = mfma32(af, qf[kk], sc[nb]);
-      }
+      for (int kk = 0; kk < D / 16; ++kk) sc[nb] = mfma32(kf[kk], qf[kk], sc[nb]);
     }
     if (tile.kind == HSAP_TILE_MASKED) {
-      const int64_t gk0 = global_pos(a.geom, c, (int64_t)tile.k_tile * BN) + (s % SUBS) * KB;
+      const int32_t rel0 = (int32_t)global_pos(a.geom, c, step_row0(tile, s)) - qstart;
 #pragma unroll
       for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int64_t gk = gk0 + 32 * nb + c_row(j, hi);
-          if (gk < qstart || gk > gq) sc[nb][j] = NEG_INF;
-        }
+        for (int j = 0; j < 16; ++j)
+          if ((uint32_t)(rel0 + 32 * nb + c_row(j, hi)) > span) sc[nb][j] = NEG_INF;
     }
-    // online softmax (this lane's row = its query)
+    // online softmax (this lane's row = its query; lanes l and l ^ 32 share it)
     float mx = sc[0][0];
 #pragma unroll
     for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
-    mx = pair_max(mx);
-    const float m_new = fmaxf(m_run, mx * a.scale_log2);
-    const float m_use = m_new == NEG_INF ? 0.f : m_new;
-    if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {  // some row's max moved: rescale
-      const float alpha = fast_exp2(m_run - m_use);
+    const float m_new = fmaxf(m_run, pair_max(mx) * a.scale_log2);
+    // The reference max only has to bound the scores loosely: O / l and
+    // m + log2(l) do not depend on it.  Rescale only when some row's max rose
+    // by more than RESCALE_SLACK (p then stays below 2^RESCALE_SLACK).
+    if (__builtin_amdgcn_ballot_w64(m_new > m_run + RESCALE_SLACK) != 0) {
+      const float alpha = fast_exp2(m_run - (m_new == NEG_INF ? 0.f : m_new));
       l_run *= alpha;
 #pragma unroll
       for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
       m_run = m_new;
     }
+    const float m_use = m_run == NEG_INF ? 0.f : m_run;
     float rs = 0.f;
     bf16x8 pb[KB / 32][2];
 #pragma unroll
@@ -242,6 +260,7 @@ extern "C" hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const v
   if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o_part) & 15)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k, v and o_part must be 16-byte aligned");
   const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
+  if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
   FwdArgs a;
   a.q = (const __bf16*)q;
   a.k = (const __bf16*)k;
