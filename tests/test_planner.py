@@ -1,0 +1,116 @@
+"""The C++ host planner (through the C ABI) against the oracle's tile classification, bit for bit.
+
+The oracle classifies tiles by counting allowed pairs row by row (itself pinned
+to brute-force pair classification); the library plans by interval
+arithmetic.  Lists, ring-step offsets and per-step pair counts must be equal.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle.plan import plan_shard, tile_pair_counts_bruteforce
+from paper_2606_30460_amd import _lib as L
+from workloads import make_workload
+
+
+def _compare(cu, N, P, layout, r, bm, bn, counter=None):
+    ref = plan_shard(cu, N, P, layout, r, bm, bn, **({"counter": counter} if counter else {}))
+    got = L.plan(cu, L.shard_desc(N, P, layout, r, bm, bn))
+    assert np.array_equal(got["tiles"], ref["tiles"])
+    assert np.array_equal(got["step_offsets"], ref["step_offsets"])
+    assert np.array_equal(got["useful_pairs"], ref["useful_pairs"])
+    return got
+
+
+def _rand_cu(rng, N):
+    ncut = int(rng.integers(0, max(2, N // 8)))
+    cuts = rng.integers(0, N + 1, size=ncut)
+    return np.sort(np.concatenate([[0, N], cuts])).astype(np.int32)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_against_bruteforce(seed):
+    rng = np.random.default_rng(1000 + seed)
+    P = int(rng.choice([1, 2, 4, 8, 16]))
+    layout = str(rng.choice(["contiguous", "zigzag"]))
+    bm, bn = int(rng.choice([16, 32, 64, 128])), int(rng.choice([16, 32, 64, 128]))
+    split = 2 * P if layout == "zigzag" else P
+    N = split * max(bm, bn) * int(rng.integers(1, 3))
+    if N > 4096:
+        N = split * max(bm, bn)
+    cu = _rand_cu(rng, N)
+    r = int(rng.integers(0, P))
+    _compare(cu, N, P, layout, r, bm, bn, counter=tile_pair_counts_bruteforce if N <= 1024 else None)
+
+
+EDGE = [
+    # one-token documents everywhere
+    (256, 4, "contiguous", 16, 16, np.arange(0, 257)),
+    # zero-length documents
+    (256, 2, "zigzag", 32, 32, [0, 0, 0, 64, 64, 200, 256, 256]),
+    # documents exactly equal to tiles
+    (512, 4, "contiguous", 32, 32, np.arange(0, 513, 32)),
+    # one document crossing every chunk
+    (1024, 8, "zigzag", 64, 64, [0, 1024]),
+    (1024, 8, "contiguous", 64, 16, [0, 1024]),
+]
+
+
+@pytest.mark.parametrize("case", EDGE)
+def test_edge_cases(case):
+    N, P, layout, bm, bn, cu = case
+    for r in range(P):
+        _compare(np.asarray(cu, dtype=np.int32), N, P, layout, r, bm, bn)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c5m"])
+def test_workload_plans(name):
+    w = make_workload(name)
+    shards = [w.shard] if w.shard is not None else range(w.sp_degree)
+    pairs = []
+    for r in shards:
+        got = _compare(w.cu_seqlens, w.total_tokens, w.sp_degree, w.layout, r, w.block_m, w.block_n)
+        pairs.append(int(got["useful_pairs"].sum()))
+    if w.shard is None:
+        # the critical shard is the argmax of useful pairs (ties: lowest id), same as the oracle's count
+        ref = oracle.useful_pairs_all_shards(w.cu_seqlens, w.total_tokens, w.sp_degree, w.layout)
+        assert pairs == ref.tolist()
+
+
+def test_pair_identity_all_shards():
+    # sum over shards and chunks of the planner's pair counts = sum_docs L(L+1)/2
+    w = make_workload("c4")
+    lengths = np.diff(w.cu_seqlens.astype(np.int64))
+    total = sum(int(L.plan(w.cu_seqlens, L.shard_desc(w.total_tokens, w.sp_degree, w.layout, r, 128, 128))
+                    ["useful_pairs"].sum()) for r in range(w.sp_degree))
+    assert total == int(np.sum(lengths * (lengths + 1) // 2))
+
+
+def _runs_ok(shard, tiles, sorted_tiles, runs, major):
+    nq = shard.total_tokens // shard.sp_degree // shard.block_m
+    covered = np.zeros(len(tiles), dtype=int)
+    for ch, t, first, count in runs:
+        seg = sorted_tiles[first:first + count]
+        assert np.all(seg[:, 0] == ch)
+        assert np.all(seg[:, 1 if major == L.MAJOR_Q else 2] == t)
+        covered[first:first + count] += 1
+    assert np.all(covered == 1)
+    counts = runs[:, 3]
+    assert np.all(np.diff(counts) <= 0)           # longest first
+    # sorted_tiles is a permutation of tiles
+    key = lambda a: sorted(map(tuple, a.tolist()))
+    assert key(sorted_tiles) == key(tiles)
+    if major == L.MAJOR_Q:
+        present = sorted(set(tiles[:, 0].tolist()))
+        assert len(runs) == len(present) * nq       # every q-tile of every chunk with tiles
+
+
+@pytest.mark.parametrize("name", ["c2", "c3", "c5m"])
+def test_runs(name):
+    w = make_workload(name)
+    r = w.shard if w.shard is not None else 1
+    d = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, r, w.block_m, w.block_n)
+    tiles = L.plan(w.cu_seqlens, d)["tiles"]
+    for major in (L.MAJOR_Q, L.MAJOR_K):
+        sorted_tiles, runs = L.plan_runs(d, tiles, major)
+        _runs_ok(d, tiles, sorted_tiles, runs, major)
