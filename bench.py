@@ -93,7 +93,7 @@ def measure(name: str, steps: int, warmup: int, backward=None):
             L.attn_bwd_preprocess(fwd["o"], d_o, sa.n, sa.hq, sa.d, bb["delta"])
             e[3].record()
             L.partial_attn_bwd(sa.desc, q, k, v, d_o, fwd["lse"], bb["delta"], sa.doc_start, sa.tiles_k, sa.runs_k,
-                               bb["dq_acc"], bb["dk_acc"], bb["dv_acc"])
+                               sa.tiles_q, sa.runs_q, bb["dq_acc"], bb["dk_acc"], bb["dv_acc"])
             e[4].record()
             L.convert_f32_bf16(bb["dq_acc"], bb["dq"])
             for c in sa.present:

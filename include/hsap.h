@@ -234,31 +234,35 @@ hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, 
                                      int32_t head_dim, float* delta, void* hip_stream);
 
 /*
- * hsap_partial_attn_bwd -- "computing" for the backward: for every run
- * (chunk c, k_tile u) and its listed q-tiles, recompute P = exp(s - LSE) from
- * the final LSE and accumulate
+ * hsap_partial_attn_bwd -- "computing" for the backward: the gradients of the
+ * forward above with P = exp(s - LSE) recomputed from the final LSE:
  *   dV_c += P^T dO,  dS = P o (dO V_c^T - delta),
  *   dQ   += scale dS K_c,  dK_c += scale dS^T Q,
- * with dK/dV summed over the query heads of each K/V head.
+ * with dK/dV summed over the query heads of each K/V head.  Two kernels run
+ * on the stream: one over the k-major runs (dK, dV) and one over the q-major
+ * runs (dQ); either list may be empty (count 0) to skip its kernel.
  *
- *   desc, q, k, v, doc_start  as for the forward.  Supported: d = 128 with
- *              BN in {64, 128}, or d = 64 with BN = 64; BM a multiple of 64.
+ *   desc, q, k, v, doc_start  as for the forward.  Supported: BM in
+ *              {64, 128}; d = 128 with BN in {64, 128}, or d = 64 with BN = 64.
  *   d_o        device bf16 [n, Hq, d] (shard r, local rows).
  *   lse        device fp32 [Hq, n]: the merged forward LSE.
  *   delta      device fp32 [Hq, n] from hsap_attn_bwd_preprocess.
- *   tiles      device: sorted_tiles of hsap_plan_runs(MAJOR_K).
- *   runs       device hsap_run [num_runs] from hsap_plan_runs(MAJOR_K).
- *   dq_acc     device fp32 [n, Hq, d], accumulated with atomic adds (+=).
+ *   tiles_k, runs_k, num_runs_k  device lists from hsap_plan_runs(MAJOR_K).
+ *   tiles_q, runs_q, num_runs_q  device lists from hsap_plan_runs(MAJOR_Q)
+ *              (the forward's lists).
+ *   dq_acc     device fp32 [n, Hq, d] (+=).  Each q-major run adds its
+ *              chunk's contribution with one fp32 atomic add per element.
  *   dk_acc, dv_acc  device fp32 [P, n, Hkv, d] sharded order (+=).  Each
- *              (chunk, k_tile) row block is owned by one workgroup, so these
- *              are plain read-modify-write.
+ *              (chunk, k_tile, K/V head) row block is owned by one
+ *              workgroup: plain read-modify-write.
  *   The caller zeroes the accumulators once; concurrent calls on the same
  *   accumulators race.
  */
 hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, const void* k,
                                   const void* v, const void* d_o, const float* lse,
                                   const float* delta, const int32_t* doc_start,
-                                  const hsap_tile* tiles, const hsap_run* runs, int64_t num_runs,
+                                  const hsap_tile* tiles_k, const hsap_run* runs_k, int64_t num_runs_k,
+                                  const hsap_tile* tiles_q, const hsap_run* runs_q, int64_t num_runs_q,
                                   float* dq_acc, float* dk_acc, float* dv_acc, void* hip_stream);
 
 /*

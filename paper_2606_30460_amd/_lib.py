@@ -70,7 +70,8 @@ _SIG = {
     "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
     "hsap_lse_merge": (ctypes.c_int, [_I32, _P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
-    "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P, _P]),
+    "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P,
+                                             _P]),
     "hsap_convert_f32_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
 }
 
@@ -269,8 +270,9 @@ def attn_bwd_preprocess(o, d_o, n: int, heads_q: int, head_dim: int, delta, stre
                                           _stream(stream)))
 
 
-def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_dev, runs_dev, dq_acc, dk_acc,
-                     dv_acc, stream=None) -> None:
+def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_k_dev, runs_k_dev, tiles_q_dev,
+                     runs_q_dev, dq_acc, dk_acc, dv_acc, stream=None) -> None:
+    """hsap_partial_attn_bwd.  Either run list may be None to skip its kernel."""
     s = desc.shard
     n = s.total_tokens // s.sp_degree
     hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
@@ -281,15 +283,18 @@ def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, ti
     _dev(lse, "float32", "lse", hq * n)
     _dev(delta, "float32", "delta", hq * n)
     _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
-    _dev(tiles_dev, "int32", "tiles")
-    _dev(runs_dev, "int32", "runs")
+    for t, name in ((tiles_k_dev, "tiles_k"), (runs_k_dev, "runs_k"), (tiles_q_dev, "tiles_q"), (runs_q_dev, "runs_q")):
+        if t is not None:
+            _dev(t, "int32", name)
     _dev(dq_acc, "float32", "dq_acc", n * hq * d)
     _dev(dk_acc, "float32", "dk_acc", P * n * hkv * d)
     _dev(dv_acc, "float32", "dv_acc", P * n * hkv * d)
+    nk = runs_k_dev.numel() // 4 if runs_k_dev is not None else 0
+    nq = runs_q_dev.numel() // 4 if runs_q_dev is not None else 0
     _check(lib().hsap_partial_attn_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(d_o), _ptr(lse),
-                                       _ptr(delta), _ptr(doc_start_dev), _ptr(tiles_dev), _ptr(runs_dev),
-                                       runs_dev.numel() // 4, _ptr(dq_acc), _ptr(dk_acc), _ptr(dv_acc),
-                                       _stream(stream)))
+                                       _ptr(delta), _ptr(doc_start_dev), _ptr(tiles_k_dev), _ptr(runs_k_dev), nk,
+                                       _ptr(tiles_q_dev), _ptr(runs_q_dev), nq, _ptr(dq_acc), _ptr(dk_acc),
+                                       _ptr(dv_acc), _stream(stream)))
 
 
 def convert_f32_bf16(src, dst, stream=None) -> None:

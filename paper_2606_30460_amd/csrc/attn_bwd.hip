@@ -1,20 +1,25 @@
 // Partial attention backward: gradients of one shard's attention with
 // respect to its queries and to the listed k-tiles of each K/V chunk (the
 // backward "computing" whose results the paper's per-rank code returns as dq
-// and dkv messages, instruction table of the SAP section).
+// and dkv messages, instruction table of the SAP section).  P is recomputed
+// from the final (merged) LSE, so no attention matrix is stored between
+// forward and backward.  Two kernels share the work, so that neither needs
+// atomics per k-tile:
 //
-// Work decomposition: one workgroup per (run, K/V head).  A run is one
+// dK/dV kernel: one workgroup per (k-major run, K/V head).  A run is one
 // (chunk, k-tile) with the q-tiles listed against it.  The workgroup has
 // WAVES waves; wave w owns 32 keys (BN = 32 * WAVES) and keeps their K and V
-// rows in registers and their dK, dV accumulators in registers for the whole
-// run, looping over the query heads of its K/V head group and over the listed
-// q-tiles in sub-tiles of 64 rows.  Per sub-tile:
-//   S  = Q K^T and dP = dO V^T     (lane = key, registers = queries)
+// rows (as MFMA B operands) and their dK, dV accumulators in registers for
+// the whole run, looping over the query heads of its K/V head group and over
+// the listed q-tiles in sub-tiles of 64 rows.  Per block of 32 queries:
+//   S  = Q K^T, dP = dO V^T           (lane = key, registers = queries)
 //   P  = exp2(S * scale*log2e - LSE*log2e) on allowed pairs, dS = P (dP - delta)
-//   dV += P^T dO,  dK += dS^T Q     (A operands straight from registers)
-//   dQ += scale * dS K              (dS through LDS; fp32 atomic adds)
-// P is recomputed from the final (merged) LSE, so no attention matrix is
-// stored between forward and backward.
+//   dV += P^T dO, dK += dS^T Q        (A operands from registers; dO and Q
+//                                      read transposed from LDS)
+// Q and dO sub-tiles are double buffered in LDS (swizzled, see mfma.h) with
+// the next sub-tile's rows loading into registers while the current one
+// computes.  Each (chunk, k-tile, K/V head) block of dK/dV has one owner.
+//
 #include "hsap_internal.h"
 #include "mfma.h"
 
@@ -44,23 +49,21 @@ struct BwdArgs {
 };
 
 template <int D, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void attn_bwd_kernel(BwdArgs a) {
+__global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BN = 32 * WAVES;
   constexpr int NT = 64 * WAVES;
-  constexpr int SUB = 64;      // query rows per LDS sub-tile
-  constexpr int QS = D + 8;    // row stride of Qs / dOs  [query][d]
-  constexpr int TS = SUB + 8;  // row stride of Qt / dOt  [d][query]
-  constexpr int SS = BN + 8;   // row stride of dSs [query][key] and Kt [d][key]
+  constexpr int SUB = 64;                 // query rows per sub-tile
+  constexpr int CPR = D / 8;              // 16-byte chunks per Q / dO / K row
+  constexpr int MB = D / 32;              // 32-wide blocks of d
+  constexpr int PER_T = SUB * CPR / NT;   // chunks of Q (and of dO) per thread per sub-tile
+  static_assert((SUB * CPR) % NT == 0 && (BN * CPR) % NT == 0, "tiles must split evenly over the threads");
+  static_assert(D == 128 || D == 64, "head_dim 64 or 128");
   constexpr float LOG2E = 1.44269504088896340736f;
-  __shared__ __attribute__((aligned(16))) __bf16 Qs[SUB * QS];
-  __shared__ __attribute__((aligned(16))) __bf16 dOs[SUB * QS];
-  __shared__ __attribute__((aligned(16))) __bf16 Qt[D * TS];
-  __shared__ __attribute__((aligned(16))) __bf16 dOt[D * TS];
-  __shared__ __attribute__((aligned(16))) __bf16 dSs[SUB * SS];
-  __shared__ __attribute__((aligned(16))) __bf16 Kt[D * SS];
-  __shared__ float lse_s[SUB];
-  __shared__ float delta_s[SUB];
-  __shared__ int32_t start_s[SUB];
+  __shared__ __attribute__((aligned(16))) __bf16 Qs[2][SUB * D];
+  __shared__ __attribute__((aligned(16))) __bf16 dOs[2][SUB * D];
+  __shared__ float lse_s[2][SUB];
+  __shared__ float delta_s[2][SUB];
+  __shared__ int32_t start_s[2][SUB];
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
@@ -70,10 +73,25 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bwd_kernel(BwdArgs a) {
   const int c = run.chunk;
   const int64_t n = a.geom.n;
   const int64_t krow0 = (int64_t)run.tile * BN;
-  const int64_t gk = global_pos(a.geom, c, krow0 + 32 * w + l32);  // this lane's key position
-  const int64_t kvrow = (int64_t)c * n + krow0;                    // first row in the sharded K/V buffers
+  const int32_t gk = (int32_t)global_pos(a.geom, c, krow0 + 32 * w + l32);  // this lane's key position
+  const int64_t kvrow = (int64_t)c * n + krow0;                            // first row in the sharded K/V buffers
 
-  // K and V rows of this lane's key as MFMA B operands; K^T of the whole tile in LDS
+  // ---- LDS offsets (elements) as lane constants + compile-time immediates -------------
+  // Row reads (row 32 qb + l32, chunk 2 kk + hi) of a swizzled [rows][D] tile:
+  //   offset = 32 qb * D + rowoff[kk]
+  // Transpose reads (rows rb + tr_row with rb = 8 k (mod 16), columns 32 mb + tr_col):
+  //   offset = rb * D + troff[mb][k]      (the swizzle of rb + tr_row depends on k only)
+  const int tr_row = 4 * hi + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int rowoff[D / 16], troff[MB][2];
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) rowoff[kk] = swz<CPR>(l32, 16 * kk + 8 * hi);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int k = 0; k < 2; ++k) troff[mb][k] = swz<CPR>(8 * k + tr_row, 32 * mb + tr_col) - 8 * k * D;
+
+  // K and V rows of this lane's key as MFMA B operands
   bf16x8 kf[D / 16], vf[D / 16];
   {
     const int64_t off = ((kvrow + 32 * w + l32) * a.hkv + g) * D + 8 * hi;
@@ -82,118 +100,136 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bwd_kernel(BwdArgs a) {
       kf[kk] = *(const bf16x8*)(a.k + off + 16 * kk);
       vf[kk] = *(const bf16x8*)(a.v + off + 16 * kk);
     }
-    for (int i = tid; i < BN * D / 8; i += NT) {
-      const int row = i / (D / 8), cc = i % (D / 8);
-      const bf16x8 x = *(const bf16x8*)(a.k + ((kvrow + row) * a.hkv + g) * D + cc * 8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Kt[(cc * 8 + e) * SS + row] = x[e];
-    }
   }
 
-  f32x16 dk[D / 32], dv[D / 32];
+  f32x16 dk[MB], dv[MB];
 #pragma unroll
-  for (int mb = 0; mb < D / 32; ++mb) {
+  for (int mb = 0; mb < MB; ++mb) {
     dk[mb] = f32x16{};
     dv[mb] = f32x16{};
   }
 
-  for (int hh = 0; hh < a.group; ++hh) {
-    const int h = g * a.group + hh;
-    for (int it = 0; it < run.count; ++it) {
-      const hsap_tile tile = a.tiles[run.first + it];
-      const bool masked = tile.kind == HSAP_TILE_MASKED;
-      for (int sub = 0; sub < a.bm / SUB; ++sub) {
-        const int64_t q0 = (int64_t)tile.q_tile * a.bm + sub * SUB;  // shard-local first row
-        const int64_t gq0 = global_pos(a.geom, a.shard, q0);
-        __syncthreads();  // previous sub-tile's LDS reads are done (and Kt is written)
-        for (int i = tid; i < SUB * D / 8; i += NT) {
-          const int row = i / (D / 8), cc = i % (D / 8);
-          const int64_t src = ((q0 + row) * a.hq + h) * D + cc * 8;
-          const bf16x8 x = *(const bf16x8*)(a.q + src);
-          const bf16x8 y = *(const bf16x8*)(a.d_o + src);
-          *(bf16x8*)(Qs + row * QS + cc * 8) = x;
-          *(bf16x8*)(dOs + row * QS + cc * 8) = y;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            Qt[(cc * 8 + e) * TS + row] = x[e];
-            dOt[(cc * 8 + e) * TS + row] = y[e];
-          }
-        }
-        for (int i = tid; i < SUB; i += NT) {
-          const float l = a.lse[(int64_t)h * n + q0 + i];
-          lse_s[i] = l == -__builtin_inff() ? __builtin_inff() : l * LOG2E;  // a row with no key gets P = 0
-          delta_s[i] = a.delta[(int64_t)h * n + q0 + i];
-          start_s[i] = a.doc_start[gq0 + i];
-        }
-        __syncthreads();
+  const int nsub = a.bm / SUB;
+  const int per_head = run.count * nsub;
+  const int total = a.group * per_head;
+  // sub-tile `it`: query head, tile of the run, 64-row slice of the tile
+  auto head_of = [&](int it) { return g * a.group + it / per_head; };
+  auto tile_of = [&](int it) { return a.tiles[run.first + (it % per_head) / nsub]; };
+  auto q0_of = [&](const hsap_tile& t, int it) { return (int64_t)t.q_tile * a.bm + ((it % per_head) % nsub) * SUB; };
 
-        f32x16 p[SUB / 32], ds[SUB / 32];
+  // staging of one sub-tile: Q and dO rows, and the per-row LSE, delta and document start
+  int32_t soff[PER_T], loff[PER_T];
 #pragma unroll
-        for (int qb = 0; qb < SUB / 32; ++qb) {
-          f32x16 sacc{}, dpacc{};
+  for (int i = 0; i < PER_T; ++i) {
+    const int idx = tid + i * NT, row = idx / CPR, cc = idx % CPR;
+    soff[i] = row * a.hq * D + cc * 8;
+    loff[i] = swz<CPR>(row, cc * 8);
+  }
+  bf16x8 qreg[PER_T], oreg[PER_T];
+  float lreg = 0.f, dreg = 0.f;
+  int32_t sreg = 0;
+  auto load_sub = [&](int it) {
+    const int h = head_of(it);
+    const hsap_tile t = tile_of(it);
+    const int64_t q0 = q0_of(t, it);
+    const int64_t base = (q0 * a.hq + h) * D;
 #pragma unroll
-          for (int kk = 0; kk < D / 16; ++kk) {
-            const bf16x8 qa = *(const bf16x8*)(Qs + (32 * qb + l32) * QS + 16 * kk + 8 * hi);
-            const bf16x8 da = *(const bf16x8*)(dOs + (32 * qb + l32) * QS + 16 * kk + 8 * hi);
-            sacc = mfma32(qa, kf[kk], sacc);
-            dpacc = mfma32(da, vf[kk], dpacc);
+    for (int i = 0; i < PER_T; ++i) {
+      qreg[i] = *(const bf16x8*)(a.q + base + soff[i]);
+      oreg[i] = *(const bf16x8*)(a.d_o + base + soff[i]);
+    }
+    if (tid < SUB) {
+      lreg = a.lse[(int64_t)h * n + q0 + tid];
+      dreg = a.delta[(int64_t)h * n + q0 + tid];
+      sreg = a.doc_start[global_pos(a.geom, a.shard, q0) + tid];
+    }
+  };
+  auto store_sub = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      *(bf16x8*)(&Qs[buf][loff[i]]) = qreg[i];
+      *(bf16x8*)(&dOs[buf][loff[i]]) = oreg[i];
+    }
+    if (tid < SUB) {
+      lse_s[buf][tid] = lreg == -__builtin_inff() ? __builtin_inff() : lreg * LOG2E;  // no key: P = 0
+      delta_s[buf][tid] = dreg;
+      start_s[buf][tid] = sreg;
+    }
+  };
+
+  load_sub(0);
+  store_sub(0);
+  __syncthreads();
+
+  for (int it = 0; it < total; ++it) {
+    const int buf = it & 1;
+    const int h = head_of(it);
+    const hsap_tile tile = tile_of(it);
+    const int64_t q0 = q0_of(tile, it);
+    const int32_t gq0 = (int32_t)global_pos(a.geom, a.shard, q0);
+    const bool masked = tile.kind == HSAP_TILE_MASKED;
+    if (it + 1 < total) load_sub(it + 1);
+    const __bf16* Q = Qs[buf];
+    const __bf16* O = dOs[buf];
+
+    // per block of 32 queries: S = Q K^T, dP = dO V^T (register j = query 32 qb + c_row(j, hi)),
+    // then P and dS, then dV += P^T dO and dK += dS^T Q, then dS^T to LDS
+#pragma unroll
+    for (int qb = 0; qb < SUB / 32; ++qb) {
+      f32x16 sacc{}, dpacc{};
+      bf16x8 qa[D / 16], oa[D / 16];  // all operand reads of the block first, then the MFMAs
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) {
+        qa[kk] = *(const bf16x8*)(Q + 32 * qb * D + rowoff[kk]);
+        oa[kk] = *(const bf16x8*)(O + 32 * qb * D + rowoff[kk]);
+      }
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) {
+        sacc = mfma32(qa[kk], kf[kk], sacc);
+        dpacc = mfma32(oa[kk], vf[kk], dpacc);
+      }
+      bf16x8 pb[2], sb[2];
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const int q4 = 32 * qb + 8 * grp + 4 * hi;  // four consecutive queries
+        const f32x4 l4 = *(const f32x4*)(&lse_s[buf][q4]);
+        const f32x4 d4 = *(const f32x4*)(&delta_s[buf][q4]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = 4 * grp + e;
+          float p = fast_exp2(__builtin_fmaf(sacc[j], a.scale_log2, -l4[e]));
+          if (masked) {
+            const int32_t st = start_s[buf][q4 + e];
+            if ((uint32_t)(gk - st) > (uint32_t)(gq0 + q4 + e - st)) p = 0.f;
           }
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int qr = 32 * qb + c_row(j, hi);
-            const bool ok = !masked || (start_s[qr] <= gk && gk <= gq0 + qr);
-            const float pv = ok ? fast_exp2(sacc[j] * a.scale_log2 - lse_s[qr]) : 0.f;
-            p[qb][j] = pv;
-            ds[qb][j] = pv * (dpacc[j] - delta_s[qr]);
-          }
+          pb[j >> 3][j & 7] = (__bf16)p;
+          sb[j >> 3][j & 7] = (__bf16)(p * (dpacc[j] - d4[e]));
         }
-        // dV += P^T dO and dK += dS^T Q (16 queries per MFMA)
+      }
 #pragma unroll
-        for (int qb = 0; qb < SUB / 32; ++qb)
+      for (int half = 0; half < 2; ++half) {
+        const int rb = (32 * qb + 16 * half) * D;
+        bf16x8 bo[MB], bq[MB];
 #pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            bf16x8 pa, sa;
+        for (int mb = 0; mb < MB; ++mb) {
+          bo[mb] = cat4(ds_read_tr16(O + rb + troff[mb][0]), ds_read_tr16(O + rb + 8 * D + troff[mb][1]));
+          bq[mb] = cat4(ds_read_tr16(Q + rb + troff[mb][0]), ds_read_tr16(Q + rb + 8 * D + troff[mb][1]));
+        }
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              pa[e] = (__bf16)p[qb][8 * half + e];
-              sa[e] = (__bf16)ds[qb][8 * half + e];
-            }
-#pragma unroll
-            for (int mb = 0; mb < D / 32; ++mb) {
-              const int o = (32 * mb + l32) * TS + 32 * qb + 16 * half + 4 * hi;
-              dv[mb] = mfma32(pa, cat4(*(const bf16x4*)(dOt + o), *(const bf16x4*)(dOt + o + 8)), dv[mb]);
-              dk[mb] = mfma32(sa, cat4(*(const bf16x4*)(Qt + o), *(const bf16x4*)(Qt + o + 8)), dk[mb]);
-            }
-          }
-        // dS to LDS as [query][key] for the dQ product
-#pragma unroll
-        for (int qb = 0; qb < SUB / 32; ++qb)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) dSs[(32 * qb + c_row(j, hi)) * SS + 32 * w + l32] = (__bf16)ds[qb][j];
-        __syncthreads();
-        // dQ[query, d] += scale * sum_key dS[query, key] K[key, d]; 32x32 blocks spread over the waves
-        constexpr int NB = (SUB / 32) * (D / 32);
-#pragma unroll
-        for (int b = w; b < NB; b += WAVES) {
-          const int qb = b / (D / 32), mb = b % (D / 32);
-          f32x16 acc{};
-#pragma unroll
-          for (int ks = 0; ks < BN / 16; ++ks) {
-            const bf16x8 sa = *(const bf16x8*)(dSs + (32 * qb + l32) * SS + 16 * ks + 8 * hi);
-            const bf16x8 kb = *(const bf16x8*)(Kt + (32 * mb + l32) * SS + 16 * ks + 8 * hi);
-            acc = mfma32(sa, kb, acc);
-          }
-          float* dst = a.dq + ((q0 + 32 * qb) * a.hq + h) * D + 32 * mb + l32;
-#pragma unroll
-          for (int j = 0; j < 16; ++j) unsafeAtomicAdd(dst + (int64_t)c_row(j, hi) * a.hq * D, acc[j] * a.scale);
+        for (int mb = 0; mb < MB; ++mb) {
+          dv[mb] = mfma32(pb[half], bo[mb], dv[mb]);
+          dk[mb] = mfma32(sb[half], bq[mb], dk[mb]);
         }
       }
     }
+
+    if (it + 1 < total) store_sub(buf ^ 1);
+    hsap_lds_barrier();
   }
 
   // this workgroup owns rows [krow0, krow0 + BN) of chunk c for K/V head g: plain read-add-write
 #pragma unroll
-  for (int mb = 0; mb < D / 32; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int64_t idx = ((kvrow + 32 * w + c_row(j, hi)) * a.hkv + g) * D + 32 * mb + l32;
@@ -202,13 +238,176 @@ __global__ __launch_bounds__(64 * WAVES) void attn_bwd_kernel(BwdArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// dQ kernel: one workgroup per (q-major run, query head), shaped like the
+// forward.  Wave w owns 32 query rows; in the transposed orientation
+// S^T = K Q^T and dP^T = V dO^T a lane holds one query, so its LSE and delta
+// are scalars of the lane.  Per step of 64 keys:
+//   P^T = exp2(S^T * scale*log2e - LSE*log2e), dS^T = P^T o (dP^T - delta),
+//   dQ^T += K^T dS^T (K^T read transposed from the [key][d] tile).
+// dQ stays in registers for the whole run and is added to dq_acc once at the
+// end (a q-tile meets one run per chunk, so at most P adds per element).
+// ---------------------------------------------------------------------------
+template <int D, int BN, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
+  constexpr int KB = 64;                     // keys per step
+  constexpr int SUBS = BN / KB;
+  constexpr int NT = 64 * WAVES;
+  constexpr int CPR = D / 8;
+  constexpr int MB = D / 32;
+  constexpr int CHUNKS = KB * CPR;
+  constexpr int PER_T = CHUNKS / NT;
+  static_assert(CHUNKS % NT == 0, "step must split evenly over the threads");
+  constexpr float LOG2E = 1.44269504088896340736f;
+  constexpr float NEG_INF = -__builtin_inff();
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[2][KB * D];  // swizzled [key][d]
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[2][KB * D];
+
+  const int tid = threadIdx.x;
+  const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
+  const int run_idx = blockIdx.x / a.hq;
+  const int h = blockIdx.x - run_idx * a.hq;
+  const hsap_run run = a.runs[run_idx];
+  if (run.count == 0) return;
+  const int c = run.chunk;
+  const int g = h / a.group;
+  const int64_t n = a.geom.n;
+  const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;
+  const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
+  const int32_t qstart = a.doc_start[gq];
+  const uint32_t span = (uint32_t)(gq - qstart);
+  const float lse_raw = a.lse[(int64_t)h * n + qrow];
+  const float lse2 = lse_raw == NEG_INF ? __builtin_inff() : lse_raw * LOG2E;  // no key: P = 0
+  const float dlt = a.delta[(int64_t)h * n + qrow];
+  bf16x8 qf[D / 16], of[D / 16];
+  {
+    const int64_t off = (qrow * a.hq + h) * D + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      qf[kk] = *(const bf16x8*)(a.q + off + 16 * kk);
+      of[kk] = *(const bf16x8*)(a.d_o + off + 16 * kk);
+    }
+  }
+  const int tr_row = 4 * hi + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int rowoff[D / 16], troff[MB][2];
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) rowoff[kk] = swz<CPR>(l32, 16 * kk + 8 * hi);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int k = 0; k < 2; ++k) troff[mb][k] = swz<CPR>(8 * k + tr_row, 32 * mb + tr_col) - 8 * k * D;
+
+  const int64_t rstride = (int64_t)a.hkv * D;
+  const __bf16* kbase = a.k + ((int64_t)c * n * a.hkv + g) * D;
+  const __bf16* vbase = a.v + ((int64_t)c * n * a.hkv + g) * D;
+  const int total = run.count * SUBS;
+  int32_t goff[PER_T], loff[PER_T];
+#pragma unroll
+  for (int i = 0; i < PER_T; ++i) {
+    const int idx = tid + i * NT, row = idx / CPR, cc = idx % CPR;
+    goff[i] = (int32_t)(row * rstride + cc * 8);
+    loff[i] = swz<CPR>(row, cc * 8);
+  }
+  bf16x8 kreg[PER_T], vreg[PER_T];
+  auto step_row0 = [&](const hsap_tile& t, int s) { return (int64_t)t.k_tile * BN + (s % SUBS) * KB; };
+  auto load_step = [&](int64_t row0) {
+    const __bf16* kb = kbase + row0 * rstride;
+    const __bf16* vb = vbase + row0 * rstride;
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      kreg[i] = *(const bf16x8*)(kb + goff[i]);
+      vreg[i] = *(const bf16x8*)(vb + goff[i]);
+    }
+  };
+  auto store_step = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      *(bf16x8*)(&Ks[buf][loff[i]]) = kreg[i];
+      *(bf16x8*)(&Vs[buf][loff[i]]) = vreg[i];
+    }
+  };
+
+  f32x16 dq[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) dq[mb] = f32x16{};
+
+  hsap_tile cur = a.tiles[run.first];
+  load_step(step_row0(cur, 0));
+  store_step(0);
+  hsap_tile nxt = cur;
+  if (run.count > 1) nxt = a.tiles[run.first + 1];
+  __syncthreads();
+
+  for (int s = 0; s < total; ++s) {
+    const int buf = s & 1;
+    const hsap_tile tile = cur;
+    if (s + 1 < total) {
+      if ((s + 1) % SUBS == 0) {
+        cur = nxt;
+        if ((s + 1) / SUBS + 1 < run.count) nxt = a.tiles[run.first + (s + 1) / SUBS + 1];
+      }
+      load_step(step_row0(cur, s + 1));
+    }
+    const __bf16* K = Ks[buf];
+    const __bf16* V = Vs[buf];
+    const bool masked = tile.kind == HSAP_TILE_MASKED;
+    const int32_t rel0 = masked ? (int32_t)global_pos(a.geom, c, step_row0(tile, s)) - qstart : 0;
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb) {
+      f32x16 st{}, dpt{};
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) {
+        st = mfma32(*(const bf16x8*)(K + 32 * nb * D + rowoff[kk]), qf[kk], st);
+        dpt = mfma32(*(const bf16x8*)(V + 32 * nb * D + rowoff[kk]), of[kk], dpt);
+      }
+      bf16x8 sb[2];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        float p = fast_exp2(__builtin_fmaf(st[j], a.scale_log2, -lse2));
+        if (masked && (uint32_t)(rel0 + 32 * nb + c_row(j, hi)) > span) p = 0.f;
+        sb[j >> 3][j & 7] = (__bf16)(p * (dpt[j] - dlt));
+      }
+      // dQ^T += K^T dS^T, 16 keys per MFMA
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int rb = (32 * nb + 16 * half) * D;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const bf16x8 ka = cat4(ds_read_tr16(K + rb + troff[mb][0]), ds_read_tr16(K + rb + 8 * D + troff[mb][1]));
+          dq[mb] = mfma32(ka, sb[half], dq[mb]);
+        }
+      }
+    }
+    if (s + 1 < total) store_step(buf ^ 1);
+    __syncthreads();
+  }
+
+  // dQ^T: this lane's query, d = 32 mb + c_row(j, hi); four consecutive d per register group
+  float* dst = a.dq + (qrow * a.hq + h) * D + 4 * hi;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) unsafeAtomicAdd(dst + 32 * mb + 8 * (j >> 2) + (j & 3), dq[mb][j] * a.scale);
+}
+
 template <int D, int WAVES>
-static hsap_status launch_bwd(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
+static hsap_status launch_dkdv(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hkv;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_bwd_kernel<D, WAVES>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, WAVES>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
   const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_bwd launch: %s", hipGetErrorString(e));
+  if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_bwd_dkdv launch: %s", hipGetErrorString(e));
+  return HSAP_OK;
+}
+
+template <int D, int BN, int WAVES>
+static hsap_status launch_dq(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
+  const int64_t blocks = num_runs * a.hq;
+  if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, BN, WAVES>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_bwd_dq launch: %s", hipGetErrorString(e));
   return HSAP_OK;
 }
 
@@ -218,21 +417,28 @@ using namespace hsap;
 
 extern "C" hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
                                              const void* d_o, const float* lse, const float* delta,
-                                             const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
-                                             int64_t num_runs, float* dq_acc, float* dk_acc, float* dv_acc,
-                                             void* hip_stream) {
+                                             const int32_t* doc_start, const hsap_tile* tiles_k,
+                                             const hsap_run* runs_k, int64_t num_runs_k, const hsap_tile* tiles_q,
+                                             const hsap_run* runs_q, int64_t num_runs_q, float* dq_acc,
+                                             float* dk_acc, float* dv_acc, void* hip_stream) {
   clear_error();
   Geom geom;
   hsap_status st = check_attn(desc, &geom);
   if (st != HSAP_OK) return st;
-  if (num_runs < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_runs < 0");
-  if (num_runs == 0) return HSAP_OK;
-  if (!q || !k || !v || !d_o || !lse || !delta || !doc_start || !tiles || !runs || !dq_acc || !dk_acc || !dv_acc)
+  if (num_runs_k < 0 || num_runs_q < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "negative run count");
+  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
+  if (bm % 64) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "backward needs BM a multiple of 64 (BM=%d)", bm);
+  const bool dkdv_ok = (d == 128 && (bn == 128 || bn == 64)) || (d == 64 && bn == 64);
+  const bool dq_ok = (bm == 128 || bm == 64) && (bn == 128 || bn == 64);
+  if (!dkdv_ok || !dq_ok)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no backward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
+  if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
+  if (num_runs_k == 0 && num_runs_q == 0) return HSAP_OK;
+  if (!q || !k || !v || !d_o || !lse || !delta || !doc_start || !dq_acc || !dk_acc || !dv_acc ||
+      (num_runs_k > 0 && (!tiles_k || !runs_k)) || (num_runs_q > 0 && (!tiles_q || !runs_q)))
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)d_o) & 15)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k, v and d_o must be 16-byte aligned");
-  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
-  if (bm % 64) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "backward needs BM a multiple of 64 (BM=%d)", bm);
   BwdArgs a;
   a.q = (const __bf16*)q;
   a.k = (const __bf16*)k;
@@ -241,8 +447,6 @@ extern "C" hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const v
   a.lse = lse;
   a.delta = delta;
   a.doc_start = doc_start;
-  a.tiles = tiles;
-  a.runs = runs;
   a.dq = dq_acc;
   a.dk = dk_acc;
   a.dv = dv_acc;
@@ -255,8 +459,28 @@ extern "C" hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const v
   a.scale = desc->softmax_scale;
   a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
   hipStream_t s = (hipStream_t)hip_stream;
-  if (d == 128 && bn == 128) return launch_bwd<128, 4>(a, num_runs, s);
-  if (d == 128 && bn == 64) return launch_bwd<128, 2>(a, num_runs, s);
-  if (d == 64 && bn == 64) return launch_bwd<64, 2>(a, num_runs, s);
-  HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no backward kernel for head_dim=%d BN=%d", d, bn);
+  if (num_runs_k > 0) {
+    a.tiles = tiles_k;
+    a.runs = runs_k;
+    if (d == 128 && bn == 128) st = launch_dkdv<128, 4>(a, num_runs_k, s);
+    else if (d == 128) st = launch_dkdv<128, 2>(a, num_runs_k, s);
+    else st = launch_dkdv<64, 2>(a, num_runs_k, s);
+    if (st != HSAP_OK) return st;
+  }
+  if (num_runs_q > 0) {
+    a.tiles = tiles_q;
+    a.runs = runs_q;
+#define HSAP_DQ_CASE(D_, BN_, W_) \
+  if (d == D_ && bn == BN_ && bm == 32 * W_) return launch_dq<D_, BN_, W_>(a, num_runs_q, s);
+    HSAP_DQ_CASE(128, 128, 4)
+    HSAP_DQ_CASE(128, 64, 4)
+    HSAP_DQ_CASE(128, 128, 2)
+    HSAP_DQ_CASE(128, 64, 2)
+    HSAP_DQ_CASE(64, 128, 4)
+    HSAP_DQ_CASE(64, 64, 4)
+    HSAP_DQ_CASE(64, 128, 2)
+    HSAP_DQ_CASE(64, 64, 2)
+#undef HSAP_DQ_CASE
+  }
+  return HSAP_OK;
 }

@@ -17,9 +17,10 @@
 // operand is read from the [key][d] tile with the LDS transpose read, whose
 // per-lane key order matches the register order of the score block.
 //
-// Pipelining: two LDS buffers.  While a step computes on one buffer, the next
-// step's K/V rows are already loading into registers; they are written to the
-// other buffer after the compute, and one barrier per step orders the two.
+// Pipelining: the scores of step s + 1 are computed on the matrix cores while
+// the vector units run the softmax of step s.  K and V each have two LDS
+// slots; the next K/V rows load into registers during a step and are written
+// to the free slots at its end, one barrier per step.
 // Scores are scaled by softmax_scale * log2(e) so the exponentials are exp2.
 // FULL tiles skip all mask arithmetic; MASKED tiles compare each key position
 // with the query's document start and position.  O is rescaled only when
@@ -89,8 +90,10 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   const __bf16* kbase = a.k + ((int64_t)c * n * a.hkv + g) * D;
   const __bf16* vbase = a.v + ((int64_t)c * n * a.hkv + g) * D;
   const int total = run.count * SUBS;
+  auto tile_at = [&](int s) { return a.tiles[run.first + s / SUBS]; };
+  auto step_row0 = [&](const hsap_tile& t, int s) { return (int64_t)t.k_tile * BN + (s % SUBS) * KB; };
 
-  // staging: thread t moves chunks t, t + NT, ... of the step's [KB][D] tiles
+  // staging: thread t moves chunks t, t + NT, ... of a step's [KB][D] tile
   int32_t goff[PER_T], koff[PER_T], voff[PER_T];
 #pragma unroll
   for (int i = 0; i < PER_T; ++i) {
@@ -100,23 +103,37 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     voff[i] = row * VS + cc * 8;
   }
   bf16x8 kreg[PER_T], vreg[PER_T];
-  auto load_step = [&](int64_t row0) {
-    const __bf16* kb = kbase + row0 * rstride;
-    const __bf16* vb = vbase + row0 * rstride;
+  auto load_k = [&](int64_t row0) {
+    const __bf16* src = kbase + row0 * rstride;
 #pragma unroll
-    for (int i = 0; i < PER_T; ++i) {
-      kreg[i] = *(const bf16x8*)(kb + goff[i]);
-      vreg[i] = *(const bf16x8*)(vb + goff[i]);
+    for (int i = 0; i < PER_T; ++i) kreg[i] = *(const bf16x8*)(src + goff[i]);
+  };
+  auto load_v = [&](int64_t row0) {
+    const __bf16* src = vbase + row0 * rstride;
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) vreg[i] = *(const bf16x8*)(src + goff[i]);
+  };
+  auto store_k = [&](int slot) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) *(bf16x8*)(&Ks[slot][koff[i]]) = kreg[i];
+  };
+  auto store_v = [&](int slot) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) *(bf16x8*)(&Vs[slot][voff[i]]) = vreg[i];
+  };
+  // S^T = K Q^T for the two 32-key blocks of a step held in K slot `slot`
+  auto scores = [&](int slot, f32x16 (&sc)[KB / 32]) {
+    const __bf16* K = Ks[slot];
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb) {
+      bf16x8 kf[D / 16];
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(K + (32 * nb + l32) * KS + 16 * kk + 8 * hi);
+      sc[nb] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) sc[nb] = mfma32(kf[kk], qf[kk], sc[nb]);
     }
   };
-  auto store_step = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < PER_T; ++i) {
-      *(bf16x8*)(&Ks[buf][koff[i]]) = kreg[i];
-      *(bf16x8*)(&Vs[buf][voff[i]]) = vreg[i];
-    }
-  };
-  auto step_row0 = [&](const hsap_tile& t, int s) { return (int64_t)t.k_tile * BN + (s % SUBS) * KB; };
 
   // transpose-read geometry for the V^T operand (see mfma.h): lane j of each
   // 16-lane group points at 4 consecutive d of key row (j / 4) of its group
@@ -128,38 +145,33 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
 
-  hsap_tile cur = a.tiles[run.first];
-  load_step(step_row0(cur, 0));
-  store_step(0);
-  hsap_tile nxt = cur;
-  if (run.count > 1) nxt = a.tiles[run.first + 1];
+  // Software pipeline: iteration s takes the softmax of step s, the scores of
+  // step s + 1 and the PV product of step s.  K runs two steps ahead of use
+  // and V one, so slot s % 2 of K (last read for the scores of step s, in
+  // iteration s - 1) and slot (s + 1) % 2 of V (last read in iteration s - 1)
+  // are free to refill during iteration s; one barrier per iteration orders
+  // the refills against the next iteration's reads.
+  hsap_tile t_cur = tile_at(0);
+  load_k(step_row0(t_cur, 0));
+  store_k(0);
+  load_v(step_row0(t_cur, 0));
+  store_v(0);
+  if (total > 1) {
+    load_k(step_row0(tile_at(1), 1));
+    store_k(1);
+  }
   __syncthreads();
+  f32x16 sc[KB / 32];
+  scores(0, sc);
 
   for (int s = 0; s < total; ++s) {
-    const int buf = s & 1;
-    const hsap_tile tile = cur;
-    if (s + 1 < total) {
-      // descriptor of step s + 1, then of the tile after it (loaded a step ahead)
-      if ((s + 1) % SUBS == 0) {
-        cur = nxt;
-        if ((s + 1) / SUBS + 1 < run.count) nxt = a.tiles[run.first + (s + 1) / SUBS + 1];
-      }
-      load_step(step_row0(cur, s + 1));
-    }
-    const __bf16* K = Ks[buf];
-    const __bf16* V = Vs[buf];
+    const hsap_tile tile = tile_at(s);
+    if (s + 2 < total) load_k(step_row0(tile_at(s + 2), s + 2));
+    if (s + 1 < total) load_v(step_row0(tile_at(s + 1), s + 1));
+    // scores of the next step: independent of this step's softmax
+    f32x16 sn[KB / 32];
+    if (s + 1 < total) scores((s + 1) & 1, sn);
 
-    // S^T = K Q^T for 2 blocks of 32 keys
-    f32x16 sc[KB / 32];
-#pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb) {
-      bf16x8 kf[D / 16];
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(K + (32 * nb + l32) * KS + 16 * kk + 8 * hi);
-      sc[nb] = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) sc[nb] = mfma32(kf[kk], qf[kk], sc[nb]);
-    }
     if (tile.kind == HSAP_TILE_MASKED) {
       const int32_t rel0 = (int32_t)global_pos(a.geom, c, step_row0(tile, s)) - qstart;
 #pragma unroll
@@ -199,6 +211,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     l_run += rs;  // the half-row sums of lanes l and l ^ 32 are combined once, at the end
 
     // O^T += V^T P^T, 16 keys per MFMA
+    const __bf16* V = Vs[s & 1];
 #pragma unroll
     for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
@@ -212,8 +225,11 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
         }
       }
 
-    if (s + 1 < total) store_step(buf ^ 1);
+    if (s + 2 < total) store_k(s & 1);
+    if (s + 1 < total) store_v((s + 1) & 1);
     __syncthreads();
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb) sc[nb] = sn[nb];
   }
 
   l_run = pair_sum(l_run);

@@ -55,4 +55,33 @@ __device__ __forceinline__ bf16x4 ds_read_tr16(const __bf16* lds_ptr) {
   return __builtin_bit_cast(bf16x4, r);
 }
 
+// Workgroup barrier for LDS producer/consumer hand-offs.  It waits for this
+// wave's LDS operations only (lgkmcnt), not for its global loads, stores or
+// atomics (vmcnt): prefetches and fire-and-forget atomics stay in flight
+// across the barrier.  Must only order LDS traffic.  The asm's memory
+// clobber keeps the compiler from moving memory operations across it.
+__device__ __forceinline__ void hsap_lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Unpadded LDS tiles of CPR 16-byte chunks per row (CPR = 16: 128 bf16 per
+// row; CPR = 8: 64 bf16) store chunk c of row r at chunk c ^ f(r).  f is
+// chosen so that both access patterns of the attention kernels hit 16
+// distinct 16-byte bank slots:
+//   row reads (ds_read_b128): 16 consecutive rows, one chunk;
+//   transpose reads (ds_read_b64_tr_b16, 32 lanes): 4 aligned rows x an
+//   aligned group of 4 chunks;
+// and a row's chunks remain a permutation of themselves.
+template <int CPR>
+__device__ __forceinline__ int swz_chunk(int r, int c) {
+  static_assert(CPR == 16 || CPR == 8, "swizzle defined for 64- and 128-wide rows");
+  if constexpr (CPR == 16) return c ^ (4 * (r & 3) + ((r >> 2) & 3));
+  else return c ^ (4 * ((r >> 1) & 1) + ((r >> 2) & 3));
+}
+// element offset of (row r, column e) in such a tile; e % 8 is kept within the chunk
+template <int CPR>
+__device__ __forceinline__ int swz(int r, int e) {
+  return r * (CPR * 8) + swz_chunk<CPR>(r, e >> 3) * 8 + (e & 7);
+}
+
 }  // namespace hsap

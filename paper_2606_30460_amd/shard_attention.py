@@ -8,7 +8,8 @@ runs inside the library:
   forward   hsap_partial_attn_fwd over the runs (one launch for every chunk,
             or one launch per ring step), then hsap_lse_merge of the chunks
             that have tiles
-  backward  hsap_attn_bwd_preprocess, hsap_partial_attn_bwd, and
+  backward  hsap_attn_bwd_preprocess, hsap_partial_attn_bwd (dK/dV over the
+            k-major runs, dQ over the forward's q-major runs), and
             hsap_convert_f32_bf16 for the gradients
 
 Tensors follow the library's layouts: the shard's q / dO are [n, Hq, d] in
@@ -133,7 +134,7 @@ class ShardAttention:
             bufs["dv_acc"].zero_()
         L.attn_bwd_preprocess(fwd["o"], d_o, self.n, self.hq, self.d, bufs["delta"])
         L.partial_attn_bwd(self.desc, q, k, v, d_o, fwd["lse"], bufs["delta"], self.doc_start, self.tiles_k,
-                           self.runs_k, bufs["dq_acc"], bufs["dk_acc"], bufs["dv_acc"])
+                           self.runs_k, self.tiles_q, self.runs_q, bufs["dq_acc"], bufs["dk_acc"], bufs["dv_acc"])
         L.convert_f32_bf16(bufs["dq_acc"], bufs["dq"])
         # only chunks with tiles receive gradient; the others stay as zeroed
         for c in (self.present if zero else range(self.P)):

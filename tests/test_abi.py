@@ -145,12 +145,16 @@ def test_backward_validates_before_launch():
     fake = ctypes.c_void_p(4096)
     d = _attn_desc(block_m=32, total_tokens=64 * 2, block_n=32)
     st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
-                                   fake, fake, None)
+                                   fake, 1, fake, fake, fake, None)
     assert st == L.HSAP_ERR_UNSUPPORTED
     d = _attn_desc(head_dim=64, block_n=128)
     st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
-                                   fake, fake, None)
+                                   fake, 1, fake, fake, fake, None)
     assert st == L.HSAP_ERR_UNSUPPORTED
+    d = _attn_desc()
+    st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, None, None, 1, fake,
+                                   fake, 1, fake, fake, fake, None)
+    assert st == L.HSAP_ERR_INVALID_ARG
 
 
 def test_merge_and_helpers_validate():
