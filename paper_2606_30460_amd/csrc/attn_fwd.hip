@@ -148,9 +148,10 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   // Software pipeline: iteration s takes the softmax of step s, the scores of
   // step s + 1 and the PV product of step s.  K runs two steps ahead of use
   // and V one, so slot s % 2 of K (last read for the scores of step s, in
-  // iteration s - 1) and slot (s + 1) % 2 of V (last read in iteration s - 1)
-  // are free to refill during iteration s; one barrier per iteration orders
-  // the refills against the next iteration's reads.
+  // iteration s - 1, or before the loop for s = 0) and slot (s + 1) % 2 of V
+  // (last read in iteration s - 1) are free to refill during iteration s; one
+  // barrier per iteration orders the refills against the next iteration's
+  // reads.
   hsap_tile t_cur = tile_at(0);
   load_k(step_row0(t_cur, 0));
   store_k(0);
@@ -163,6 +164,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   __syncthreads();
   f32x16 sc[KB / 32];
   scores(0, sc);
+  __syncthreads();  // every wave has read K slot 0 before iteration 0 refills it
 
   for (int s = 0; s < total; ++s) {
     const hsap_tile tile = tile_at(s);
