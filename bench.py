@@ -208,6 +208,56 @@ def cpu_baseline(name: str, budget_s: float):
             "cpu": cpu_model, "affinity_cores": cores}
 
 
+FWD_SOURCES = ("paper_2606_30460_amd/csrc/attn_fwd.hip", "paper_2606_30460_amd/csrc/mfma.h",
+               "paper_2606_30460_amd/csrc/hsap_internal.h")
+TRAFFIC_SUMMARY = "profiles/attn_fwd_hbm_traffic.md"
+
+
+def fwd_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in FWD_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per forward launch from the committed counter summary, or None.
+
+    The summary records the bytes measured with rocprofv3 (FETCH_SIZE +
+    WRITE_SIZE, scaled by a plain copy of known size) together with the hash of
+    the forward kernel's sources at the time; a changed kernel reports None.
+    """
+    path = os.path.join(ROOT, TRAFFIC_SUMMARY)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ":" in line:
+                k, v = line[2:].split(":", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    if fields.get("kernel_source_sha256_16") != fwd_source_hash() or fields.get("workload") != workload:
+        return None
+    try:
+        return int(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def calibrate_copy(nbytes: int) -> None:
+    """A plain device-to-device copy of known size, for scaling HBM byte counters."""
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": src.numel() * 4, "copies": 3}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -216,7 +266,12 @@ def main():
     ap.add_argument("--workload", default="c2")
     ap.add_argument("--extra", default="c3,c4,c5", help="other workloads reported under 'extra' ('' for none)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle budget for the CPU baseline (0: skip)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (counter calibration) and exit")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the sequence-parallel split is simulated in memory on a single "
               "MI355X; run it with --gpus 1", file=sys.stderr)
@@ -262,7 +317,7 @@ def main():
         "pct_of_bf16_peak": round(100.0 * main_res["tflops"] / PEAK_BF16_TFLOPS, 3),
         "roofline": {"bound": "mfma", "kernel": "attn_fwd_kernel", "achieved": round(achieved, 3),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
-                     "traffic": None},
+                     "traffic": measured_traffic(args.workload), "kernel_source_sha256_16": fwd_source_hash()},
         "cpu_baseline": cpu,
         "detail": main_res,
         "extra": extra,
