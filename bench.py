@@ -82,11 +82,11 @@ def measure(name: str, steps: int, warmup: int, backward=None):
         e[0].record()
         L.partial_attn_fwd(sa.desc, q, k, v, sa.doc_start, sa.tiles_q, sa.runs_q, fwd["o_part"], fwd["lse_part"])
         e[1].record()
-        L.lse_merge([fwd["o_part"][c] for c in sa.present], [fwd["lse_part"][c] for c in sa.present], sa.n, sa.hq,
+        L.lse_merge([fwd["o_part"][s] for s in sa.present], [fwd["lse_part"][s] for s in sa.present], sa.n, sa.hq,
                     sa.d, fwd["o"], fwd["lse"])
         e[2].record()
         if bwd:
-            for c in sa.present:
+            for c in sa.chunks_present:
                 bb["dk_acc"][c].zero_()
                 bb["dv_acc"][c].zero_()
             bb["dq_acc"].zero_()
@@ -96,7 +96,7 @@ def measure(name: str, steps: int, warmup: int, backward=None):
                                sa.tiles_q, sa.runs_q, bb["dq_acc"], bb["dk_acc"], bb["dv_acc"])
             e[4].record()
             L.convert_f32_bf16(bb["dq_acc"], bb["dq"])
-            for c in sa.present:
+            for c in sa.chunks_present:
                 L.convert_f32_bf16(bb["dk_acc"][c], bb["dk"][c])
                 L.convert_f32_bf16(bb["dv_acc"][c], bb["dv"][c])
         events.append(e)
@@ -137,7 +137,8 @@ def measure(name: str, steps: int, warmup: int, backward=None):
         "block_m": w.block_m, "block_n": w.block_n, "backward": bool(bwd), "docs": w.num_docs,
         "useful_pairs": pairs, "tiles": tiles, "full_tiles": int(np.sum(sa.tiles_q.view(-1, 4)[:, 3].cpu().numpy() == 0)),
         "tile_efficiency": pairs / float(tiles * w.block_m * w.block_n),
-        "chunks_with_tiles": len(sa.present),
+        "chunks_with_tiles": len(sa.chunks_present),
+        "partial_slots": len(sa.present), "split_length": int(sa.split),
         "useful_gflop_per_step": (fwd_flops + bwd_flops) / 1e9,
         "ms_per_step": ms_step,
         "tflops": (fwd_flops + bwd_flops) / (ms_step * 1e-3) / 1e12,

@@ -79,9 +79,12 @@ typedef struct {
 
 /* A run of tiles that share (chunk, q_tile) [HSAP_MAJOR_Q] or
  * (chunk, k_tile) [HSAP_MAJOR_K]: tiles[first .. first+count-1] of the list
- * hsap_plan_runs returns.  `tile` is the shared q_tile or k_tile. */
+ * hsap_plan_runs returns, all of one chunk.  `tile` is the shared q_tile or
+ * k_tile.  `slot` is the partial-output slot the run writes: chunk +
+ * P * piece, where piece > 0 only when a long q-major run was split (see
+ * hsap_plan_runs); for k-major runs slot = chunk. */
 typedef struct {
-  int32_t chunk;
+  int32_t slot;
   int32_t tile;
   int32_t first;
   int32_t count;
@@ -144,20 +147,39 @@ hsap_status hsap_plan(const int32_t* cu_seqlens, int32_t num_docs, const hsap_sh
  * planner's list onto workgroups.
  *
  *   tiles, num_tiles  the list hsap_plan returned for `shard`.
- *   major        HSAP_MAJOR_Q: one run per (chunk, q_tile) for every q_tile of
- *                every chunk that has at least one tile -- q-tiles with none
- *                get a run with count 0, so the forward writes LSE = -inf for
- *                their rows.  sorted_tiles is the input order.
- *                HSAP_MAJOR_K: one run per (chunk, k_tile) that has tiles;
- *                sorted_tiles is ordered by ring step, k_tile, q_tile.
+ *   major        HSAP_MAJOR_Q: runs of one (chunk, q_tile).  A q-tile with
+ *                more than max_run_tiles tiles in a chunk is cut into
+ *                ceil(count / max_run_tiles) pieces of near-equal length,
+ *                piece i writing slot chunk + P * i (split-K: the LSE merge
+ *                combines the pieces like chunks).  Every slot a chunk uses
+ *                has a run for every q_tile -- count 0 where the q_tile has
+ *                no tile there -- so the forward writes LSE = -inf for every
+ *                row of a used slot it does not compute.  Chunks without
+ *                tiles get no runs.  sorted_tiles is the input order.
+ *                HSAP_MAJOR_K: one run per (chunk, k_tile) that has tiles,
+ *                slot = chunk; sorted_tiles is ordered by ring step, k_tile,
+ *                q_tile.  max_run_tiles is ignored.
+ *   max_run_tiles  longest q-major run; <= 0 means no splitting.
  *   sorted_tiles host [num_tiles] out: the tiles the runs index.
  *   runs         host [capacity] or NULL, out: ordered by count descending
- *                (longest work first), ties by ring step then tile ascending.
+ *                (longest work first), ties by ring step, tile, slot.
  *   num_runs     out: number of runs (also on HSAP_ERR_CAPACITY).
+ *   num_slots    out, nullable: 1 + the largest slot used, i.e. the number
+ *                of [n, Hq, d] partial slots the forward's outputs need.
  */
 hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles, int64_t num_tiles,
-                           int32_t major, hsap_tile* sorted_tiles, hsap_run* runs, int64_t capacity,
-                           int64_t* num_runs);
+                           int32_t major, int32_t max_run_tiles, hsap_tile* sorted_tiles, hsap_run* runs,
+                           int64_t capacity, int64_t* num_runs, int32_t* num_slots);
+
+/*
+ * hsap_split_length -- a max_run_tiles for hsap_plan_runs (host).  Returns 0
+ * (no split) unless the longest possible q-major run exceeds the average
+ * work per resident workgroup, num_tiles * heads_q / resident_workgroups;
+ * then that average, rounded up, floored at 4 tiles and at a quarter of a
+ * chunk's k-tiles (at most four pieces).  Returns -1 for invalid arguments.
+ */
+int32_t hsap_split_length(const hsap_shard_desc* shard, int64_t num_tiles, int32_t heads_q,
+                          int32_t resident_workgroups);
 
 /*
  * hsap_doc_start -- device int32 [N]: start(t) for every position t.
@@ -178,9 +200,9 @@ hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, voi
                               int64_t row_bytes, void* hip_stream);
 
 /*
- * hsap_partial_attn_fwd -- "computing" for the forward: for every run (chunk
- * c, q_tile t), the queries of q-tile t of shard r against the listed k-tiles
- * of chunk c, producing c's partial output and log-sum-exp (attention
+ * hsap_partial_attn_fwd -- "computing" for the forward: for every run (slot,
+ * q_tile t), the queries of q-tile t of shard r against the run's k-tiles of
+ * one chunk, producing that slot's partial output and log-sum-exp (attention
  * equation of the inter-group SP section restricted to the packing mask).
  *
  *   desc       shard layout (N, P, layout, r, BM, BN) and heads / head_dim /
@@ -192,20 +214,24 @@ hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, voi
  *   tiles      device hsap_tile [..]: sorted_tiles of hsap_plan_runs(MAJOR_Q).
  *   runs       device hsap_run [num_runs] from hsap_plan_runs(MAJOR_Q); any
  *              subset of them may be passed (e.g. one ring step's).
- *   o_part     device fp32 [P, n, Hq, d]: for each run with count > 0, rows of
- *              q-tile t in slot c receive the normalised partial output over
- *              c's allowed keys (0 for a row with none).
- *   lse_part   device fp32 [P, Hq, n]: rows of q-tile t in slot c receive the
- *              partial LSE, -inf where the row has no allowed key in c
- *              (always for a run with count 0).
+ *   o_part     device fp32 [num_slots, n, Hq, d]: for each run with count > 0,
+ *              rows of q-tile t in the run's slot receive the normalised
+ *              partial output over the run's allowed keys (0 for a row with
+ *              none).
+ *   lse_part   device fp32 [num_slots, Hq, n]: rows of q-tile t in the run's
+ *              slot receive the partial LSE, -inf where the row has no
+ *              allowed key among the run's tiles (always for count 0).
+ *   num_slots  slots o_part and lse_part hold (>= 1); a run whose slot is not
+ *              below it is skipped by the kernel.
  *   Rows of o_part whose LSE is -inf are not written when count == 0 and
  *   must not be read (hsap_lse_merge does not).  Rows outside every passed
- *   run are untouched.
+ *   run are untouched.  tiles and runs must be the lists hsap_plan_runs made
+ *   for this shard: the kernel trusts their tile indices.
  */
 hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, const void* k,
                                   const void* v, const int32_t* doc_start, const hsap_tile* tiles,
                                   const hsap_run* runs, int64_t num_runs, float* o_part,
-                                  float* lse_part, void* hip_stream);
+                                  float* lse_part, int32_t num_slots, void* hip_stream);
 
 /*
  * hsap_lse_merge -- online-softmax combination of partial results (the ring's
@@ -249,9 +275,9 @@ hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, 
  *   delta      device fp32 [Hq, n] from hsap_attn_bwd_preprocess.
  *   tiles_k, runs_k, num_runs_k  device lists from hsap_plan_runs(MAJOR_K).
  *   tiles_q, runs_q, num_runs_q  device lists from hsap_plan_runs(MAJOR_Q)
- *              (the forward's lists).
+ *              (the forward's lists, split or not).
  *   dq_acc     device fp32 [n, Hq, d] (+=).  Each q-major run adds its
- *              chunk's contribution with one fp32 atomic add per element.
+ *              contribution with one fp32 atomic add per element.
  *   dk_acc, dv_acc  device fp32 [P, n, Hkv, d] sharded order (+=).  Each
  *              (chunk, k_tile, K/V head) row block is owned by one
  *              workgroup: plain read-modify-write.

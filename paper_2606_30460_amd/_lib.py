@@ -33,7 +33,7 @@ MAX_MERGE_PARTS = 64
 
 # Every symbol include/hsap.h declares.
 EXPORTED = (
-    "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_doc_start",
+    "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_doc_start",
     "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
     "hsap_partial_attn_bwd", "hsap_convert_f32_bf16",
 )
@@ -64,10 +64,11 @@ _SIG = {
     "hsap_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "hsap_last_error": (ctypes.c_char_p, []),
     "hsap_plan": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _P, _P]),
-    "hsap_plan_runs": (ctypes.c_int, [_P, _P, _I64, _I32, _P, _P, _I64, _P]),
+    "hsap_plan_runs": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P, _I64, _P, _P]),
+    "hsap_split_length": (ctypes.c_int32, [_P, _I64, _I32, _I32]),
     "hsap_doc_start": (ctypes.c_int, [_P, _I32, _I64, _P, _P]),
     "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
-    "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
+    "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_lse_merge": (ctypes.c_int, [_I32, _P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P,
@@ -171,19 +172,30 @@ def plan(cu_seqlens, shard: ShardDesc) -> Dict[str, np.ndarray]:
     return {"tiles": tiles[: num.value], "step_offsets": offs, "useful_pairs": pairs[:P]}
 
 
-def plan_runs(shard: ShardDesc, tiles: np.ndarray, major: int) -> Tuple[np.ndarray, np.ndarray]:
-    """hsap_plan_runs.  Returns (sorted_tiles int32 [T, 4], runs int32 [R, 4])."""
+def plan_runs(shard: ShardDesc, tiles: np.ndarray, major: int, max_run_tiles: int = 0):
+    """hsap_plan_runs.  Returns (sorted_tiles int32 [T, 4], runs int32 [R, 4] of (slot, tile, first, count),
+    num_slots)."""
     tiles = np.ascontiguousarray(tiles, dtype=np.int32).reshape(-1, 4)
     sorted_tiles = np.zeros((max(len(tiles), 1), 4), dtype=np.int32)
     num = ctypes.c_int64(0)
-    st = lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), len(tiles), int(major), _ptr(sorted_tiles), None, 0,
-                              ctypes.byref(num))
+    slots = ctypes.c_int32(0)
+    st = lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), len(tiles), int(major), int(max_run_tiles),
+                              _ptr(sorted_tiles), None, 0, ctypes.byref(num), ctypes.byref(slots))
     if st != HSAP_ERR_CAPACITY:
         _check(st)
     runs = np.zeros((max(num.value, 1), 4), dtype=np.int32)
-    _check(lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), len(tiles), int(major), _ptr(sorted_tiles),
-                                _ptr(runs), runs.shape[0], ctypes.byref(num)))
-    return sorted_tiles[: len(tiles)], runs[: num.value]
+    _check(lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), len(tiles), int(major), int(max_run_tiles),
+                                _ptr(sorted_tiles), _ptr(runs), runs.shape[0], ctypes.byref(num),
+                                ctypes.byref(slots)))
+    return sorted_tiles[: len(tiles)], runs[: num.value], slots.value
+
+
+def split_length(shard: ShardDesc, num_tiles: int, heads_q: int, resident_workgroups: int) -> int:
+    """hsap_split_length: max_run_tiles for hsap_plan_runs (0 = no split)."""
+    v = lib().hsap_split_length(ctypes.byref(shard), int(num_tiles), int(heads_q), int(resident_workgroups))
+    if v < 0:
+        raise HsapError(HSAP_ERR_INVALID_ARG, lib().hsap_last_error().decode())
+    return v
 
 
 def plan_into(cu_seqlens: np.ndarray, shard: ShardDesc, tiles_out: np.ndarray, step_offsets_out: np.ndarray,
@@ -197,13 +209,15 @@ def plan_into(cu_seqlens: np.ndarray, shard: ShardDesc, tiles_out: np.ndarray, s
     return num.value
 
 
-def plan_runs_into(shard: ShardDesc, tiles: np.ndarray, num_tiles: int, major: int, sorted_out: np.ndarray,
-                   runs_out: np.ndarray) -> int:
-    """hsap_plan_runs into caller-provided host buffers; returns the run count."""
+def plan_runs_into(shard: ShardDesc, tiles: np.ndarray, num_tiles: int, major: int, max_run_tiles: int,
+                   sorted_out: np.ndarray, runs_out: np.ndarray):
+    """hsap_plan_runs into caller-provided host buffers; returns (run count, slot count)."""
     num = ctypes.c_int64(0)
-    _check(lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), int(num_tiles), int(major), _ptr(sorted_out),
-                                _ptr(runs_out), runs_out.shape[0], ctypes.byref(num)))
-    return num.value
+    slots = ctypes.c_int32(0)
+    _check(lib().hsap_plan_runs(ctypes.byref(shard), _ptr(tiles), int(num_tiles), int(major), int(max_run_tiles),
+                                _ptr(sorted_out), _ptr(runs_out), runs_out.shape[0], ctypes.byref(num),
+                                ctypes.byref(slots)))
+    return num.value, slots.value
 
 
 # ---------------------------------------------------------------------------
@@ -239,11 +253,14 @@ def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev
     _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
     _dev(tiles_dev, "int32", "tiles")
     _dev(runs_dev, "int32", "runs")
-    _dev(o_part, "float32", "o_part", P * n * hq * d)
-    _dev(lse_part, "float32", "lse_part", P * hq * n)
+    _dev(o_part, "float32", "o_part")
+    _dev(lse_part, "float32", "lse_part")
+    slots = o_part.numel() // (n * hq * d)
+    if o_part.numel() != slots * n * hq * d or lse_part.numel() != slots * hq * n or slots < 1:
+        raise ValueError("o_part / lse_part must hold a whole number of [n, Hq, d] / [Hq, n] slots")
     _check(lib().hsap_partial_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(doc_start_dev),
                                        _ptr(tiles_dev), _ptr(runs_dev), runs_dev.numel() // 4, _ptr(o_part),
-                                       _ptr(lse_part), _stream(stream)))
+                                       _ptr(lse_part), int(slots), _stream(stream)))
 
 
 def lse_merge(o_parts: Sequence, lse_parts: Sequence, n: int, heads_q: int, head_dim: int, o_out, lse_out,

@@ -70,7 +70,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   const int run_idx = blockIdx.x / a.hkv;
   const int g = blockIdx.x - run_idx * a.hkv;
   const hsap_run run = a.runs[run_idx];
-  const int c = run.chunk;
+  const int c = a.tiles[run.first].chunk;  // k-major runs are never empty
   const int64_t n = a.geom.n;
   const int64_t krow0 = (int64_t)run.tile * BN;
   const int32_t gk = (int32_t)global_pos(a.geom, c, krow0 + 32 * w + l32);  // this lane's key position
@@ -269,7 +269,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
   const int h = blockIdx.x - run_idx * a.hq;
   const hsap_run run = a.runs[run_idx];
   if (run.count == 0) return;
-  const int c = run.chunk;
+  const int c = a.tiles[run.first].chunk;  // all tiles of a run belong to one chunk
   const int g = h / a.group;
   const int64_t n = a.geom.n;
   const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;

@@ -3,7 +3,8 @@
 // attention equation of the inter-group SP section under the packing mask).
 //
 // Work decomposition: one workgroup per (run, query head).  A run is one
-// (chunk, q-tile) with its listed k-tiles.  The workgroup has WAVES waves;
+// q-tile against some listed k-tiles of one chunk, written to its own
+// partial slot (a long run may be split into several).  The workgroup has WAVES waves;
 // wave w owns 32 query rows, so BM = 32 * WAVES.  Every listed k-tile of BN
 // keys is consumed in steps of KB = 64 keys.
 //
@@ -39,6 +40,7 @@ struct FwdArgs {
   const hsap_run* runs;
   float* o_part;
   float* lse_part;
+  int32_t num_slots;
   Geom geom;
   int32_t shard;
   int32_t hq;
@@ -67,15 +69,17 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   const int run_idx = blockIdx.x / a.hq;  // runs are longest first: long work starts first
   const int h = blockIdx.x - run_idx * a.hq;
   const hsap_run run = a.runs[run_idx];
-  const int c = run.chunk;
+  const int slot = run.slot;  // partial-output slot of this run
+  if (slot < 0 || slot >= a.num_slots) return;
   const int g = h / a.group;
   const int64_t n = a.geom.n;
   const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;  // this lane's query row (shard-local)
 
-  if (run.count == 0) {  // no key of chunk c for this q-tile
-    if (hi == 0) a.lse_part[((int64_t)c * a.hq + h) * n + qrow] = NEG_INF;
+  if (run.count == 0) {  // no key for this q-tile in this slot
+    if (hi == 0) a.lse_part[((int64_t)slot * a.hq + h) * n + qrow] = NEG_INF;
     return;
   }
+  const int c = a.tiles[run.first].chunk;  // all tiles of a run belong to one chunk
 
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
   const int32_t qstart = a.doc_start[gq];
@@ -236,7 +240,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 
   l_run = pair_sum(l_run);
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-  float* op = a.o_part + (((int64_t)c * n + qrow) * a.hq + h) * D + 4 * hi;
+  float* op = a.o_part + (((int64_t)slot * n + qrow) * a.hq + h) * D + 4 * hi;
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
@@ -246,7 +250,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
       *(f32x4*)(op + 32 * mb + 8 * grp) = val;
     }
   if (hi == 0)
-    a.lse_part[((int64_t)c * a.hq + h) * n + qrow] =
+    a.lse_part[((int64_t)slot * a.hq + h) * n + qrow] =
         l_run > 0.f ? (m_run + __log2f(l_run)) * 0.69314718055994530942f : NEG_INF;
 }
 
@@ -266,12 +270,14 @@ using namespace hsap;
 
 extern "C" hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
                                              const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
-                                             int64_t num_runs, float* o_part, float* lse_part, void* hip_stream) {
+                                             int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots,
+                                             void* hip_stream) {
   clear_error();
   Geom geom;
   hsap_status st = check_attn(desc, &geom);
   if (st != HSAP_OK) return st;
   if (num_runs < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_runs < 0");
+  if (num_slots < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_slots < 1");
   if (num_runs == 0) return HSAP_OK;
   if (!q || !k || !v || !doc_start || !tiles || !runs || !o_part || !lse_part)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
@@ -288,6 +294,7 @@ extern "C" hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const v
   a.runs = runs;
   a.o_part = o_part;
   a.lse_part = lse_part;
+  a.num_slots = num_slots;
   a.geom = geom;
   a.shard = desc->shard.shard_id;
   a.hq = desc->heads_q;

@@ -209,7 +209,8 @@ hsap_status hsap_plan(const int32_t* cu, int32_t num_docs, const hsap_shard_desc
 }
 
 hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles, int64_t num_tiles, int32_t major,
-                           hsap_tile* sorted_tiles, hsap_run* runs, int64_t capacity, int64_t* num_runs) {
+                           int32_t max_run_tiles, hsap_tile* sorted_tiles, hsap_run* runs, int64_t capacity,
+                           int64_t* num_runs, int32_t* num_slots) {
   clear_error();
   Geom g;
   hsap_status st = check_shard(shard, &g);
@@ -237,18 +238,36 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
     }
   }
   std::vector<hsap_run> out;
+  int32_t slots = 0;
   if (major == HSAP_MAJOR_Q) {
     if (num_tiles > 0) std::memcpy(sorted_tiles, tiles, sizeof(hsap_tile) * num_tiles);
+    const int64_t max_run = max_run_tiles > 0 ? max_run_tiles : INT64_MAX;
     int64_t i = 0;
+    std::vector<int64_t> first(nq), count(nq);
     while (i < num_tiles) {
       const int32_t c = tiles[i].chunk;
-      // every q-tile of this chunk gets a run, empty or not
+      // per q-tile extent of this chunk's tiles, and the pieces the longest needs
+      int64_t pieces = 1;
       for (int32_t t = 0; t < nq; ++t) {
         int64_t j = i;
         while (j < num_tiles && tiles[j].chunk == c && tiles[j].q_tile == t) ++j;
-        out.push_back(hsap_run{c, t, (int32_t)i, (int32_t)(j - i)});
+        first[t] = i;
+        count[t] = j - i;
+        pieces = std::max<int64_t>(pieces, (count[t] + max_run - 1) / max_run);
         i = j;
       }
+      // every q-tile gets a run in every slot the chunk uses (count 0 where it has nothing there)
+      for (int32_t t = 0; t < nq; ++t) {
+        const int64_t need = std::max<int64_t>(1, (count[t] + max_run - 1) / max_run);
+        int64_t at = first[t];
+        for (int64_t piece = 0; piece < pieces; ++piece) {
+          int64_t len = 0;
+          if (piece < need) len = count[t] / need + (piece < count[t] % need ? 1 : 0);
+          out.push_back(hsap_run{(int32_t)(c + P * piece), t, (int32_t)at, (int32_t)len});
+          at += len;
+        }
+      }
+      slots = std::max<int32_t>(slots, (int32_t)(c + P * (pieces - 1) + 1));
     }
   } else {
     std::vector<int64_t> order(num_tiles);
@@ -266,22 +285,41 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
              sorted_tiles[j].k_tile == sorted_tiles[i].k_tile)
         ++j;
       out.push_back(hsap_run{sorted_tiles[i].chunk, sorted_tiles[i].k_tile, (int32_t)i, (int32_t)(j - i)});
+      slots = std::max<int32_t>(slots, sorted_tiles[i].chunk + 1);
       i = j;
     }
   }
-  // longest first; ties by ring step then tile, so the order is unique
+  // longest first; ties by ring step, tile, then slot, so the order is unique
   std::stable_sort(out.begin(), out.end(), [&](const hsap_run& a, const hsap_run& b) {
     if (a.count != b.count) return a.count > b.count;
-    const int32_t sa = step_of(a.chunk), sb = step_of(b.chunk);
+    const int32_t sa = step_of(a.slot % P), sb = step_of(b.slot % P);
     if (sa != sb) return sa < sb;
-    return a.tile < b.tile;
+    if (a.tile != b.tile) return a.tile < b.tile;
+    return a.slot < b.slot;
   });
   *num_runs = (int64_t)out.size();
+  if (num_slots) *num_slots = slots;
   if (!runs || (int64_t)out.size() > capacity)
     HSAP_FAIL(HSAP_ERR_CAPACITY, "run list needs %lld entries, capacity %lld", (long long)out.size(),
               (long long)capacity);
   std::copy(out.begin(), out.end(), runs);
   return HSAP_OK;
+}
+
+int32_t hsap_split_length(const hsap_shard_desc* shard, int64_t num_tiles, int32_t heads_q,
+                          int32_t resident_workgroups) {
+  clear_error();
+  Geom g;
+  if (check_shard(shard, &g) != HSAP_OK) return -1;
+  if (num_tiles < 0 || heads_q <= 0 || resident_workgroups <= 0) {
+    set_error("bad num_tiles, heads_q or resident_workgroups");
+    return -1;
+  }
+  const int64_t nk = g.n / shard->block_n;
+  const int64_t avg = (num_tiles * heads_q + resident_workgroups - 1) / resident_workgroups;
+  if (nk <= avg) return 0;  // no run can exceed the average load
+  const int64_t len = std::max<int64_t>({avg, 4, (nk + 3) / 4});
+  return len >= nk ? 0 : (int32_t)len;
 }
 
 }  // extern "C"

@@ -3,18 +3,19 @@
 This is call sequencing and buffer allocation only; every step of the path
 runs inside the library:
 
-  plan      hsap_plan (host C++) -> hsap_plan_runs -> upload of the lists,
-            hsap_doc_start (device)
+  plan      hsap_plan (host C++) -> hsap_split_length / hsap_plan_runs ->
+            upload of the lists, hsap_doc_start (device)
   forward   hsap_partial_attn_fwd over the runs (one launch for every chunk,
-            or one launch per ring step), then hsap_lse_merge of the chunks
-            that have tiles
+            or one launch per ring step), then hsap_lse_merge of every slot
+            the runs wrote
   backward  hsap_attn_bwd_preprocess, hsap_partial_attn_bwd (dK/dV over the
             k-major runs, dQ over the forward's q-major runs), and
             hsap_convert_f32_bf16 for the gradients
 
 Tensors follow the library's layouts: the shard's q / dO are [n, Hq, d] in
 its local row order; k / v and the dK / dV accumulators are in sharded order
-[P, n, Hkv, d]; partial outputs are [P, n, Hq, d] fp32 with LSE [P, Hq, n].
+[P, n, Hkv, d]; partial outputs are [slots, n, Hq, d] fp32 with LSE
+[slots, Hq, n], where slot = chunk + P * piece (piece > 0 only for split runs).
 """
 from __future__ import annotations
 
@@ -26,13 +27,25 @@ import torch
 
 from . import _lib as L
 
+# forward workgroups resident per compute unit (two 4-wave workgroups share a CU)
+_FWD_WORKGROUPS_PER_CU = 2
+
+
+def _resident_workgroups(device) -> int:
+    return _FWD_WORKGROUPS_PER_CU * torch.cuda.get_device_properties(device).multi_processor_count
+
 
 class ShardAttention:
-    """Plan and run one shard of packed, document-masked causal attention."""
+    """Plan and run one shard of packed, document-masked causal attention.
+
+    ``max_run_tiles``: longest q-major run before it is split into pieces
+    (split-K over partial slots); None picks it from the plan and the number
+    of resident workgroups (hsap_split_length), 0 disables splitting.
+    """
 
     def __init__(self, cu_seqlens, total_tokens: int, sp_degree: int, layout, shard_id: int, heads_q: int,
                  heads_kv: int, head_dim: int, block_m: int = 128, block_n: int = 128,
-                 softmax_scale: Optional[float] = None, device: str = "cuda"):
+                 softmax_scale: Optional[float] = None, device: str = "cuda", max_run_tiles: Optional[int] = None):
         self.device = torch.device(device)
         self.cu_host = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
         self.N = int(total_tokens)
@@ -42,7 +55,13 @@ class ShardAttention:
         self.scale = float(softmax_scale) if softmax_scale is not None else 1.0 / math.sqrt(head_dim)
         self.shard = L.shard_desc(total_tokens, sp_degree, layout, shard_id, block_m, block_n)
         self.desc = L.attn_desc(self.shard, heads_q, heads_kv, head_dim, self.scale)
+        self.max_run_tiles = max_run_tiles
         self.planned = False
+
+    def _split(self, num_tiles: int) -> int:
+        if self.max_run_tiles is not None:
+            return int(self.max_run_tiles)
+        return L.split_length(self.shard, num_tiles, self.hq, _resident_workgroups(self.device))
 
     # ------------------------------------------------------------------ plan
     def plan(self, backward: bool = False) -> Dict:
@@ -52,19 +71,20 @@ class ShardAttention:
         self.step_offsets = p["step_offsets"]
         self.useful_pairs = p["useful_pairs"]
         self.chunks = [(self.shard.shard_id - s) % self.P for s in range(self.P)]
-        self.present = [self.chunks[s] for s in range(self.P) if self.step_offsets[s + 1] > self.step_offsets[s]]
-        tiles_q, runs_q = L.plan_runs(self.shard, self.tiles, L.MAJOR_Q)
+        self.split = self._split(len(self.tiles))
+        tiles_q, runs_q, self.num_slots = L.plan_runs(self.shard, self.tiles, L.MAJOR_Q, self.split)
         self.runs_q_host = runs_q
+        self.present = sorted(set(runs_q[:, 0].tolist()))
         dev = self.device
-        self.tiles_q = torch.from_numpy(tiles_q.reshape(-1)).to(dev, non_blocking=False)
+        self.tiles_q = torch.from_numpy(tiles_q.reshape(-1)).to(dev)
         self.runs_q = torch.from_numpy(runs_q.reshape(-1)).to(dev)
         # per ring step run lists, for executing chunk by chunk
         self.runs_q_step = []
         for c in self.chunks:
-            sel = runs_q[runs_q[:, 0] == c]
+            sel = runs_q[runs_q[:, 0] % self.P == c]
             self.runs_q_step.append(torch.from_numpy(np.ascontiguousarray(sel).reshape(-1)).to(dev) if len(sel) else None)
         if backward:
-            tiles_k, runs_k = L.plan_runs(self.shard, self.tiles, L.MAJOR_K)
+            tiles_k, runs_k, _ = L.plan_runs(self.shard, self.tiles, L.MAJOR_K)
             self.tiles_k = torch.from_numpy(tiles_k.reshape(-1)).to(dev)
             self.runs_k = torch.from_numpy(runs_k.reshape(-1)).to(dev)
         self.cu_dev = torch.from_numpy(self.cu_host).to(dev)
@@ -77,12 +97,16 @@ class ShardAttention:
     def total_useful_pairs(self) -> int:
         return int(self.useful_pairs.sum())
 
+    @property
+    def chunks_present(self) -> List[int]:
+        return sorted(set(s % self.P for s in self.present))
+
     # ---------------------------------------------------------- allocation
     def alloc_forward(self) -> Dict[str, torch.Tensor]:
         dev = self.device
         return {
-            "o_part": torch.empty(self.P, self.n, self.hq, self.d, dtype=torch.float32, device=dev),
-            "lse_part": torch.empty(self.P, self.hq, self.n, dtype=torch.float32, device=dev),
+            "o_part": torch.empty(self.num_slots, self.n, self.hq, self.d, dtype=torch.float32, device=dev),
+            "lse_part": torch.empty(self.num_slots, self.hq, self.n, dtype=torch.float32, device=dev),
             "o": torch.empty(self.n, self.hq, self.d, dtype=torch.bfloat16, device=dev),
             "lse": torch.empty(self.hq, self.n, dtype=torch.float32, device=dev),
         }
@@ -119,7 +143,7 @@ class ShardAttention:
         else:
             L.partial_attn_fwd(self.desc, q, k, v, self.doc_start, self.tiles_q, self.runs_q, bufs["o_part"],
                                bufs["lse_part"])
-        L.lse_merge([bufs["o_part"][c] for c in self.present], [bufs["lse_part"][c] for c in self.present],
+        L.lse_merge([bufs["o_part"][s] for s in self.present], [bufs["lse_part"][s] for s in self.present],
                     self.n, self.hq, self.d, bufs["o"], bufs["lse"])
 
     # ------------------------------------------------------------- backward
@@ -128,20 +152,24 @@ class ShardAttention:
         """dQ for the shard and dK/dV contributions to every chunk, as bf16."""
         if not hasattr(self, "runs_k"):
             raise RuntimeError("call plan(backward=True) first")
+        present = self.chunks_present
         if zero:
             bufs["dq_acc"].zero_()
-            bufs["dk_acc"].zero_()
-            bufs["dv_acc"].zero_()
+            for c in present:
+                bufs["dk_acc"][c].zero_()
+                bufs["dv_acc"][c].zero_()
         L.attn_bwd_preprocess(fwd["o"], d_o, self.n, self.hq, self.d, bufs["delta"])
         L.partial_attn_bwd(self.desc, q, k, v, d_o, fwd["lse"], bufs["delta"], self.doc_start, self.tiles_k,
                            self.runs_k, self.tiles_q, self.runs_q, bufs["dq_acc"], bufs["dk_acc"], bufs["dv_acc"])
         L.convert_f32_bf16(bufs["dq_acc"], bufs["dq"])
-        # only chunks with tiles receive gradient; the others stay as zeroed
-        for c in (self.present if zero else range(self.P)):
-            L.convert_f32_bf16(bufs["dk_acc"][c], bufs["dk"][c])
-            L.convert_f32_bf16(bufs["dv_acc"][c], bufs["dv"][c])
-        if zero:
-            for c in set(range(self.P)) - set(self.present):
+        # only chunks with tiles receive gradient; the others are zero
+        for c in range(self.P):
+            if c in present:
+                L.convert_f32_bf16(bufs["dk_acc"][c], bufs["dk"][c])
+                L.convert_f32_bf16(bufs["dv_acc"][c], bufs["dv"][c])
+            elif zero:
+                bufs["dk_acc"][c].zero_()
+                bufs["dv_acc"][c].zero_()
                 bufs["dk"][c].zero_()
                 bufs["dv"][c].zero_()
 
@@ -155,7 +183,9 @@ class PlanPipeline:
     the event recorded behind its last copy has completed, so the host can
     plan step i+1 while the GPU still runs step i.  Device list buffers are
     single: stream order puts each step's upload after the previous step's
-    kernels.  After ``step`` the ShardAttention's lists point at the new plan.
+    kernels.  The split length is fixed when the pipeline is built (partial
+    buffers are sized for it); after ``step`` the ShardAttention's lists point
+    at the new plan.
     """
 
     def __init__(self, sa: ShardAttention, backward: bool = False):
@@ -164,7 +194,12 @@ class PlanPipeline:
         s = sa.shard
         nq, nk = sa.n // s.block_m, sa.n // s.block_n
         self.cap_tiles = sa.P * nq * nk
-        cap_rq, cap_rk = sa.P * nq, sa.P * nk
+        first = L.plan(sa.cu_host, s)
+        self.split = sa._split(len(first["tiles"]))
+        pieces = -(-nk // self.split) if self.split > 0 else 1
+        sa.split = self.split
+        sa.num_slots = sa.P * pieces
+        cap_rq, cap_rk = sa.P * nq * pieces, sa.P * nk
         dev = sa.device
 
         def pinned(count):
@@ -201,13 +236,13 @@ class PlanPipeline:
         T = L.plan_into(cu, sa.shard, tiles, self.offs, self.pairs)
         sorted_q = slot["sorted_q"].numpy().reshape(-1, 4)
         runs_q = slot["runs_q"].numpy().reshape(-1, 4)
-        R = L.plan_runs_into(sa.shard, tiles, T, L.MAJOR_Q, sorted_q, runs_q)
+        R, _ = L.plan_runs_into(sa.shard, tiles, T, L.MAJOR_Q, self.split, sorted_q, runs_q)
         self.dev_tiles_q[: T * 4].copy_(slot["sorted_q"][: T * 4], non_blocking=True)
         self.dev_runs_q[: R * 4].copy_(slot["runs_q"][: R * 4], non_blocking=True)
         if self.backward:
             sorted_k = slot["sorted_k"].numpy().reshape(-1, 4)
             runs_k = slot["runs_k"].numpy().reshape(-1, 4)
-            RK = L.plan_runs_into(sa.shard, tiles, T, L.MAJOR_K, sorted_k, runs_k)
+            RK, _ = L.plan_runs_into(sa.shard, tiles, T, L.MAJOR_K, 0, sorted_k, runs_k)
             self.dev_tiles_k[: T * 4].copy_(slot["sorted_k"][: T * 4], non_blocking=True)
             self.dev_runs_k[: RK * 4].copy_(slot["runs_k"][: RK * 4], non_blocking=True)
             sa.tiles_k = self.dev_tiles_k[: T * 4]
@@ -220,7 +255,7 @@ class PlanPipeline:
         sa.step_offsets = self.offs.copy()
         sa.useful_pairs = self.pairs.copy()
         sa.chunks = [(sa.shard.shard_id - st) % sa.P for st in range(sa.P)]
-        sa.present = [sa.chunks[st] for st in range(sa.P) if self.offs[st + 1] > self.offs[st]]
+        sa.present = sorted(set(runs_q[:R, 0].tolist()))
         sa.planned = True
 
 

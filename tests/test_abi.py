@@ -100,7 +100,7 @@ def test_plan_runs_rejects_non_canonical_list():
     tiles = p["tiles"].copy()
     tiles[[0, 1]] = tiles[[1, 0]]
     with pytest.raises(L.HsapError) as e:
-        L.plan_runs(d, tiles, L.MAJOR_Q)
+        L.plan_runs(d, tiles, L.MAJOR_Q, 0)
     assert e.value.status == L.HSAP_ERR_INVALID_ARG
 
 
@@ -124,7 +124,7 @@ def test_forward_validates_before_launch(over, code):
     lib = L.lib()
     d = _attn_desc(**over)
     fake = ctypes.c_void_p(4096)     # never dereferenced: validation fails first
-    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, None)
+    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
     assert st == code, lib.hsap_last_error().decode()
 
 
@@ -132,12 +132,14 @@ def test_forward_rejects_null_and_misaligned():
     lib = L.lib()
     d = _attn_desc()
     fake = ctypes.c_void_p(4096)
-    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), None, fake, fake, fake, fake, fake, 1, fake, fake, None)
+    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), None, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
     assert st == L.HSAP_ERR_INVALID_ARG
     odd = ctypes.c_void_p(4098)
-    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), odd, fake, fake, fake, fake, fake, 1, fake, fake, None)
+    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), odd, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
     assert st == L.HSAP_ERR_INVALID_ARG
-    assert lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 0, fake, fake, None) == 0
+    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 0, None)
+    assert st == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 0, fake, fake, 1, None) == 0
 
 
 def test_backward_validates_before_launch():

@@ -64,6 +64,23 @@ def test_forward_small(case):
         assert np.array_equal(gpu2["o"], gpu["o"]) and np.array_equal(gpu2["lse"], gpu["lse"])
 
 
+@pytest.mark.parametrize("split", [0, 1, 3])
+def test_forward_split_runs(split):
+    # long runs cut into pieces of at most `split` tiles (0: never) give the same result
+    N, P = 4096, 2
+    lengths = [3000, 40, 1, 1055]
+    cu = np.concatenate([[0], np.cumsum(lengths)])
+    c = Case(cu, N, P, "contiguous", 1, 4, 2, 128, 128, 128, seed=9)
+    gpu = c.run_gpu(max_run_tiles=split)
+    ref = c.run_oracle()
+    compare_forward(gpu, ref)
+    sa = gpu["sa"]
+    if split:
+        assert sa.num_slots > P and len(sa.present) > len(sa.chunks_present)
+    else:
+        assert len(sa.present) == len(sa.chunks_present)
+
+
 def test_forward_one_token_documents_exact():
     # a one-token document attends only to itself: O equals its V row bit for bit
     N, P = 1024, 2

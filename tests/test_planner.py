@@ -86,31 +86,49 @@ def test_pair_identity_all_shards():
     assert total == int(np.sum(lengths * (lengths + 1) // 2))
 
 
-def _runs_ok(shard, tiles, sorted_tiles, runs, major):
-    nq = shard.total_tokens // shard.sp_degree // shard.block_m
+def _runs_ok(shard, tiles, sorted_tiles, runs, major, split=0, num_slots=None):
+    P = shard.sp_degree
+    nq = shard.total_tokens // P // shard.block_m
     covered = np.zeros(len(tiles), dtype=int)
-    for ch, t, first, count in runs:
+    for slot, t, first, count in runs:
         seg = sorted_tiles[first:first + count]
-        assert np.all(seg[:, 0] == ch)
+        assert np.all(seg[:, 0] == slot % P)              # a run's tiles belong to its slot's chunk
         assert np.all(seg[:, 1 if major == L.MAJOR_Q else 2] == t)
+        if split and major == L.MAJOR_Q:
+            assert count <= split
         covered[first:first + count] += 1
     assert np.all(covered == 1)
     counts = runs[:, 3]
     assert np.all(np.diff(counts) <= 0)           # longest first
-    # sorted_tiles is a permutation of tiles
     key = lambda a: sorted(map(tuple, a.tolist()))
-    assert key(sorted_tiles) == key(tiles)
+    assert key(sorted_tiles) == key(tiles)        # sorted_tiles is a permutation of tiles
     if major == L.MAJOR_Q:
-        present = sorted(set(tiles[:, 0].tolist()))
-        assert len(runs) == len(present) * nq       # every q-tile of every chunk with tiles
+        # every slot in use has exactly one run per q-tile
+        slots = sorted(set(runs[:, 0].tolist()))
+        assert num_slots == max(slots) + 1
+        for s in slots:
+            assert sorted(runs[runs[:, 0] == s][:, 1].tolist()) == list(range(nq))
+        assert set(s % P for s in slots) == set(tiles[:, 0].tolist())
+    else:
+        assert np.all(runs[:, 0] == sorted_tiles[runs[:, 2], 0])
 
 
 @pytest.mark.parametrize("name", ["c2", "c3", "c5m"])
-def test_runs(name):
+@pytest.mark.parametrize("split", [0, 1, 5])
+def test_runs(name, split):
     w = make_workload(name)
     r = w.shard if w.shard is not None else 1
     d = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, r, w.block_m, w.block_n)
     tiles = L.plan(w.cu_seqlens, d)["tiles"]
     for major in (L.MAJOR_Q, L.MAJOR_K):
-        sorted_tiles, runs = L.plan_runs(d, tiles, major)
-        _runs_ok(d, tiles, sorted_tiles, runs, major)
+        sorted_tiles, runs, slots = L.plan_runs(d, tiles, major, split)
+        _runs_ok(d, tiles, sorted_tiles, runs, major, split, slots)
+
+
+def test_split_length():
+    d = L.shard_desc(32768, 8, "contiguous", 3, 128, 128)       # 32 k-tiles per chunk
+    assert L.split_length(d, 407, 32, 512) == 26                # average 25.4 tiles per workgroup, rounded up
+    assert L.split_length(d, 25000, 8, 512) == 0                # every run shorter than the average load
+    assert L.split_length(d, 10, 1, 512) == 8                   # floor: a quarter of a chunk's k-tiles
+    with pytest.raises(L.HsapError):
+        L.split_length(d, 10, 0, 512)
