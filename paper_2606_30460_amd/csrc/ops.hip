@@ -9,10 +9,12 @@ namespace hsap {
 // ---------------------------------------------------------------------------
 // LSE merge (online-softmax combination of the ring's partial results)
 //
-// Thread layout: D/4 consecutive lanes own one (row, head) and 4 consecutive
-// d each, so a (row, head) of a partial is one contiguous 4*D-byte read.
-// Each lane reads the partials' LSE values itself (same address across the
-// D/4 lanes: one broadcast), and skips the O read of parts at -inf.
+// Thread layout: D/4 consecutive lanes own one (row, head) item and 4
+// consecutive d each, so an item of a partial is one contiguous 4*D-byte
+// read.  Each thread carries ITEMS items spaced a grid apart and issues the
+// LSE loads of all of them, then the O loads of all of them, before using
+// any: the merge is HBM-bound and needs many bytes in flight.  Parts whose
+// LSE is -inf are never read.
 // ---------------------------------------------------------------------------
 struct MergeArgs {
   const float* o[HSAP_MAX_MERGE_PARTS];
@@ -24,37 +26,69 @@ struct MergeArgs {
   float* lse_out;
 };
 
-template <int D>
+template <int D, int ITEMS>
 __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
   constexpr int TPR = D / 4;
   constexpr float NEG_INF = -__builtin_inff();
   constexpr float LOG2E = 1.44269504088896340736f;
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t rh = gid / TPR;  // rh = row * hq + head
-  const int part = (int)(gid % TPR);
-  if (rh >= a.n * a.hq) return;
-  const int64_t row = rh / a.hq;
-  const int h = (int)(rh - row * a.hq);
-  const int64_t li = (int64_t)h * a.n + row;
-  float mx = NEG_INF;
-  for (int p = 0; p < a.num_parts; ++p) mx = fmaxf(mx, a.lse[p][li]);
-  f32x4 acc{0.f, 0.f, 0.f, 0.f};
-  float L = NEG_INF;
-  if (mx != NEG_INF) {
-    float sum = 0.f;
-    for (int p = 0; p < a.num_parts; ++p) sum += fast_exp2((a.lse[p][li] - mx) * LOG2E);
-    L = mx + __logf(sum);
-    for (int p = 0; p < a.num_parts; ++p) {
-      const float lp = a.lse[p][li];
-      if (lp == NEG_INF) continue;
-      const float wgt = fast_exp2((lp - L) * LOG2E);
-      const f32x4 x = *(const f32x4*)(a.o[p] + rh * D + 4 * part);
-      acc += wgt * x;
+  constexpr float LN2 = 0.69314718055994530942f;
+  const int64_t items = a.n * a.hq;
+  const int part = (int)(threadIdx.x % TPR);
+  const int64_t stride = (int64_t)gridDim.x * (256 / TPR);
+  const int64_t base = ((int64_t)blockIdx.x * 256 + threadIdx.x) / TPR;
+  int64_t li[ITEMS], rh[ITEMS];
+  bool live[ITEMS];
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    rh[it] = base + it * stride;  // rh = row * hq + head
+    live[it] = rh[it] < items;
+    const int64_t row = rh[it] / a.hq;
+    li[it] = (int64_t)(rh[it] - row * a.hq) * a.n + row;  // index into [Hq, n]
+  }
+  // pass 1: running max and sum of 2^(LSE*log2e) over the parts (log2 domain)
+  float mx[ITEMS], sum[ITEMS];
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    mx[it] = NEG_INF;
+    sum[it] = 0.f;
+  }
+  for (int p = 0; p < a.num_parts; ++p) {
+    float l[ITEMS];
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) l[it] = live[it] ? a.lse[p][li[it]] * LOG2E : NEG_INF;
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const float m_new = fmaxf(mx[it], l[it]);
+      if (m_new != NEG_INF) sum[it] = sum[it] * fast_exp2(mx[it] - m_new) + fast_exp2(l[it] - m_new);
+      mx[it] = m_new;
     }
   }
-  const bf16x4 out{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
-  *(bf16x4*)(a.o_out + rh * D + 4 * part) = out;
-  if (part == 0) a.lse_out[li] = L;
+  float L2[ITEMS];  // merged LSE in log2 units
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) L2[it] = mx[it] == NEG_INF ? NEG_INF : mx[it] + __log2f(sum[it]);
+  // pass 2: weighted sum of the finite parts
+  f32x4 acc[ITEMS];
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) acc[it] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < a.num_parts; ++p) {
+    float wgt[ITEMS];
+    f32x4 x[ITEMS];
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const float l = live[it] ? a.lse[p][li[it]] * LOG2E : NEG_INF;
+      wgt[it] = l == NEG_INF ? 0.f : fast_exp2(l - L2[it]);
+      x[it] = wgt[it] > 0.f ? *(const f32x4*)(a.o[p] + rh[it] * D + 4 * part) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) acc[it] += wgt[it] * x[it];
+  }
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    if (!live[it]) continue;
+    const bf16x4 out{(__bf16)acc[it][0], (__bf16)acc[it][1], (__bf16)acc[it][2], (__bf16)acc[it][3]};
+    *(bf16x4*)(a.o_out + rh[it] * D + 4 * part) = out;
+    if (part == 0) a.lse_out[li[it]] = L2[it] == NEG_INF ? NEG_INF : L2[it] * LN2;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -173,12 +207,13 @@ hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const
   a.n = n;
   a.o_out = (__bf16*)o_out;
   a.lse_out = lse_out;
+  constexpr int ITEMS = 4;
   const int64_t threads = n * heads_q * (head_dim / 4);
-  const int64_t blocks = (threads + 255) / 256;
+  const int64_t blocks = (threads + 256 * ITEMS - 1) / (256 * ITEMS);
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "problem too large");
   hipStream_t s = (hipStream_t)hip_stream;
-  if (head_dim == 128) hipLaunchKernelGGL(lse_merge_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(lse_merge_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  if (head_dim == 128) hipLaunchKernelGGL((lse_merge_kernel<128, ITEMS>), dim3((unsigned)blocks), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((lse_merge_kernel<64, ITEMS>), dim3((unsigned)blocks), dim3(256), 0, s, a);
   return check_launch("lse_merge");
 }
 
