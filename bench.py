@@ -115,6 +115,22 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     merge_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
     bwd_ms = np.array([e[3].elapsed_time(e[4]) for e in events]) if bwd else None
 
+    # the fused forward (partials and merge in one pass), timed on the same inputs
+    fused_ms = None
+    if not bwd:
+        sa.plan()
+        fo = {"o": torch.empty_like(fwd["o"]), "lse": torch.empty_like(fwd["lse"])}
+        for _ in range(3):
+            sa.forward_fused(q, k, v, fo)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(steps):
+            sa.forward_fused(q, k, v, fo)
+        ev[1].record()
+        torch.cuda.synchronize()
+        fused_ms = ev[0].elapsed_time(ev[1]) / steps
+
     # planner host time (not overlapped), for reference
     t1 = time.perf_counter()
     reps = 20
@@ -150,6 +166,8 @@ def measure(name: str, steps: int, warmup: int, backward=None):
         "merge_gbs": merge_bytes / (merge_ms.mean() * 1e-3) / 1e9,
         "planner_host_ms": plan_ms,
     }
+    if fused_ms is not None:
+        res.update({"fused_fwd_kernel_ms": fused_ms, "fused_fwd_tflops": fwd_flops / (fused_ms * 1e-3) / 1e12})
     if bwd:
         res.update({"bwd_kernel_ms_mean": float(bwd_ms.mean()), "bwd_kernel_ms_median": float(np.median(bwd_ms)),
                     "bwd_kernel_tflops": bwd_flops / (bwd_ms.mean() * 1e-3) / 1e12})

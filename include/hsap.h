@@ -63,9 +63,11 @@ typedef enum { HSAP_LAYOUT_CONTIGUOUS = 0, HSAP_LAYOUT_ZIGZAG = 1 } hsap_layout;
 typedef enum { HSAP_TILE_FULL = 0, HSAP_TILE_MASKED = 1 } hsap_tile_kind;
 
 /* Which tile index groups a run: HSAP_MAJOR_Q groups the tiles of one
- * (chunk, q_tile) -- the forward's unit of work; HSAP_MAJOR_K groups the tiles
- * of one (chunk, k_tile) -- the backward's. */
-typedef enum { HSAP_MAJOR_Q = 0, HSAP_MAJOR_K = 1 } hsap_major;
+ * (chunk, q_tile) -- the partial forward's unit of work; HSAP_MAJOR_K groups
+ * the tiles of one (chunk, k_tile) -- the backward's; HSAP_MAJOR_Q_ALL groups
+ * every tile of one q_tile across all chunks, in ring order -- the fused
+ * forward's. */
+typedef enum { HSAP_MAJOR_Q = 0, HSAP_MAJOR_K = 1, HSAP_MAJOR_Q_ALL = 2 } hsap_major;
 
 /* One non-empty (q-tile, k-tile) block: 16-byte POD.  q_tile counts BM-row
  * tiles of the shard's local rows, k_tile counts BN-row tiles of chunk
@@ -159,6 +161,10 @@ hsap_status hsap_plan(const int32_t* cu_seqlens, int32_t num_docs, const hsap_sh
  *                HSAP_MAJOR_K: one run per (chunk, k_tile) that has tiles,
  *                slot = chunk; sorted_tiles is ordered by ring step, k_tile,
  *                q_tile.  max_run_tiles is ignored.
+ *                HSAP_MAJOR_Q_ALL: one run per q_tile over all chunks (every
+ *                q_tile has one: a query always attends itself), slot = 0;
+ *                sorted_tiles is ordered by q_tile, ring step, k_tile.
+ *                max_run_tiles is ignored.
  *   max_run_tiles  longest q-major run; <= 0 means no splitting.
  *   sorted_tiles host [num_tiles] out: the tiles the runs index.
  *   runs         host [capacity] or NULL, out: ordered by count descending
@@ -232,6 +238,25 @@ hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, con
                                   const void* v, const int32_t* doc_start, const hsap_tile* tiles,
                                   const hsap_run* runs, int64_t num_runs, float* o_part,
                                   float* lse_part, int32_t num_slots, void* hip_stream);
+
+/*
+ * hsap_attn_fwd_fused -- the partial forward and the merge in one pass: for
+ * every q_tile, the queries against the listed k-tiles of every chunk in
+ * ring order, with one online softmax carried across the chunks (the ring's
+ * online accumulation), writing the final output directly.  This is the
+ * fusion of the copy and rescale operations into the attention computation
+ * that the paper's Limitations section proposes as future work.
+ *
+ *   desc, q, k, v, doc_start  as for hsap_partial_attn_fwd (same supported
+ *              shapes).
+ *   tiles, runs, num_runs  device lists from hsap_plan_runs(MAJOR_Q_ALL).
+ *   o_out      device bf16 [n, Hq, d] (round to nearest even).
+ *   lse_out    device fp32 [Hq, n].
+ *   Rows of q-tiles outside the passed runs are untouched.
+ */
+hsap_status hsap_attn_fwd_fused(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
+                                int64_t num_runs, void* o_out, float* lse_out, void* hip_stream);
 
 /*
  * hsap_lse_merge -- online-softmax combination of partial results (the ring's

@@ -10,6 +10,7 @@ from ._lib import (  # noqa: F401
     LIB_PATH,
     MAJOR_K,
     MAJOR_Q,
+    MAJOR_Q_ALL,
     TILE_FULL,
     TILE_MASKED,
     AttnDesc,
@@ -17,6 +18,7 @@ from ._lib import (  # noqa: F401
     ShardDesc,
     attn_bwd_preprocess,
     attn_desc,
+    attn_fwd_fused,
     convert_f32_bf16,
     doc_start,
     lib,

@@ -29,12 +29,13 @@ TILE_FULL = 0
 TILE_MASKED = 1
 MAJOR_Q = 0
 MAJOR_K = 1
+MAJOR_Q_ALL = 2
 MAX_MERGE_PARTS = 64
 
 # Every symbol include/hsap.h declares.
 EXPORTED = (
     "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_doc_start",
-    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
+    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
     "hsap_partial_attn_bwd", "hsap_convert_f32_bf16",
 )
 
@@ -69,6 +70,7 @@ _SIG = {
     "hsap_doc_start": (ctypes.c_int, [_P, _I32, _I64, _P, _P]),
     "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
     "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
+    "hsap_attn_fwd_fused": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
     "hsap_lse_merge": (ctypes.c_int, [_I32, _P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P,
@@ -261,6 +263,24 @@ def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev
     _check(lib().hsap_partial_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(doc_start_dev),
                                        _ptr(tiles_dev), _ptr(runs_dev), runs_dev.numel() // 4, _ptr(o_part),
                                        _ptr(lse_part), int(slots), _stream(stream)))
+
+
+def attn_fwd_fused(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev, o_out, lse_out, stream=None) -> None:
+    """hsap_attn_fwd_fused over MAJOR_Q_ALL runs: final bf16 O and LSE in one pass."""
+    s = desc.shard
+    n = s.total_tokens // s.sp_degree
+    hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
+    _dev(q, "bfloat16", "q", n * hq * d)
+    _dev(k, "bfloat16", "k", P * n * hkv * d)
+    _dev(v, "bfloat16", "v", P * n * hkv * d)
+    _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
+    _dev(tiles_dev, "int32", "tiles")
+    _dev(runs_dev, "int32", "runs")
+    _dev(o_out, "bfloat16", "o_out", n * hq * d)
+    _dev(lse_out, "float32", "lse_out", hq * n)
+    _check(lib().hsap_attn_fwd_fused(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(doc_start_dev),
+                                     _ptr(tiles_dev), _ptr(runs_dev), runs_dev.numel() // 4, _ptr(o_out),
+                                     _ptr(lse_out), _stream(stream)))
 
 
 def lse_merge(o_parts: Sequence, lse_parts: Sequence, n: int, heads_q: int, head_dim: int, o_out, lse_out,

@@ -41,6 +41,8 @@ struct FwdArgs {
   float* o_part;
   float* lse_part;
   int32_t num_slots;
+  __bf16* o_out;    // fused forward: final output [n, Hq, d]
+  float* lse_out;   // fused forward: final LSE [Hq, n]
   Geom geom;
   int32_t shard;
   int32_t hq;
@@ -49,7 +51,7 @@ struct FwdArgs {
   float scale_log2;
 };
 
-template <int D, int BN, int WAVES>
+template <int D, int BN, int WAVES, bool FUSED>
 __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   constexpr int KB = 64;                     // keys per step
   constexpr int SUBS = BN / KB;              // steps per listed k-tile
@@ -69,17 +71,23 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   const int run_idx = blockIdx.x / a.hq;  // runs are longest first: long work starts first
   const int h = blockIdx.x - run_idx * a.hq;
   const hsap_run run = a.runs[run_idx];
-  const int slot = run.slot;  // partial-output slot of this run
-  if (slot < 0 || slot >= a.num_slots) return;
+  const int slot = run.slot;  // partial-output slot of this run (partial forward)
+  if (!FUSED && (slot < 0 || slot >= a.num_slots)) return;
   const int g = h / a.group;
   const int64_t n = a.geom.n;
   const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;  // this lane's query row (shard-local)
 
-  if (run.count == 0) {  // no key for this q-tile in this slot
-    if (hi == 0) a.lse_part[((int64_t)slot * a.hq + h) * n + qrow] = NEG_INF;
+  if (run.count == 0) {  // no key for this q-tile in this run
+    if (FUSED) {
+      bf16x4* op = (bf16x4*)(a.o_out + (qrow * a.hq + h) * D + 4 * hi);
+#pragma unroll
+      for (int e = 0; e < D / 8; ++e) op[2 * e] = bf16x4{};
+      if (hi == 0) a.lse_out[(int64_t)h * n + qrow] = NEG_INF;
+    } else if (hi == 0) {
+      a.lse_part[((int64_t)slot * a.hq + h) * n + qrow] = NEG_INF;
+    }
     return;
   }
-  const int c = a.tiles[run.first].chunk;  // all tiles of a run belong to one chunk
 
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
   const int32_t qstart = a.doc_start[gq];
@@ -91,11 +99,16 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
   }
   const int64_t rstride = (int64_t)a.hkv * D;
-  const __bf16* kbase = a.k + ((int64_t)c * n * a.hkv + g) * D;
-  const __bf16* vbase = a.v + ((int64_t)c * n * a.hkv + g) * D;
   const int total = run.count * SUBS;
   auto tile_at = [&](int s) { return a.tiles[run.first + s / SUBS]; };
+  // first K/V row of step s of tile t in the sharded buffers (chunk t.chunk, head g)
   auto step_row0 = [&](const hsap_tile& t, int s) { return (int64_t)t.k_tile * BN + (s % SUBS) * KB; };
+  // a partial run stays in one chunk, so its base is fixed; a fused run changes chunk between tiles
+  const int64_t run_base = FUSED ? 0 : (((int64_t)a.tiles[run.first].chunk * n) * a.hkv + g) * D;
+  auto step_off = [&](const hsap_tile& t, int s) {
+    if (FUSED) return (((int64_t)t.chunk * n + step_row0(t, s)) * a.hkv + g) * D;
+    return run_base + step_row0(t, s) * rstride;
+  };
 
   // staging: thread t moves chunks t, t + NT, ... of a step's [KB][D] tile
   int32_t goff[PER_T], koff[PER_T], voff[PER_T];
@@ -107,13 +120,13 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     voff[i] = row * VS + cc * 8;
   }
   bf16x8 kreg[PER_T], vreg[PER_T];
-  auto load_k = [&](int64_t row0) {
-    const __bf16* src = kbase + row0 * rstride;
+  auto load_k = [&](int64_t off) {
+    const __bf16* src = a.k + off;
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) kreg[i] = *(const bf16x8*)(src + goff[i]);
   };
-  auto load_v = [&](int64_t row0) {
-    const __bf16* src = vbase + row0 * rstride;
+  auto load_v = [&](int64_t off) {
+    const __bf16* src = a.v + off;
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) vreg[i] = *(const bf16x8*)(src + goff[i]);
   };
@@ -144,6 +157,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   const int tr_row = 4 * hi + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
+  constexpr int MB_OUT = D / 32;
   float m_run = NEG_INF, l_run = 0.f;
   f32x16 o[D / 32];
 #pragma unroll
@@ -156,13 +170,13 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   // (last read in iteration s - 1) are free to refill during iteration s; one
   // barrier per iteration orders the refills against the next iteration's
   // reads.
-  hsap_tile t_cur = tile_at(0);
-  load_k(step_row0(t_cur, 0));
+  const hsap_tile t_first = tile_at(0);
+  load_k(step_off(t_first, 0));
   store_k(0);
-  load_v(step_row0(t_cur, 0));
+  load_v(step_off(t_first, 0));
   store_v(0);
   if (total > 1) {
-    load_k(step_row0(tile_at(1), 1));
+    load_k(step_off(tile_at(1), 1));
     store_k(1);
   }
   __syncthreads();
@@ -172,14 +186,14 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 
   for (int s = 0; s < total; ++s) {
     const hsap_tile tile = tile_at(s);
-    if (s + 2 < total) load_k(step_row0(tile_at(s + 2), s + 2));
-    if (s + 1 < total) load_v(step_row0(tile_at(s + 1), s + 1));
+    if (s + 2 < total) load_k(step_off(tile_at(s + 2), s + 2));
+    if (s + 1 < total) load_v(step_off(tile_at(s + 1), s + 1));
     // scores of the next step: independent of this step's softmax
     f32x16 sn[KB / 32];
     if (s + 1 < total) scores((s + 1) & 1, sn);
 
     if (tile.kind == HSAP_TILE_MASKED) {
-      const int32_t rel0 = (int32_t)global_pos(a.geom, c, step_row0(tile, s)) - qstart;
+      const int32_t rel0 = (int32_t)global_pos(a.geom, tile.chunk, step_row0(tile, s)) - qstart;
 #pragma unroll
       for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
@@ -240,28 +254,85 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 
   l_run = pair_sum(l_run);
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-  float* op = a.o_part + (((int64_t)slot * n + qrow) * a.hq + h) * D + 4 * hi;
+  const float lse = l_run > 0.f ? (m_run + __log2f(l_run)) * 0.69314718055994530942f : NEG_INF;
+  if (FUSED) {
+    // final output: this lane's query, d = 32 mb + 8 grp + 4 hi + 0..3
+    __bf16* op = a.o_out + (qrow * a.hq + h) * D + 4 * hi;
 #pragma unroll
-  for (int mb = 0; mb < D / 32; ++mb)
+    for (int mb = 0; mb < MB_OUT; ++mb)
 #pragma unroll
-    for (int grp = 0; grp < 4; ++grp) {
-      const f32x4 val{o[mb][4 * grp] * inv, o[mb][4 * grp + 1] * inv, o[mb][4 * grp + 2] * inv,
-                      o[mb][4 * grp + 3] * inv};
-      *(f32x4*)(op + 32 * mb + 8 * grp) = val;
-    }
-  if (hi == 0)
-    a.lse_part[((int64_t)slot * a.hq + h) * n + qrow] =
-        l_run > 0.f ? (m_run + __log2f(l_run)) * 0.69314718055994530942f : NEG_INF;
+      for (int grp = 0; grp < 4; ++grp) {
+        const bf16x4 val{(__bf16)(o[mb][4 * grp] * inv), (__bf16)(o[mb][4 * grp + 1] * inv),
+                         (__bf16)(o[mb][4 * grp + 2] * inv), (__bf16)(o[mb][4 * grp + 3] * inv)};
+        *(bf16x4*)(op + 32 * mb + 8 * grp) = val;
+      }
+    if (hi == 0) a.lse_out[(int64_t)h * n + qrow] = lse;
+  } else {
+    float* op = a.o_part + (((int64_t)slot * n + qrow) * a.hq + h) * D + 4 * hi;
+#pragma unroll
+    for (int mb = 0; mb < MB_OUT; ++mb)
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const f32x4 val{o[mb][4 * grp] * inv, o[mb][4 * grp + 1] * inv, o[mb][4 * grp + 2] * inv,
+                        o[mb][4 * grp + 3] * inv};
+        *(f32x4*)(op + 32 * mb + 8 * grp) = val;
+      }
+    if (hi == 0) a.lse_part[((int64_t)slot * a.hq + h) * n + qrow] = lse;
+  }
 }
 
-template <int D, int BN, int WAVES>
+template <int D, int BN, int WAVES, bool FUSED>
 static hsap_status launch(const FwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_fwd_kernel<D, BN, WAVES>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, BN, WAVES, FUSED>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
   return HSAP_OK;
+}
+
+// shared argument checks and dispatch of the partial and fused forwards
+template <bool FUSED>
+static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                           const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs, int64_t num_runs,
+                           FwdArgs& a, hipStream_t s) {
+  Geom geom;
+  hsap_status st = check_attn(desc, &geom);
+  if (st != HSAP_OK) return st;
+  if (num_runs < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_runs < 0");
+  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
+  if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
+  const bool shape_ok = (d == 128 || d == 64) && (bn == 128 || bn == 64) && (bm == 128 || bm == 64);
+  if (!shape_ok)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no forward kernel for head_dim=%d BM=%d BN=%d (BM, BN in {64, 128})", d, bm, bn);
+  if (num_runs == 0) return HSAP_OK;
+  if (!q || !k || !v || !doc_start || !tiles || !runs) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v) & 15)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k and v must be 16-byte aligned");
+  a.q = (const __bf16*)q;
+  a.k = (const __bf16*)k;
+  a.v = (const __bf16*)v;
+  a.doc_start = doc_start;
+  a.tiles = tiles;
+  a.runs = runs;
+  a.geom = geom;
+  a.shard = desc->shard.shard_id;
+  a.hq = desc->heads_q;
+  a.hkv = desc->heads_kv;
+  a.group = desc->heads_q / desc->heads_kv;
+  a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
+#define HSAP_FWD_CASE(D_, BN_, W_) \
+  if (d == D_ && bn == BN_ && bm == 32 * W_) return launch<D_, BN_, W_, FUSED>(a, num_runs, s);
+  HSAP_FWD_CASE(128, 128, 4)
+  HSAP_FWD_CASE(128, 64, 4)
+  HSAP_FWD_CASE(128, 128, 2)
+  HSAP_FWD_CASE(128, 64, 2)
+  HSAP_FWD_CASE(64, 128, 4)
+  HSAP_FWD_CASE(64, 64, 4)
+  HSAP_FWD_CASE(64, 128, 2)
+  HSAP_FWD_CASE(64, 64, 2)
+#undef HSAP_FWD_CASE
+  HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no forward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
 }
 
 }  // namespace hsap
@@ -273,45 +344,25 @@ extern "C" hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const v
                                              int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots,
                                              void* hip_stream) {
   clear_error();
-  Geom geom;
-  hsap_status st = check_attn(desc, &geom);
-  if (st != HSAP_OK) return st;
-  if (num_runs < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_runs < 0");
   if (num_slots < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_slots < 1");
-  if (num_runs == 0) return HSAP_OK;
-  if (!q || !k || !v || !doc_start || !tiles || !runs || !o_part || !lse_part)
-    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
-  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o_part) & 15)
-    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k, v and o_part must be 16-byte aligned");
-  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
-  if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
-  FwdArgs a;
-  a.q = (const __bf16*)q;
-  a.k = (const __bf16*)k;
-  a.v = (const __bf16*)v;
-  a.doc_start = doc_start;
-  a.tiles = tiles;
-  a.runs = runs;
+  if (num_runs > 0 && (!o_part || !lse_part)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if ((uintptr_t)o_part & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_part must be 16-byte aligned");
+  FwdArgs a{};
   a.o_part = o_part;
   a.lse_part = lse_part;
   a.num_slots = num_slots;
-  a.geom = geom;
-  a.shard = desc->shard.shard_id;
-  a.hq = desc->heads_q;
-  a.hkv = desc->heads_kv;
-  a.group = desc->heads_q / desc->heads_kv;
-  a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
-  hipStream_t s = (hipStream_t)hip_stream;
-#define HSAP_FWD_CASE(D_, BN_, W_) \
-  if (d == D_ && bn == BN_ && bm == 32 * W_) return launch<D_, BN_, W_>(a, num_runs, s);
-  HSAP_FWD_CASE(128, 128, 4)
-  HSAP_FWD_CASE(128, 64, 4)
-  HSAP_FWD_CASE(128, 128, 2)
-  HSAP_FWD_CASE(128, 64, 2)
-  HSAP_FWD_CASE(64, 128, 4)
-  HSAP_FWD_CASE(64, 64, 4)
-  HSAP_FWD_CASE(64, 128, 2)
-  HSAP_FWD_CASE(64, 64, 2)
-#undef HSAP_FWD_CASE
-  HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no forward kernel for head_dim=%d BM=%d BN=%d (BM, BN in {64, 128})", d, bm, bn);
+  return forward<false>(desc, q, k, v, doc_start, tiles, runs, num_runs, a, (hipStream_t)hip_stream);
+}
+
+extern "C" hsap_status hsap_attn_fwd_fused(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                           const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
+                                           int64_t num_runs, void* o_out, float* lse_out, void* hip_stream) {
+  clear_error();
+  if (num_runs > 0 && (!o_out || !lse_out)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if ((uintptr_t)o_out & 7) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_out must be 8-byte aligned");
+  FwdArgs a{};
+  a.o_out = (__bf16*)o_out;
+  a.lse_out = lse_out;
+  a.num_slots = 1;
+  return forward<true>(desc, q, k, v, doc_start, tiles, runs, num_runs, a, (hipStream_t)hip_stream);
 }

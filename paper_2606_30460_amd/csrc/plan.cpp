@@ -215,7 +215,8 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
   Geom g;
   hsap_status st = check_shard(shard, &g);
   if (st != HSAP_OK) return st;
-  if (major != HSAP_MAJOR_Q && major != HSAP_MAJOR_K) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "unknown major %d", major);
+  if (major != HSAP_MAJOR_Q && major != HSAP_MAJOR_K && major != HSAP_MAJOR_Q_ALL)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "unknown major %d", major);
   if (num_tiles < 0 || (num_tiles > 0 && !tiles)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "tiles is NULL");
   if (num_tiles > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many tiles");
   if (!num_runs) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_runs is NULL");
@@ -269,6 +270,23 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
       }
       slots = std::max<int32_t>(slots, (int32_t)(c + P * (pieces - 1) + 1));
     }
+  } else if (major == HSAP_MAJOR_Q_ALL) {
+    std::vector<int64_t> order(num_tiles);
+    std::iota(order.begin(), order.end(), 0);
+    auto key = [&](int64_t i) {
+      const hsap_tile& t = tiles[i];
+      return ((int64_t)t.q_tile * P + step_of(t.chunk)) * nk + t.k_tile;
+    };
+    std::sort(order.begin(), order.end(), [&](int64_t a, int64_t b) { return key(a) < key(b); });
+    for (int64_t i = 0; i < num_tiles; ++i) sorted_tiles[i] = tiles[order[i]];
+    int64_t i = 0;
+    for (int32_t t = 0; t < nq; ++t) {
+      int64_t j = i;
+      while (j < num_tiles && sorted_tiles[j].q_tile == t) ++j;
+      out.push_back(hsap_run{0, t, (int32_t)i, (int32_t)(j - i)});
+      i = j;
+    }
+    slots = 1;
   } else {
     std::vector<int64_t> order(num_tiles);
     std::iota(order.begin(), order.end(), 0);

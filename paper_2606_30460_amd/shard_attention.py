@@ -7,7 +7,8 @@ runs inside the library:
             upload of the lists, hsap_doc_start (device)
   forward   hsap_partial_attn_fwd over the runs (one launch for every chunk,
             or one launch per ring step), then hsap_lse_merge of every slot
-            the runs wrote
+            the runs wrote; or hsap_attn_fwd_fused, one pass over every chunk
+            per q-tile without partials
   backward  hsap_attn_bwd_preprocess, hsap_partial_attn_bwd (dK/dV over the
             k-major runs, dQ over the forward's q-major runs), and
             hsap_convert_f32_bf16 for the gradients
@@ -83,6 +84,9 @@ class ShardAttention:
         for c in self.chunks:
             sel = runs_q[runs_q[:, 0] % self.P == c]
             self.runs_q_step.append(torch.from_numpy(np.ascontiguousarray(sel).reshape(-1)).to(dev) if len(sel) else None)
+        tiles_a, runs_a, _ = L.plan_runs(self.shard, self.tiles, L.MAJOR_Q_ALL)
+        self.tiles_all = torch.from_numpy(tiles_a.reshape(-1)).to(dev)
+        self.runs_all = torch.from_numpy(runs_a.reshape(-1)).to(dev)
         if backward:
             tiles_k, runs_k, _ = L.plan_runs(self.shard, self.tiles, L.MAJOR_K)
             self.tiles_k = torch.from_numpy(tiles_k.reshape(-1)).to(dev)
@@ -145,6 +149,12 @@ class ShardAttention:
                                bufs["lse_part"])
         L.lse_merge([bufs["o_part"][s] for s in self.present], [bufs["lse_part"][s] for s in self.present],
                     self.n, self.hq, self.d, bufs["o"], bufs["lse"])
+
+    def forward_fused(self, q, k, v, bufs: Dict[str, torch.Tensor]) -> None:
+        """The fused forward: final O and LSE into bufs["o"], bufs["lse"], no partials."""
+        if not self.planned:
+            raise RuntimeError("call plan() first")
+        L.attn_fwd_fused(self.desc, q, k, v, self.doc_start, self.tiles_all, self.runs_all, bufs["o"], bufs["lse"])
 
     # ------------------------------------------------------------- backward
     def backward(self, q, k, v, d_o, fwd: Dict[str, torch.Tensor], bufs: Dict[str, torch.Tensor],

@@ -65,6 +65,10 @@ class Case:
         sa.forward(q_sh, k_sh, v_sh, fwd, ring_steps=ring_steps)
         out = {"sa": sa, "o": fwd["o"].float().cpu().numpy(), "lse": fwd["lse"].cpu().numpy(),
                "o_part": fwd["o_part"].cpu().numpy(), "lse_part": fwd["lse_part"].cpu().numpy()}
+        fused = {"o": torch.full_like(fwd["o"], float("nan")), "lse": torch.full_like(fwd["lse"], float("nan"))}
+        sa.forward_fused(q_sh, k_sh, v_sh, fused)
+        out["o_fused"] = fused["o"].float().cpu().numpy()
+        out["lse_fused"] = fused["lse"].cpu().numpy()
         if self.backward:
             do_sh = to_sharded(sa.shard, self.do.to(dev))[self.shard].contiguous()
             bwd = sa.alloc_backward()
@@ -123,6 +127,11 @@ def compare_forward(gpu: Dict, ref: Dict, rows=None) -> Dict[str, float]:
     report["lse"] = max_abs(gpu["lse"][:, sl], ref["lse"])
     assert report["o"] <= O_ATOL, report
     assert report["lse"] <= LSE_ATOL, report
+    if "o_fused" in gpu:                                  # the fused forward meets the same bar
+        report["o_fused"] = max_abs(gpu["o_fused"][sl], ref["o"])
+        report["lse_fused"] = max_abs(gpu["lse_fused"][:, sl], ref["lse"])
+        assert report["o_fused"] <= O_ATOL, report
+        assert report["lse_fused"] <= LSE_ATOL, report
     return report
 
 

@@ -142,6 +142,16 @@ def test_forward_rejects_null_and_misaligned():
     assert lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 0, fake, fake, 1, None) == 0
 
 
+def test_fused_forward_validates_before_launch():
+    lib = L.lib()
+    fake = ctypes.c_void_p(4096)
+    st = lib.hsap_attn_fwd_fused(ctypes.byref(_attn_desc(head_dim=96)), fake, fake, fake, fake, fake, fake, 1, fake,
+                                 fake, None)
+    assert st == L.HSAP_ERR_UNSUPPORTED
+    st = lib.hsap_attn_fwd_fused(ctypes.byref(_attn_desc()), fake, fake, fake, fake, fake, fake, 1, None, fake, None)
+    assert st == L.HSAP_ERR_INVALID_ARG
+
+
 def test_backward_validates_before_launch():
     lib = L.lib()
     fake = ctypes.c_void_p(4096)

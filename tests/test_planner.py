@@ -92,8 +92,9 @@ def _runs_ok(shard, tiles, sorted_tiles, runs, major, split=0, num_slots=None):
     covered = np.zeros(len(tiles), dtype=int)
     for slot, t, first, count in runs:
         seg = sorted_tiles[first:first + count]
-        assert np.all(seg[:, 0] == slot % P)              # a run's tiles belong to its slot's chunk
-        assert np.all(seg[:, 1 if major == L.MAJOR_Q else 2] == t)
+        if major != L.MAJOR_Q_ALL:
+            assert np.all(seg[:, 0] == slot % P)          # a run's tiles belong to its slot's chunk
+        assert np.all(seg[:, 1 if major in (L.MAJOR_Q, L.MAJOR_Q_ALL) else 2] == t)
         if split and major == L.MAJOR_Q:
             assert count <= split
         covered[first:first + count] += 1
@@ -102,6 +103,17 @@ def _runs_ok(shard, tiles, sorted_tiles, runs, major, split=0, num_slots=None):
     assert np.all(np.diff(counts) <= 0)           # longest first
     key = lambda a: sorted(map(tuple, a.tolist()))
     assert key(sorted_tiles) == key(tiles)        # sorted_tiles is a permutation of tiles
+    if major == L.MAJOR_Q_ALL:
+        # one run per q-tile over all chunks, its tiles in ring order
+        assert sorted(runs[:, 1].tolist()) == list(range(nq)) and np.all(runs[:, 0] == 0)
+        r = shard.shard_id
+        for _, t, first, count in runs:
+            seg = sorted_tiles[first:first + count]
+            assert np.all(seg[:, 1] == t)
+            steps = (r - seg[:, 0]) % P
+            keys = steps.astype(np.int64) * 100000 + seg[:, 2]
+            assert np.all(np.diff(keys) > 0)
+        return
     if major == L.MAJOR_Q:
         # every slot in use has exactly one run per q-tile
         slots = sorted(set(runs[:, 0].tolist()))
@@ -120,7 +132,7 @@ def test_runs(name, split):
     r = w.shard if w.shard is not None else 1
     d = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, r, w.block_m, w.block_n)
     tiles = L.plan(w.cu_seqlens, d)["tiles"]
-    for major in (L.MAJOR_Q, L.MAJOR_K):
+    for major in (L.MAJOR_Q, L.MAJOR_K, L.MAJOR_Q_ALL):
         sorted_tiles, runs, slots = L.plan_runs(d, tiles, major, split)
         _runs_ok(d, tiles, sorted_tiles, runs, major, split, slots)
 
