@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import platform
 import sys
@@ -50,10 +51,10 @@ def _critical_shard(L, w):
 
 
 def measure(name: str, steps: int, warmup: int, backward=None):
-    """Time `steps` pipelined steps of one workload; returns a result dict (GPU side only)."""
+    """Time `steps` steps of one workload through the step executor; returns a result dict (GPU side only)."""
     import torch
     from paper_2606_30460_amd import _lib as L
-    from paper_2606_30460_amd.shard_attention import PlanPipeline, ShardAttention, to_sharded
+    from paper_2606_30460_amd.shard_attention import ShardAttention, to_sharded
     from workloads import make_workload
 
     w = make_workload(name)
@@ -62,99 +63,106 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     log("[bench] %s: generating inputs (shard %d)" % (w.name, shard))
     t = w.tensors(backward=bwd)
     dev = torch.device("cuda")
-    sa = ShardAttention(w.cu_seqlens, w.total_tokens, w.sp_degree, w.layout, shard, w.heads_q, w.heads_kv,
-                        w.head_dim, w.block_m, w.block_n)
-    q = to_sharded(sa.shard, t["q"].to(dev))[shard].contiguous()
-    k = to_sharded(sa.shard, t["k"].to(dev))
-    v = to_sharded(sa.shard, t["v"].to(dev))
-    d_o = to_sharded(sa.shard, t["do"].to(dev))[shard].contiguous() if bwd else None
+    sd = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, shard, w.block_m, w.block_n)
+    desc = L.attn_desc(sd, w.heads_q, w.heads_kv, w.head_dim, 1.0 / math.sqrt(w.head_dim))
+    ex = L.Executor(desc, backward=bwd, fused=True)
+    q = to_sharded(sd, t["q"].to(dev))[shard].contiguous()
+    k = to_sharded(sd, t["k"].to(dev))
+    v = to_sharded(sd, t["v"].to(dev))
+    d_o = to_sharded(sd, t["do"].to(dev))[shard].contiguous() if bwd else None
     del t
-    pipe = PlanPipeline(sa, backward=bwd)
-    fwd = sa.alloc_forward()
-    bb = sa.alloc_backward() if bwd else None
+    n = w.total_tokens // w.sp_degree
+    o = torch.empty(n, w.heads_q, w.head_dim, dtype=torch.bfloat16, device=dev)
+    lse = torch.empty(w.heads_q, n, dtype=torch.float32, device=dev)
+    if bwd:
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    cu = np.ascontiguousarray(w.cu_seqlens, dtype=np.int32)
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
     torch.cuda.synchronize()
 
-    events = []
-
-    def one_step():
-        pipe.step()
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
-        e[0].record()
-        L.partial_attn_fwd(sa.desc, q, k, v, sa.doc_start, sa.tiles_q, sa.runs_q, fwd["o_part"], fwd["lse_part"])
-        e[1].record()
-        L.lse_merge([fwd["o_part"][s] for s in sa.present], [fwd["lse_part"][s] for s in sa.present], sa.n, sa.hq,
-                    sa.d, fwd["o"], fwd["lse"])
-        e[2].record()
+    def one_step(e):
+        # a training step re-plans its batch: host planner, one upload, document starts
+        ex.plan(cu)
+        if e:
+            e[0].record()
+        ex.partial_forward(q, k, v)
+        if e:
+            e[1].record()
+        ex.merge(o, lse)
+        if e:
+            e[2].record()
         if bwd:
-            for c in sa.chunks_present:
-                bb["dk_acc"][c].zero_()
-                bb["dv_acc"][c].zero_()
-            bb["dq_acc"].zero_()
-            L.attn_bwd_preprocess(fwd["o"], d_o, sa.n, sa.hq, sa.d, bb["delta"])
-            e[3].record()
-            L.partial_attn_bwd(sa.desc, q, k, v, d_o, fwd["lse"], bb["delta"], sa.doc_start, sa.tiles_k, sa.runs_k,
-                               sa.tiles_q, sa.runs_q, bb["dq_acc"], bb["dk_acc"], bb["dv_acc"])
-            e[4].record()
-            L.convert_f32_bf16(bb["dq_acc"], bb["dq"])
-            for c in sa.chunks_present:
-                L.convert_f32_bf16(bb["dk_acc"][c], bb["dk"][c])
-                L.convert_f32_bf16(bb["dv_acc"][c], bb["dv"][c])
-        events.append(e)
+            ex.backward(q, k, v, d_o, o, lse, dq, dk, dv)
+            if e:
+                e[3].record()
 
     for _ in range(warmup):
-        one_step()
+        one_step(None)
     torch.cuda.synchronize()
-    events.clear()
     t0 = time.perf_counter()
-    for _ in range(steps):
-        one_step()
+    for i in range(steps):
+        one_step(events[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    info = ex.info()
 
     fwd_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     merge_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
-    bwd_ms = np.array([e[3].elapsed_time(e[4]) for e in events]) if bwd else None
+    bwd_ms = np.array([e[2].elapsed_time(e[3]) for e in events]) if bwd else None
 
-    # the fused forward (partials and merge in one pass), timed on the same inputs
+    # the fused forward (partials and merge in one pass), same plan and inputs, launches back to back
     fused_ms = None
     if not bwd:
-        sa.plan()
-        fo = {"o": torch.empty_like(fwd["o"]), "lse": torch.empty_like(fwd["lse"])}
+        fo, fl = torch.empty_like(o), torch.empty_like(lse)
         for _ in range(3):
-            sa.forward_fused(q, k, v, fo)
-        torch.cuda.synchronize()
+            ex.forward(q, k, v, fo, fl, fused=True)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         ev[0].record()
         for _ in range(steps):
-            sa.forward_fused(q, k, v, fo)
+            ex.forward(q, k, v, fo, fl, fused=True)
         ev[1].record()
         torch.cuda.synchronize()
         fused_ms = ev[0].elapsed_time(ev[1]) / steps
 
-    # planner host time (not overlapped), for reference
+    # planner host time alone (hsap_plan; overlapped with the GPU inside a step)
     t1 = time.perf_counter()
     reps = 20
     for _ in range(reps):
-        L.plan(sa.cu_host, sa.shard)
+        L.plan(cu, sd)
     plan_ms = (time.perf_counter() - t1) / reps * 1e3
 
-    pairs = sa.total_useful_pairs
-    tiles = int(sa.step_offsets[-1])
+    # algorithmic merge bytes: every part's LSE row, the O row of parts whose LSE is finite, the outputs.
+    # The finite rows are counted on the same parts computed through the entry points.
+    sa = ShardAttention(cu, w.total_tokens, w.sp_degree, w.layout, shard, w.heads_q, w.heads_kv, w.head_dim,
+                        w.block_m, w.block_n, max_run_tiles=info["split_length"])
+    sa.plan()
+    part = {"o_part": torch.empty(len(sa.present), n, w.heads_q, w.head_dim, dtype=torch.float32, device=dev)}
+    part["lse_part"] = torch.empty(len(sa.present), w.heads_q, n, dtype=torch.float32, device=dev)
+    finite_rows = 0
+    for i, slot in enumerate(sa.present):
+        sel = sa.runs_q_host[sa.runs_q_host[:, 0] == slot].copy()
+        sel[:, 0] = 0
+        L.partial_attn_fwd(sa.desc, q, k, v, sa.doc_start, sa.tiles_q, torch.from_numpy(sel.reshape(-1)).to(dev),
+                           part["o_part"][i], part["lse_part"][i])
+        finite_rows += int(torch.isfinite(part["lse_part"][i]).sum().item())
+    assert len(sa.present) == info["num_parts"]
+    del part, sa
+    merge_bytes = (info["num_parts"] * w.heads_q * n * 4 + finite_rows * w.head_dim * 4
+                   + n * w.heads_q * (2 * w.head_dim + 4))
+
+    pairs = info["useful_pairs"]
+    tiles = info["num_tiles"]
     fwd_flops = 4.0 * w.head_dim * w.heads_q * pairs
     bwd_flops = 10.0 * w.head_dim * w.heads_q * pairs if bwd else 0.0
-    # merge bytes actually required: every part's LSE row, the O row of parts whose LSE is finite, the outputs
-    lse_present = fwd["lse_part"][sa.present]
-    finite_rows = int(torch.isfinite(lse_present).sum().item())
-    merge_bytes = (len(sa.present) * sa.hq * sa.n * 4 + finite_rows * sa.d * 4 + sa.n * sa.hq * (2 * sa.d + 4))
     ms_step = wall / steps * 1e3
     res = {
         "workload": w.name, "shard": shard, "tokens": w.total_tokens, "sp_degree": w.sp_degree,
         "layout": w.layout, "heads_q": w.heads_q, "heads_kv": w.heads_kv, "head_dim": w.head_dim,
         "block_m": w.block_m, "block_n": w.block_n, "backward": bool(bwd), "docs": w.num_docs,
-        "useful_pairs": pairs, "tiles": tiles, "full_tiles": int(np.sum(sa.tiles_q.view(-1, 4)[:, 3].cpu().numpy() == 0)),
+        "useful_pairs": pairs, "tiles": tiles, "full_tiles": info["num_full_tiles"],
         "tile_efficiency": pairs / float(tiles * w.block_m * w.block_n),
-        "chunks_with_tiles": len(sa.chunks_present),
-        "partial_slots": len(sa.present), "split_length": int(sa.split),
+        "chunks_with_tiles": info["chunks_with_tiles"],
+        "partial_slots": info["num_parts"], "split_length": info["split_length"],
         "useful_gflop_per_step": (fwd_flops + bwd_flops) / 1e9,
         "ms_per_step": ms_step,
         "tflops": (fwd_flops + bwd_flops) / (ms_step * 1e-3) / 1e12,
@@ -169,12 +177,13 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     if fused_ms is not None:
         res.update({"fused_fwd_kernel_ms": fused_ms, "fused_fwd_tflops": fwd_flops / (fused_ms * 1e-3) / 1e12})
     if bwd:
-        res.update({"bwd_kernel_ms_mean": float(bwd_ms.mean()), "bwd_kernel_ms_median": float(np.median(bwd_ms)),
-                    "bwd_kernel_tflops": bwd_flops / (bwd_ms.mean() * 1e-3) / 1e12})
+        res.update({"bwd_ms_mean": float(bwd_ms.mean()), "bwd_ms_median": float(np.median(bwd_ms)),
+                    "bwd_tflops": bwd_flops / (bwd_ms.mean() * 1e-3) / 1e12})
     res["_fwd_flops"] = fwd_flops
     log("[bench] %s: %.3f ms/step, %.1f TFLOP/s useful (fwd kernel %.3f ms = %.1f TFLOP/s)" % (
         w.name, ms_step, res["tflops"], res["fwd_kernel_ms_mean"], res["fwd_kernel_tflops"]))
-    del q, k, v, fwd, bb, pipe, sa
+    ex.close()
+    del q, k, v, o, lse
     torch.cuda.empty_cache()
     return res
 

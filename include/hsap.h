@@ -29,8 +29,9 @@
  *   - Query head h reads K/V head h / (Hq / Hkv).
  *   - bf16 is IEEE bfloat16 (1-8-7); LSE is the natural-log log-sum-exp of
  *     the scaled scores, fp32, laid out [Hq, rows].
- *   - Device pointers are caller-owned; the library allocates no device
- *     memory and keeps no state between calls.  Kernels run asynchronously on
+ *   - Device pointers are caller-owned; apart from an hsap_executor (which
+ *     owns its list buffers and workspace, see below) the library allocates
+ *     no device memory and keeps no state between calls.  Kernels run asynchronously on
  *     the given HIP stream (NULL = default stream).  HSAP_ERR_HIP reports a
  *     launch failure only; a fault inside a kernel surfaces at the caller's
  *     next synchronisation.
@@ -322,6 +323,119 @@ hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, con
  * aligned when count is a multiple of 8.
  */
 hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, void* hip_stream);
+
+/* ------------------------------------------------------------------------
+ * Step executor -- the library's runtime for one shard geometry: each packed
+ * batch is planned on the host and run with one call per stage.  Not in the
+ * paper; it sequences the entry points above the way a training step uses
+ * them (plan before any transfer, then the shard's attention against every
+ * chunk, then the backward), keeping the host cost of a step small next to
+ * its kernels.
+ *
+ * An executor owns: two pinned staging buffers for the planner's lists, one
+ * device list buffer, the device doc_start array, the fp32 partial outputs
+ * of the forward (grown to the largest plan seen) and, with
+ * HSAP_EXEC_BACKWARD, the backward's fp32 accumulators and delta.  Buffers
+ * grow on demand; a growth synchronises the stream first.
+ *
+ * Threading and streams: one executor is used by one host thread at a time,
+ * on one device (the device current at creation), and all its calls should
+ * pass the same stream: the single device list buffer is reused in stream
+ * order.  Inputs and outputs are caller-owned device tensors in the layouts
+ * of hsap_partial_attn_fwd / hsap_partial_attn_bwd.
+ * --------------------------------------------------------------------- */
+typedef struct hsap_executor hsap_executor;
+
+/* Options of hsap_executor_create (bit mask). */
+enum {
+  HSAP_EXEC_BACKWARD = 1,  /* also plan k-major runs and own backward workspace */
+  HSAP_EXEC_FUSED = 2      /* also plan MAJOR_Q_ALL runs for the fused forward   */
+};
+
+/* What the current plan holds (hsap_executor_info). */
+typedef struct {
+  int64_t num_tiles;        /* non-empty tiles over all ring steps          */
+  int64_t num_full_tiles;   /* of which FULL                                 */
+  int64_t useful_pairs;     /* allowed (query, key) pairs per head           */
+  int64_t num_runs_q;       /* q-major runs (forward, dQ)                    */
+  int64_t num_runs_k;       /* k-major runs (dK, dV); 0 without BACKWARD     */
+  int64_t num_runs_all;     /* fused-forward runs; 0 without FUSED           */
+  int32_t num_parts;        /* partial outputs the forward writes and merges */
+  int32_t split_length;     /* max_run_tiles used for the q-major runs (0: none) */
+  int32_t chunks_with_tiles;
+  int32_t reserved;
+} hsap_exec_info;
+
+/*
+ * hsap_executor_create -- an executor for the shard and heads in `desc`
+ * (same supported shapes as hsap_partial_attn_fwd; with HSAP_EXEC_BACKWARD
+ * those of hsap_partial_attn_bwd).
+ *   options        HSAP_EXEC_* bits.
+ *   max_run_tiles  q-major split: -1 picks hsap_split_length per plan from
+ *                  the device's compute-unit count, 0 never splits, > 0 is
+ *                  used as given.  A plan whose split would need more than
+ *                  HSAP_MAX_MERGE_PARTS partials is planned without split.
+ *   out            receives the executor; NULL on failure.
+ * Returns HSAP_ERR_HIP when device or pinned memory cannot be allocated.
+ */
+hsap_status hsap_executor_create(const hsap_attn_desc* desc, int32_t options, int32_t max_run_tiles,
+                                 hsap_executor** out);
+
+/* Waits for the device, then frees everything the executor owns.  NULL is a
+ * no-op. */
+void hsap_executor_destroy(hsap_executor* ex);
+
+/*
+ * hsap_executor_plan -- plan one packed batch: hsap_plan, hsap_plan_runs for
+ * the q-major runs (partial slots renumbered densely 0..num_parts-1 in
+ * increasing original slot order) and, per the options, the k-major and
+ * MAJOR_Q_ALL runs; then one asynchronous upload of every list and
+ * cu_seqlens from a pinned staging buffer, and hsap_doc_start, on `stream`.
+ * The host blocks only while the staging buffer it is about to reuse is
+ * still being uploaded (two plans in flight).
+ *   cu_seqlens  host int32 [num_docs + 1] for the executor's N (rules of
+ *               hsap_plan); read before the call returns.
+ */
+hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int32_t num_docs, void* hip_stream);
+
+/* Counts of the current plan; HSAP_ERR_INVALID_ARG before the first plan. */
+hsap_status hsap_executor_info(const hsap_executor* ex, hsap_exec_info* info);
+
+/*
+ * hsap_executor_forward -- the shard's attention against every chunk for the
+ * current plan.  fused = 0: hsap_partial_attn_fwd over all q-major runs into
+ * the executor's partials, then hsap_lse_merge of the num_parts partials.
+ * fused = 1 (needs HSAP_EXEC_FUSED): hsap_attn_fwd_fused.
+ *   q        device bf16 [n, Hq, d];  k, v  device bf16 [P, n, Hkv, d].
+ *   o_out    device bf16 [n, Hq, d];  lse_out  device fp32 [Hq, n].
+ */
+hsap_status hsap_executor_forward(hsap_executor* ex, const void* q, const void* k, const void* v, int32_t fused,
+                                  void* o_out, float* lse_out, void* hip_stream);
+
+/*
+ * hsap_executor_partial_forward, hsap_executor_merge -- the two stages of
+ * hsap_executor_forward(fused = 0), callable one by one (e.g. to time them):
+ * the partial attention of every q-major run into the executor's partials,
+ * then their merge into o_out / lse_out.  The merge reads the partials of
+ * the last partial forward; call them in this order, after the same plan.
+ */
+hsap_status hsap_executor_partial_forward(hsap_executor* ex, const void* q, const void* k, const void* v,
+                                          void* hip_stream);
+hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, void* hip_stream);
+
+/*
+ * hsap_executor_backward -- gradients of the forward for the current plan
+ * (needs HSAP_EXEC_BACKWARD): zeroes the executor's accumulators, then
+ * hsap_attn_bwd_preprocess, hsap_partial_attn_bwd over the k-major and
+ * q-major runs, and the conversion to bf16.
+ *   q, k, v  as for the forward;  d_o, o  device bf16 [n, Hq, d] (o: the
+ *            forward's output);  lse  device fp32 [Hq, n] (the forward's).
+ *   dq       device bf16 [n, Hq, d].
+ *   dk, dv   device bf16 [P, n, Hkv, d], sharded order: chunks without tiles
+ *            receive zeros.
+ */
+hsap_status hsap_executor_backward(hsap_executor* ex, const void* q, const void* k, const void* v, const void* d_o,
+                                   const void* o, const float* lse, void* dq, void* dk, void* dv, void* hip_stream);
 
 #ifdef __cplusplus
 }

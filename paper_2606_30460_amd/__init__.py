@@ -14,6 +14,7 @@ from ._lib import (  # noqa: F401
     TILE_FULL,
     TILE_MASKED,
     AttnDesc,
+    Executor,
     HsapError,
     ShardDesc,
     attn_bwd_preprocess,

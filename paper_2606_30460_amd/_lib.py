@@ -36,8 +36,13 @@ MAX_MERGE_PARTS = 64
 EXPORTED = (
     "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_doc_start",
     "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
-    "hsap_partial_attn_bwd", "hsap_convert_f32_bf16",
+    "hsap_partial_attn_bwd", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
+    "hsap_executor_plan", "hsap_executor_info", "hsap_executor_forward", "hsap_executor_partial_forward",
+    "hsap_executor_merge", "hsap_executor_backward",
 )
+
+EXEC_BACKWARD = 1
+EXEC_FUSED = 2
 
 
 class HsapError(RuntimeError):
@@ -54,6 +59,13 @@ class ShardDesc(ctypes.Structure):
 class AttnDesc(ctypes.Structure):
     _fields_ = [("shard", ShardDesc), ("heads_q", ctypes.c_int32), ("heads_kv", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
+
+
+class ExecInfo(ctypes.Structure):
+    _fields_ = [("num_tiles", ctypes.c_int64), ("num_full_tiles", ctypes.c_int64), ("useful_pairs", ctypes.c_int64),
+                ("num_runs_q", ctypes.c_int64), ("num_runs_k", ctypes.c_int64), ("num_runs_all", ctypes.c_int64),
+                ("num_parts", ctypes.c_int32), ("split_length", ctypes.c_int32),
+                ("chunks_with_tiles", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -76,6 +88,14 @@ _SIG = {
     "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P,
                                              _P]),
     "hsap_convert_f32_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
+    "hsap_executor_create": (ctypes.c_int, [_P, _I32, _I32, _P]),
+    "hsap_executor_destroy": (None, [_P]),
+    "hsap_executor_plan": (ctypes.c_int, [_P, _P, _I32, _P]),
+    "hsap_executor_info": (ctypes.c_int, [_P, _P]),
+    "hsap_executor_forward": (ctypes.c_int, [_P, _P, _P, _P, _I32, _P, _P, _P]),
+    "hsap_executor_partial_forward": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+    "hsap_executor_merge": (ctypes.c_int, [_P, _P, _P, _P]),
+    "hsap_executor_backward": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
 }
 
 
@@ -338,3 +358,93 @@ def convert_f32_bf16(src, dst, stream=None) -> None:
     _dev(src, "float32", "src")
     _dev(dst, "bfloat16", "dst", src.numel())
     _check(lib().hsap_convert_f32_bf16(_ptr(src), _ptr(dst), src.numel(), _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# step executor
+# ---------------------------------------------------------------------------
+
+class Executor:
+    """hsap_executor: plan a packed batch, then run the shard's forward and
+    backward, one library call each.
+
+    ``max_run_tiles``: -1 picks the q-major split per plan, 0 never splits.
+    Tensors are checked once per call (dtype, size, contiguity); all calls
+    should use the same stream.
+    """
+
+    def __init__(self, desc: AttnDesc, backward: bool = False, fused: bool = False, max_run_tiles: int = -1):
+        self.desc = desc
+        s = desc.shard
+        self.n = s.total_tokens // s.sp_degree
+        self.P = s.sp_degree
+        self._q_numel = self.n * desc.heads_q * desc.head_dim
+        self._kv_numel = self.P * self.n * desc.heads_kv * desc.head_dim
+        self._lse_numel = desc.heads_q * self.n
+        opts = (EXEC_BACKWARD if backward else 0) | (EXEC_FUSED if fused else 0)
+        handle = ctypes.c_void_p(0)
+        _check(lib().hsap_executor_create(ctypes.byref(desc), opts, int(max_run_tiles), ctypes.byref(handle)))
+        self._h = handle
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().hsap_executor_destroy(self._h)
+        self._h = None
+
+    def __del__(self):  # pragma: no cover - interpreter shutdown order
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _handle(self):
+        if self._h is None:
+            raise RuntimeError("executor is closed")
+        return self._h
+
+    def plan(self, cu_seqlens: np.ndarray, stream=None) -> None:
+        """Plan one batch (host int32 cu_seqlens [num_docs + 1])."""
+        cu = cu_seqlens
+        if not (isinstance(cu, np.ndarray) and cu.dtype == np.int32 and cu.flags.c_contiguous):
+            cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+        _check(lib().hsap_executor_plan(self._handle(), cu.ctypes.data, len(cu) - 1, _stream(stream)))
+
+    def info(self) -> Dict[str, int]:
+        out = ExecInfo()
+        _check(lib().hsap_executor_info(self._handle(), ctypes.byref(out)))
+        return {name: int(getattr(out, name)) for name, _ in ExecInfo._fields_ if name != "reserved"}
+
+    def forward(self, q, k, v, o_out, lse_out, fused: bool = False, stream=None) -> None:
+        _dev(q, "bfloat16", "q", self._q_numel)
+        _dev(k, "bfloat16", "k", self._kv_numel)
+        _dev(v, "bfloat16", "v", self._kv_numel)
+        _dev(o_out, "bfloat16", "o_out", self._q_numel)
+        _dev(lse_out, "float32", "lse_out", self._lse_numel)
+        _check(lib().hsap_executor_forward(self._handle(), _ptr(q), _ptr(k), _ptr(v), int(bool(fused)), _ptr(o_out),
+                                           _ptr(lse_out), _stream(stream)))
+
+    def partial_forward(self, q, k, v, stream=None) -> None:
+        """First stage of forward(fused=False): partial attention into the executor's partials."""
+        _dev(q, "bfloat16", "q", self._q_numel)
+        _dev(k, "bfloat16", "k", self._kv_numel)
+        _dev(v, "bfloat16", "v", self._kv_numel)
+        _check(lib().hsap_executor_partial_forward(self._handle(), _ptr(q), _ptr(k), _ptr(v), _stream(stream)))
+
+    def merge(self, o_out, lse_out, stream=None) -> None:
+        """Second stage: LSE merge of the partials into o_out / lse_out."""
+        _dev(o_out, "bfloat16", "o_out", self._q_numel)
+        _dev(lse_out, "float32", "lse_out", self._lse_numel)
+        _check(lib().hsap_executor_merge(self._handle(), _ptr(o_out), _ptr(lse_out), _stream(stream)))
+
+    def backward(self, q, k, v, d_o, o, lse, dq, dk, dv, stream=None) -> None:
+        _dev(q, "bfloat16", "q", self._q_numel)
+        _dev(k, "bfloat16", "k", self._kv_numel)
+        _dev(v, "bfloat16", "v", self._kv_numel)
+        _dev(d_o, "bfloat16", "d_o", self._q_numel)
+        _dev(o, "bfloat16", "o", self._q_numel)
+        _dev(lse, "float32", "lse", self._lse_numel)
+        _dev(dq, "bfloat16", "dq", self._q_numel)
+        _dev(dk, "bfloat16", "dk", self._kv_numel)
+        _dev(dv, "bfloat16", "dv", self._kv_numel)
+        _check(lib().hsap_executor_backward(self._handle(), _ptr(q), _ptr(k), _ptr(v), _ptr(d_o), _ptr(o), _ptr(lse),
+                                            _ptr(dq), _ptr(dk), _ptr(dv), _stream(stream)))

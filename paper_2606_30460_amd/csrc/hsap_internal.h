@@ -55,4 +55,10 @@ hsap_status check_shard(const hsap_shard_desc* d, Geom* g);
 // Validates an attention descriptor (shard part plus heads, head_dim, scale).
 hsap_status check_attn(const hsap_attn_desc* d, Geom* g);
 
+#if defined(__HIPCC__)
+// Writes `bytes` zero bytes at dst on `stream` with a kernel (bytes a multiple
+// of 4, dst 16-byte aligned).
+hsap_status zero_fill(void* dst, int64_t bytes, hipStream_t stream);
+#endif
+
 }  // namespace hsap

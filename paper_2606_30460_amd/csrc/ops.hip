@@ -168,6 +168,16 @@ __global__ __launch_bounds__(256) void gather_kernel(Geom g, const uint4* src, u
   }
 }
 
+// ---------------------------------------------------------------------------
+// zero fill, 16 bytes per lane (a kernel rather than a memset node, so the
+// sequence stays valid inside captured graphs)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void zero_kernel(uint4* dst, int64_t words16, uint32_t* tail, int32_t tail_words) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < words16; i += stride) dst[i] = uint4{0, 0, 0, 0};
+  if (blockIdx.x == 0 && (int)threadIdx.x < tail_words) tail[threadIdx.x] = 0;
+}
+
 static hsap_status check_launch(const char* what) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
@@ -177,6 +187,16 @@ static hsap_status check_launch(const char* what) {
 static unsigned grid_for(int64_t threads) {
   const int64_t b = (threads + 255) / 256;
   return (unsigned)(b < 1 ? 1 : (b > 65536 ? 65536 : b));
+}
+
+hsap_status zero_fill(void* dst, int64_t bytes, hipStream_t stream) {
+  if (bytes == 0) return HSAP_OK;
+  if (!dst || bytes < 0 || (bytes & 3) || ((uintptr_t)dst & 15))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "zero_fill: bad buffer or size %lld", (long long)bytes);
+  const int64_t words16 = bytes / 16;
+  hipLaunchKernelGGL(zero_kernel, dim3(grid_for(words16)), dim3(256), 0, stream, (uint4*)dst, words16,
+                     (uint32_t*)((char*)dst + words16 * 16), (int32_t)((bytes - words16 * 16) / 4));
+  return check_launch("zero_fill");
 }
 
 }  // namespace hsap

@@ -224,7 +224,9 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
   if (capacity < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "capacity < 0");
   const int32_t P = g.P, r = shard->shard_id;
   const int64_t nq = g.n / shard->block_m, nk = g.n / shard->block_n;
-  auto step_of = [&](int32_t c) { return ((r - c) % P + P) % P; };
+  std::vector<int32_t> step_tab(P);  // ring step at which shard r holds chunk c
+  for (int32_t c = 0; c < P; ++c) step_tab[c] = ((r - c) % P + P) % P;
+  auto step_of = [&](int32_t c) { return step_tab[c]; };
   // the list must be canonical: ring step, q_tile, k_tile strictly increasing
   for (int64_t i = 0; i < num_tiles; ++i) {
     const hsap_tile& t = tiles[i];
@@ -238,6 +240,17 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
       if (b <= a) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "tile list not in canonical order at %lld", (long long)i);
     }
   }
+  // Stable counting sort of tiles[lo, hi) by `bucket` into sorted_tiles[lo, hi).  The
+  // canonical list is ordered by (ring step, q_tile, k_tile), so a stable pass by q_tile
+  // over the whole list orders by (q_tile, ring step, k_tile), and one by k_tile within
+  // each ring step's segment orders that segment by (k_tile, q_tile).
+  std::vector<int64_t> bucket_at;
+  auto counting_sort = [&](int64_t lo, int64_t hi, int64_t buckets, auto bucket) {
+    bucket_at.assign((size_t)buckets + 1, 0);
+    for (int64_t i = lo; i < hi; ++i) ++bucket_at[(size_t)bucket(tiles[i]) + 1];
+    for (int64_t b = 0; b < buckets; ++b) bucket_at[(size_t)b + 1] += bucket_at[(size_t)b];
+    for (int64_t i = lo; i < hi; ++i) sorted_tiles[lo + bucket_at[(size_t)bucket(tiles[i])]++] = tiles[i];
+  };
   std::vector<hsap_run> out;
   int32_t slots = 0;
   if (major == HSAP_MAJOR_Q) {
@@ -271,14 +284,7 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
       slots = std::max<int32_t>(slots, (int32_t)(c + P * (pieces - 1) + 1));
     }
   } else if (major == HSAP_MAJOR_Q_ALL) {
-    std::vector<int64_t> order(num_tiles);
-    std::iota(order.begin(), order.end(), 0);
-    auto key = [&](int64_t i) {
-      const hsap_tile& t = tiles[i];
-      return ((int64_t)t.q_tile * P + step_of(t.chunk)) * nk + t.k_tile;
-    };
-    std::sort(order.begin(), order.end(), [&](int64_t a, int64_t b) { return key(a) < key(b); });
-    for (int64_t i = 0; i < num_tiles; ++i) sorted_tiles[i] = tiles[order[i]];
+    counting_sort(0, num_tiles, nq, [](const hsap_tile& t) { return t.q_tile; });
     int64_t i = 0;
     for (int32_t t = 0; t < nq; ++t) {
       int64_t j = i;
@@ -288,14 +294,12 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
     }
     slots = 1;
   } else {
-    std::vector<int64_t> order(num_tiles);
-    std::iota(order.begin(), order.end(), 0);
-    auto key = [&](int64_t i) {
-      const hsap_tile& t = tiles[i];
-      return ((int64_t)step_of(t.chunk) * nk + t.k_tile) * nq + t.q_tile;
-    };
-    std::sort(order.begin(), order.end(), [&](int64_t a, int64_t b) { return key(a) < key(b); });
-    for (int64_t i = 0; i < num_tiles; ++i) sorted_tiles[i] = tiles[order[i]];
+    for (int64_t lo = 0; lo < num_tiles;) {  // one ring step (one chunk) at a time
+      int64_t hi = lo;
+      while (hi < num_tiles && tiles[hi].chunk == tiles[lo].chunk) ++hi;
+      counting_sort(lo, hi, nk, [](const hsap_tile& t) { return t.k_tile; });
+      lo = hi;
+    }
     int64_t i = 0;
     while (i < num_tiles) {
       int64_t j = i;

@@ -1,7 +1,8 @@
 """One sequence-parallel shard's document-masked attention, sequenced over libhsap.
 
-This is call sequencing and buffer allocation only; every step of the path
-runs inside the library:
+This is call sequencing and buffer allocation only, one entry point at a
+time (the library's hsap_executor runs the same sequence natively, one call
+per stage); every step of the path runs inside the library:
 
   plan      hsap_plan (host C++) -> hsap_split_length / hsap_plan_runs ->
             upload of the lists, hsap_doc_start (device)
@@ -182,91 +183,6 @@ class ShardAttention:
                 bufs["dv_acc"][c].zero_()
                 bufs["dk"][c].zero_()
                 bufs["dv"][c].zero_()
-
-
-class PlanPipeline:
-    """Re-plans a packed batch every step without stalling the GPU.
-
-    The host planner writes the tile and run lists into one of two pinned
-    staging slots and the lists are uploaded with asynchronous copies on the
-    current stream, followed by hsap_doc_start.  A slot is reused only after
-    the event recorded behind its last copy has completed, so the host can
-    plan step i+1 while the GPU still runs step i.  Device list buffers are
-    single: stream order puts each step's upload after the previous step's
-    kernels.  The split length is fixed when the pipeline is built (partial
-    buffers are sized for it); after ``step`` the ShardAttention's lists point
-    at the new plan.
-    """
-
-    def __init__(self, sa: ShardAttention, backward: bool = False):
-        self.sa = sa
-        self.backward = backward
-        s = sa.shard
-        nq, nk = sa.n // s.block_m, sa.n // s.block_n
-        self.cap_tiles = sa.P * nq * nk
-        first = L.plan(sa.cu_host, s)
-        self.split = sa._split(len(first["tiles"]))
-        pieces = -(-nk // self.split) if self.split > 0 else 1
-        sa.split = self.split
-        sa.num_slots = sa.P * pieces
-        cap_rq, cap_rk = sa.P * nq * pieces, sa.P * nk
-        dev = sa.device
-
-        def pinned(count):
-            return torch.empty(count, dtype=torch.int32, pin_memory=True)
-
-        self.slots = []
-        for _ in range(2):
-            slot = {"tiles": pinned(self.cap_tiles * 4), "sorted_q": pinned(self.cap_tiles * 4),
-                    "runs_q": pinned(cap_rq * 4), "cu": pinned(len(sa.cu_host)), "event": torch.cuda.Event()}
-            if backward:
-                slot["sorted_k"] = pinned(self.cap_tiles * 4)
-                slot["runs_k"] = pinned(cap_rk * 4)
-            slot["event"].record()
-            self.slots.append(slot)
-        self.offs = np.zeros(sa.P + 1, dtype=np.int64)
-        self.pairs = np.zeros(sa.P, dtype=np.int64)
-        self.dev_tiles_q = torch.empty(self.cap_tiles * 4, dtype=torch.int32, device=dev)
-        self.dev_runs_q = torch.empty(cap_rq * 4, dtype=torch.int32, device=dev)
-        if backward:
-            self.dev_tiles_k = torch.empty(self.cap_tiles * 4, dtype=torch.int32, device=dev)
-            self.dev_runs_k = torch.empty(cap_rk * 4, dtype=torch.int32, device=dev)
-        self.dev_cu = torch.empty(len(sa.cu_host), dtype=torch.int32, device=dev)
-        sa.doc_start = torch.empty(sa.N, dtype=torch.int32, device=dev)
-        self.count = 0
-
-    def step(self, cu_seqlens: Optional[np.ndarray] = None) -> None:
-        sa = self.sa
-        slot = self.slots[self.count % 2]
-        self.count += 1
-        slot["event"].synchronize()              # the slot's previous upload has completed
-        cu = slot["cu"].numpy()
-        cu[:] = sa.cu_host if cu_seqlens is None else cu_seqlens
-        tiles = slot["tiles"].numpy().reshape(-1, 4)
-        T = L.plan_into(cu, sa.shard, tiles, self.offs, self.pairs)
-        sorted_q = slot["sorted_q"].numpy().reshape(-1, 4)
-        runs_q = slot["runs_q"].numpy().reshape(-1, 4)
-        R, _ = L.plan_runs_into(sa.shard, tiles, T, L.MAJOR_Q, self.split, sorted_q, runs_q)
-        self.dev_tiles_q[: T * 4].copy_(slot["sorted_q"][: T * 4], non_blocking=True)
-        self.dev_runs_q[: R * 4].copy_(slot["runs_q"][: R * 4], non_blocking=True)
-        if self.backward:
-            sorted_k = slot["sorted_k"].numpy().reshape(-1, 4)
-            runs_k = slot["runs_k"].numpy().reshape(-1, 4)
-            RK, _ = L.plan_runs_into(sa.shard, tiles, T, L.MAJOR_K, 0, sorted_k, runs_k)
-            self.dev_tiles_k[: T * 4].copy_(slot["sorted_k"][: T * 4], non_blocking=True)
-            self.dev_runs_k[: RK * 4].copy_(slot["runs_k"][: RK * 4], non_blocking=True)
-            sa.tiles_k = self.dev_tiles_k[: T * 4]
-            sa.runs_k = self.dev_runs_k[: RK * 4]
-        self.dev_cu.copy_(slot["cu"], non_blocking=True)
-        slot["event"].record()
-        L.doc_start(self.dev_cu, sa.N, sa.doc_start)
-        sa.tiles_q = self.dev_tiles_q[: T * 4]
-        sa.runs_q = self.dev_runs_q[: R * 4]
-        sa.step_offsets = self.offs.copy()
-        sa.useful_pairs = self.pairs.copy()
-        sa.chunks = [(sa.shard.shard_id - st) % sa.P for st in range(sa.P)]
-        sa.present = sorted(set(runs_q[:R, 0].tolist()))
-        sa.planned = True
 
 
 def to_sharded(shard: L.ShardDesc, x: torch.Tensor) -> torch.Tensor:

@@ -79,6 +79,43 @@ class Case:
         torch.cuda.synchronize()
         return out
 
+    def run_executor(self, max_run_tiles: int = -1, cu=None) -> Dict[str, np.ndarray]:
+        """The same shard through one hsap_executor: plan, forward (partial + merge, and
+        fused), backward when the case has one.  ``cu`` plans other documents on the
+        same inputs."""
+        s = L.shard_desc(self.N, self.P, self.layout, self.shard, self.bm, self.bn)
+        desc = L.attn_desc(s, self.hq, self.hkv, self.d, 1.0 / float(np.sqrt(self.d)))
+        ex = L.Executor(desc, backward=self.backward, fused=True, max_run_tiles=max_run_tiles)
+        try:
+            dev = torch.device("cuda")
+            q_sh = to_sharded(s, self.q.to(dev))[self.shard].contiguous()
+            k_sh = to_sharded(s, self.k.to(dev))
+            v_sh = to_sharded(s, self.v.to(dev))
+            ex.plan(self.cu if cu is None else cu)
+            n = self.N // self.P
+            o = torch.full((n, self.hq, self.d), float("nan"), dtype=torch.bfloat16, device=dev)
+            lse = torch.full((self.hq, n), float("nan"), dtype=torch.float32, device=dev)
+            ex.forward(q_sh, k_sh, v_sh, o, lse)
+            of, lsef = torch.full_like(o, float("nan")), torch.full_like(lse, float("nan"))
+            ex.forward(q_sh, k_sh, v_sh, of, lsef, fused=True)
+            os_, lses = torch.full_like(o, float("nan")), torch.full_like(lse, float("nan"))
+            ex.partial_forward(q_sh, k_sh, v_sh)     # the same forward as two stage calls
+            ex.merge(os_, lses)
+            out = {"info": ex.info(), "o": o.float().cpu().numpy(), "lse": lse.cpu().numpy(),
+                   "o_fused": of.float().cpu().numpy(), "lse_fused": lsef.cpu().numpy(),
+                   "o_staged": os_.float().cpu().numpy(), "lse_staged": lses.cpu().numpy()}
+            if self.backward:
+                do_sh = to_sharded(s, self.do.to(dev))[self.shard].contiguous()
+                dq = torch.full_like(q_sh, float("nan"))
+                dk, dv = torch.full_like(k_sh, float("nan")), torch.full_like(v_sh, float("nan"))
+                ex.backward(q_sh, k_sh, v_sh, do_sh, o, lse, dq, dk, dv)
+                out.update({"dq": dq.float().cpu().numpy(), "dk": dk.float().cpu().numpy(),
+                            "dv": dv.float().cpu().numpy()})
+            torch.cuda.synchronize()
+            return out
+        finally:
+            ex.close()
+
     # --------------------------------------------------------------- oracle
     def run_oracle(self, rows=None) -> Dict:
         q, k, v = self.q.float().numpy(), self.k.float().numpy(), self.v.float().numpy()

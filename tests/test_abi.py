@@ -184,3 +184,32 @@ def test_merge_and_helpers_validate():
     assert lib.hsap_shard_gather(ctypes.byref(d), fake, fake, 16, None) == L.HSAP_ERR_INVALID_ARG
     d = L.shard_desc(96, 3, "contiguous", 0, 1, 1)
     assert lib.hsap_shard_gather(ctypes.byref(d), fake, fake, 12, None) == L.HSAP_ERR_INVALID_ARG
+
+
+def test_executor_struct_layout():
+    assert ctypes.sizeof(L.ExecInfo) == 64
+
+
+def test_executor_validates_before_touching_the_device():
+    lib = L.lib()
+    good = L.attn_desc(L.shard_desc(2048, 2, "contiguous", 0, 128, 128), 4, 4, 128, 0.1)
+    h = ctypes.c_void_p(123)
+    # no output pointer, a malformed shard, an unsupported head_dim, unknown options, a bad split
+    assert lib.hsap_executor_create(ctypes.byref(good), 0, -1, None) == L.HSAP_ERR_INVALID_ARG
+    bad_shard = L.attn_desc(L.shard_desc(2047, 2, "contiguous", 0, 128, 128), 4, 4, 128, 0.1)
+    assert lib.hsap_executor_create(ctypes.byref(bad_shard), 0, -1, ctypes.byref(h)) == L.HSAP_ERR_INVALID_ARG
+    assert h.value is None                                   # *out cleared on failure
+    bad_d = L.attn_desc(L.shard_desc(2048, 2, "contiguous", 0, 128, 128), 4, 4, 96, 0.1)
+    assert lib.hsap_executor_create(ctypes.byref(bad_d), 0, -1, ctypes.byref(h)) == L.HSAP_ERR_UNSUPPORTED
+    assert lib.hsap_executor_create(ctypes.byref(good), 4, -1, ctypes.byref(h)) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_executor_create(ctypes.byref(good), 0, -2, ctypes.byref(h)) == L.HSAP_ERR_INVALID_ARG
+    # calls on a NULL executor
+    cu = np.asarray([0, 2048], dtype=np.int32)
+    assert lib.hsap_executor_plan(None, cu.ctypes.data, 1, None) == L.HSAP_ERR_INVALID_ARG
+    info = L.ExecInfo()
+    assert lib.hsap_executor_info(None, ctypes.byref(info)) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_executor_forward(None, 1, 1, 1, 0, 1, 1, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_executor_backward(None, 1, 1, 1, 1, 1, 1, 1, 1, 1, None) == L.HSAP_ERR_INVALID_ARG
+    lib.hsap_executor_destroy(None)                          # no-op
+    assert lib.hsap_executor_partial_forward(None, 1, 1, 1, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_executor_merge(None, 1, 1, None) == L.HSAP_ERR_INVALID_ARG

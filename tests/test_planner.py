@@ -103,6 +103,17 @@ def _runs_ok(shard, tiles, sorted_tiles, runs, major, split=0, num_slots=None):
     assert np.all(np.diff(counts) <= 0)           # longest first
     key = lambda a: sorted(map(tuple, a.tolist()))
     assert key(sorted_tiles) == key(tiles)        # sorted_tiles is a permutation of tiles
+    # the documented order of the whole list
+    st = ((shard.shard_id - sorted_tiles[:, 0]) % P).astype(np.int64)
+    nk = shard.total_tokens // P // shard.block_n
+    if major == L.MAJOR_K:
+        order = (st * nk + sorted_tiles[:, 2]) * nq + sorted_tiles[:, 1]
+        assert np.all(np.diff(order) > 0)
+    elif major == L.MAJOR_Q_ALL:
+        order = (sorted_tiles[:, 1].astype(np.int64) * P + st) * nk + sorted_tiles[:, 2]
+        assert np.all(np.diff(order) > 0)
+    else:
+        assert np.array_equal(sorted_tiles, tiles)
     if major == L.MAJOR_Q_ALL:
         # one run per q-tile over all chunks, its tiles in ring order
         assert sorted(runs[:, 1].tolist()) == list(range(nq)) and np.all(runs[:, 0] == 0)
