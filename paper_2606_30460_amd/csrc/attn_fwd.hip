@@ -302,9 +302,12 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   if (num_runs < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_runs < 0");
   const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
   if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
-  const bool shape_ok = (d == 128 || d == 64) && (bn == 128 || bn == 64) && (bm == 128 || bm == 64);
+  const bool shape_ok = (d == 128 || d == 64) && (bn == 128 || bn == 64) &&
+                        (bm == 128 || bm == 64 || (bm == 256 && d == 128));
   if (!shape_ok)
-    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no forward kernel for head_dim=%d BM=%d BN=%d (BM, BN in {64, 128})", d, bm, bn);
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED,
+              "no forward kernel for head_dim=%d BM=%d BN=%d (BM in {64, 128}, or 256 with d = 128; BN in {64, 128})",
+              d, bm, bn);
   if (num_runs == 0) return HSAP_OK;
   if (!q || !k || !v || !doc_start || !tiles || !runs) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v) & 15)
@@ -323,6 +326,8 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
 #define HSAP_FWD_CASE(D_, BN_, W_) \
   if (d == D_ && bn == BN_ && bm == 32 * W_) return launch<D_, BN_, W_, FUSED>(a, num_runs, s);
+  HSAP_FWD_CASE(128, 128, 8)
+  HSAP_FWD_CASE(128, 64, 8)
   HSAP_FWD_CASE(128, 128, 4)
   HSAP_FWD_CASE(128, 64, 4)
   HSAP_FWD_CASE(128, 128, 2)

@@ -12,7 +12,14 @@ using namespace hsap;
 
 namespace {
 
-constexpr int kFwdWorkgroupsPerCU = 2;  // two 4-wave forward workgroups share a compute unit
+// Forward workgroups resident per compute unit: the kernel runs two waves per SIMD (eight
+// per CU, BM / 32 per workgroup) and double-buffers 64-key K and V steps in LDS (rows padded
+// by 8 and 32 elements) out of 160 KiB.
+int fwd_resident_per_cu(int bm, int d) {
+  const int by_waves = std::max(1, 8 / std::max(1, bm / 32));
+  const int lds = 2 * 64 * (d + 8) * 2 + 2 * 64 * (d + 32) * 2;
+  return std::min(by_waves, std::max(1, 160 * 1024 / lds));
+}
 
 // Device or pinned allocation that grows (never shrinks) to the largest size asked for.
 struct DevBuf {
@@ -179,7 +186,7 @@ hsap_status hsap_executor_create(const hsap_attn_desc* desc, int32_t options, in
     release(ex);
     return hip_fail("create", e);
   }
-  ex->resident_workgroups = kFwdWorkgroupsPerCU * std::max(cus, 1);
+  ex->resident_workgroups = fwd_resident_per_cu(desc->shard.block_m, desc->head_dim) * std::max(cus, 1);
   *out = ex;
   return HSAP_OK;
 }

@@ -45,6 +45,8 @@ SMALL = [
     (4096, 8, "zigzag", 4, 4, 64, 64, 64, 40),
     (2048, 2, "zigzag", 2, 2, 128, 64, 64, 5),
     (3072, 3, "contiguous", 6, 3, 64, 128, 64, 3000),
+    (4096, 2, "zigzag", 4, 2, 128, 256, 128, 700),
+    (4096, 4, "contiguous", 2, 2, 128, 256, 64, 300),
 ]
 
 
