@@ -1,6 +1,8 @@
 // Memory-bound kernels of libhsap: the LSE merge of partial results, the
 // backward's row term delta = rowsum(dO * O), fp32 -> bf16 conversion, the
 // per-position document start, and the gather into sharded order.
+#include <algorithm>
+
 #include "hsap_internal.h"
 #include "mfma.h"
 
@@ -9,12 +11,10 @@ namespace hsap {
 // ---------------------------------------------------------------------------
 // LSE merge (online-softmax combination of the ring's partial results)
 //
-// Thread layout: D/4 consecutive lanes own one (row, head) item and 4
-// consecutive d each, so an item of a partial is one contiguous 4*D-byte
-// read.  Each thread carries ITEMS items spaced a grid apart and issues the
-// LSE loads of all of them, then the O loads of all of them, before using
-// any: the merge is HBM-bound and needs many bytes in flight.  Parts whose
-// LSE is -inf are never read.
+// Work unit: one wave merges one head's 16 consecutive rows, so the LSE values
+// it reads and writes per part are one 64-byte line, and each O row (D fp32
+// per part) is read by D/4 lanes, 16 bytes each.  Parts whose LSE is -inf
+// are never read.
 // ---------------------------------------------------------------------------
 struct MergeArgs {
   const float* o[HSAP_MAX_MERGE_PARTS];
@@ -26,6 +26,75 @@ struct MergeArgs {
   float* lse_out;
 };
 
+// Few parts (num_parts <= PR): one wave merges one head's 16 consecutive rows.
+// Lane i reads (and finally writes) the LSE of row i & 15, so each part's LSE
+// values for the group are one 64-byte line; the per-row weights then move to
+// the lanes that handle the O rows (2 rows of D fp32 per wave instruction, D/4
+// lanes per row) with a lane permute.  Each instruction's loads for every part
+// are issued together; few registers per wave keep many waves resident, which
+// is what keeps the loads in flight (holding a whole group's loads per wave
+// measured slower).
+template <int D, int PR>
+__global__ __launch_bounds__(256) void lse_merge_few_kernel(MergeArgs a) {
+  constexpr int RPI = 256 / D;              // rows per wave instruction: 64 lanes x 4 floats / D
+  constexpr int STEPS = 16 / RPI;           // instructions per 16-row group
+  constexpr float NEG_INF = -__builtin_inff();
+  constexpr float LOG2E = 1.44269504088896340736f;
+  constexpr float LN2 = 0.69314718055994530942f;
+  const int lane = threadIdx.x & 63;
+  const int64_t groups_per_head = (a.n + 15) / 16;
+  const int64_t groups = groups_per_head * a.hq;
+  const int64_t wave0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) / 64;
+  const int64_t waves = (int64_t)gridDim.x * 4;
+  const int sub = lane / (D / 4);           // which row of an instruction this lane serves
+  const int d0 = 4 * (lane % (D / 4));      // its 4 consecutive d
+  for (int64_t grp = wave0; grp < groups; grp += waves) {
+    const int64_t h = grp / groups_per_head;
+    const int64_t r0 = (grp - h * groups_per_head) * 16;
+    // LSE of row r0 + (lane & 15) for every part
+    const int64_t my_row = r0 + (lane & 15);
+    const bool row_ok = my_row < a.n;
+    float l[PR];
+#pragma unroll
+    for (int p = 0; p < PR; ++p) l[p] = (p < a.num_parts && row_ok) ? a.lse[p][h * a.n + my_row] * LOG2E : NEG_INF;
+    float mx = l[0];
+#pragma unroll
+    for (int p = 1; p < PR; ++p) mx = fmaxf(mx, l[p]);
+    float sum = 0.f;
+#pragma unroll
+    for (int p = 0; p < PR; ++p) sum += l[p] == NEG_INF ? 0.f : fast_exp2(l[p] - mx);
+    const float L2 = mx == NEG_INF ? NEG_INF : mx + __log2f(sum);
+    float wl[PR];
+#pragma unroll
+    for (int p = 0; p < PR; ++p) wl[p] = l[p] == NEG_INF ? 0.f : fast_exp2(l[p] - L2);
+    // O rows: instruction k covers rows r0 + RPI * k + sub
+#pragma unroll
+    for (int k = 0; k < STEPS; ++k) {
+      const int j = RPI * k + sub;  // row within the group; its weights live in lane j
+      const int64_t row = r0 + j;
+      float w[PR];
+      f32x4 x[PR];
+#pragma unroll
+      for (int p = 0; p < PR; ++p) {
+        w[p] = __int_as_float(__builtin_amdgcn_ds_bpermute(4 * j, __float_as_int(wl[p])));
+        x[p] = (w[p] > 0.f && row < a.n) ? *(const f32x4*)(a.o[p] + (row * a.hq + h) * D + d0)
+                                         : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      if (row >= a.n) continue;
+      f32x4 acc{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int p = 0; p < PR; ++p) acc += w[p] * x[p];
+      const bf16x4 out{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+      *(bf16x4*)(a.o_out + (row * a.hq + h) * D + d0) = out;
+    }
+    if (lane < 16 && row_ok) a.lse_out[h * a.n + my_row] = L2 == NEG_INF ? NEG_INF : L2 * LN2;
+  }
+}
+
+// Any number of parts: D/4 consecutive lanes own one (row, head) item, 4
+// consecutive d each; each thread carries ITEMS items spaced a grid apart and
+// issues the LSE loads of all of them, then the O loads of all of them, before
+// using any.  (For many parts this measured faster than the 16-row groups.)
 template <int D, int ITEMS>
 __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
   constexpr int TPR = D / 4;
@@ -227,13 +296,28 @@ hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const
   a.n = n;
   a.o_out = (__bf16*)o_out;
   a.lse_out = lse_out;
-  constexpr int ITEMS = 4;
-  const int64_t threads = n * heads_q * (head_dim / 4);
-  const int64_t blocks = (threads + 256 * ITEMS - 1) / (256 * ITEMS);
-  if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "problem too large");
   hipStream_t s = (hipStream_t)hip_stream;
-  if (head_dim == 128) hipLaunchKernelGGL((lse_merge_kernel<128, ITEMS>), dim3((unsigned)blocks), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((lse_merge_kernel<64, ITEMS>), dim3((unsigned)blocks), dim3(256), 0, s, a);
+  const dim3 block(256);
+  if (num_parts <= 4) {
+    // one wave per (head, 16 rows) group, four waves per block, grid-stride beyond 65536 blocks
+    const int64_t groups = ((n + 15) / 16) * heads_q;
+    const dim3 grid((unsigned)std::min<int64_t>((groups + 3) / 4, 65536));
+    if (head_dim == 128) {
+      if (num_parts <= 2) hipLaunchKernelGGL((lse_merge_few_kernel<128, 2>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((lse_merge_few_kernel<128, 4>), grid, block, 0, s, a);
+    } else {
+      if (num_parts <= 2) hipLaunchKernelGGL((lse_merge_few_kernel<64, 2>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((lse_merge_few_kernel<64, 4>), grid, block, 0, s, a);
+    }
+  } else {
+    constexpr int ITEMS = 4;
+    const int64_t threads = n * heads_q * (head_dim / 4);
+    const int64_t blocks = (threads + 256 * ITEMS - 1) / (256 * ITEMS);
+    if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "problem too large");
+    const dim3 grid((unsigned)blocks);
+    if (head_dim == 128) hipLaunchKernelGGL((lse_merge_kernel<128, ITEMS>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((lse_merge_kernel<64, ITEMS>), grid, block, 0, s, a);
+  }
   return check_launch("lse_merge");
 }
 
