@@ -300,10 +300,15 @@ hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, 
  *   lse        device fp32 [Hq, n]: the merged forward LSE.
  *   delta      device fp32 [Hq, n] from hsap_attn_bwd_preprocess.
  *   tiles_k, runs_k, num_runs_k  device lists from hsap_plan_runs(MAJOR_K).
- *   tiles_q, runs_q, num_runs_q  device lists from hsap_plan_runs(MAJOR_Q)
- *              (the forward's lists, split or not).
- *   dq_acc     device fp32 [n, Hq, d] (+=).  Each q-major run adds its
- *              contribution with one fp32 atomic add per element.
+ *   tiles_q, runs_q, num_runs_q  device q-tile runs in which no q_tile
+ *              appears twice: hsap_plan_runs(MAJOR_Q_ALL) (every chunk in
+ *              one pass), or the runs of one chunk from
+ *              hsap_plan_runs(MAJOR_Q) with max_run_tiles = 0 (one ring
+ *              step).  A run may span several chunks.
+ *   dq_acc     device fp32 [n, Hq, d] (+=).  Each run owns its q-tile's rows
+ *              for the call: plain read-modify-write, no atomics (so runs
+ *              sharing a q-tile, e.g. split pieces, must go to separate
+ *              calls).
  *   dk_acc, dv_acc  device fp32 [P, n, Hkv, d] sharded order (+=).  Each
  *              (chunk, k_tile, K/V head) row block is owned by one
  *              workgroup: plain read-modify-write.
@@ -316,6 +321,29 @@ hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, con
                                   const hsap_tile* tiles_k, const hsap_run* runs_k, int64_t num_runs_k,
                                   const hsap_tile* tiles_q, const hsap_run* runs_q, int64_t num_runs_q,
                                   float* dq_acc, float* dk_acc, float* dv_acc, void* hip_stream);
+
+/*
+ * hsap_attn_bwd_bf16 -- hsap_partial_attn_bwd over every chunk in one pass
+ * with the finalisation fused: each q-tile and each (chunk, k_tile, K/V
+ * head) block has exactly one owning run, so its gradient is complete in
+ * registers and stored once, as bf16 (round to nearest even), instead of
+ * being added to fp32 accumulators and converted afterwards.
+ *
+ *   desc, q, k, v, d_o, lse, delta, doc_start  as for hsap_partial_attn_bwd
+ *              (same supported shapes).
+ *   tiles_k, runs_k, num_runs_k  hsap_plan_runs(MAJOR_K) lists.
+ *   tiles_q, runs_q, num_runs_q  hsap_plan_runs(MAJOR_Q_ALL) lists.
+ *   dq         device bf16 [n, Hq, d], 8-byte aligned: the rows of every
+ *              q-tile of runs_q are written (0 where a q-tile has no key).
+ *   dk, dv     device bf16 [P, n, Hkv, d] sharded order: the rows of every
+ *              (chunk, k_tile) with a k-major run are written; all other
+ *              rows are left untouched (the caller zeroes them).
+ */
+hsap_status hsap_attn_bwd_bf16(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                               const void* d_o, const float* lse, const float* delta, const int32_t* doc_start,
+                               const hsap_tile* tiles_k, const hsap_run* runs_k, int64_t num_runs_k,
+                               const hsap_tile* tiles_q, const hsap_run* runs_q, int64_t num_runs_q, void* dq,
+                               void* dk, void* dv, void* hip_stream);
 
 /*
  * hsap_convert_f32_bf16 -- dst[i] = bf16(src[i]), round to nearest even
@@ -335,8 +363,8 @@ hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, vo
  * An executor owns: two pinned staging buffers for the planner's lists, one
  * device list buffer, the device doc_start array, the fp32 partial outputs
  * of the forward (grown to the largest plan seen) and, with
- * HSAP_EXEC_BACKWARD, the backward's fp32 accumulators and delta.  Buffers
- * grow on demand; a growth synchronises the stream first.
+ * HSAP_EXEC_BACKWARD, the backward's delta.  Buffers grow on demand; a
+ * growth synchronises the stream first.
  *
  * Threading and streams: one executor is used by one host thread at a time,
  * on one device (the device current at creation), and all its calls should
@@ -348,7 +376,7 @@ typedef struct hsap_executor hsap_executor;
 
 /* Options of hsap_executor_create (bit mask). */
 enum {
-  HSAP_EXEC_BACKWARD = 1,  /* also plan k-major runs and own backward workspace */
+  HSAP_EXEC_BACKWARD = 1,  /* also plan k-major and MAJOR_Q_ALL runs, own delta */
   HSAP_EXEC_FUSED = 2      /* also plan MAJOR_Q_ALL runs for the fused forward   */
 };
 
@@ -359,7 +387,7 @@ typedef struct {
   int64_t useful_pairs;     /* allowed (query, key) pairs per head           */
   int64_t num_runs_q;       /* q-major runs (forward, dQ)                    */
   int64_t num_runs_k;       /* k-major runs (dK, dV); 0 without BACKWARD     */
-  int64_t num_runs_all;     /* fused-forward runs; 0 without FUSED           */
+  int64_t num_runs_all;     /* MAJOR_Q_ALL runs; 0 without FUSED or BACKWARD */
   int32_t num_parts;        /* partial outputs the forward writes and merges */
   int32_t split_length;     /* max_run_tiles used for the q-major runs (0: none) */
   int32_t chunks_with_tiles;
@@ -425,9 +453,9 @@ hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, 
 
 /*
  * hsap_executor_backward -- gradients of the forward for the current plan
- * (needs HSAP_EXEC_BACKWARD): zeroes the executor's accumulators, then
- * hsap_attn_bwd_preprocess, hsap_partial_attn_bwd over the k-major and
- * q-major runs, and the conversion to bf16.
+ * (needs HSAP_EXEC_BACKWARD): zeroes dk and dv, then
+ * hsap_attn_bwd_preprocess and hsap_attn_bwd_bf16 over the k-major and
+ * MAJOR_Q_ALL runs.
  *   q, k, v  as for the forward;  d_o, o  device bf16 [n, Hq, d] (o: the
  *            forward's output);  lse  device fp32 [Hq, n] (the forward's).
  *   dq       device bf16 [n, Hq, d].

@@ -17,6 +17,7 @@ from ._lib import (  # noqa: F401
     Executor,
     HsapError,
     ShardDesc,
+    attn_bwd_bf16,
     attn_bwd_preprocess,
     attn_desc,
     attn_fwd_fused,

@@ -36,7 +36,7 @@ MAX_MERGE_PARTS = 64
 EXPORTED = (
     "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_doc_start",
     "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
-    "hsap_partial_attn_bwd", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
+    "hsap_partial_attn_bwd", "hsap_attn_bwd_bf16", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
     "hsap_executor_plan", "hsap_executor_info", "hsap_executor_forward", "hsap_executor_partial_forward",
     "hsap_executor_merge", "hsap_executor_backward",
 )
@@ -87,6 +87,7 @@ _SIG = {
     "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P,
                                              _P]),
+    "hsap_attn_bwd_bf16": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P, _P]),
     "hsap_convert_f32_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
     "hsap_executor_create": (ctypes.c_int, [_P, _I32, _I32, _P]),
     "hsap_executor_destroy": (None, [_P]),
@@ -352,6 +353,31 @@ def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, ti
                                        _ptr(delta), _ptr(doc_start_dev), _ptr(tiles_k_dev), _ptr(runs_k_dev), nk,
                                        _ptr(tiles_q_dev), _ptr(runs_q_dev), nq, _ptr(dq_acc), _ptr(dk_acc),
                                        _ptr(dv_acc), _stream(stream)))
+
+
+def attn_bwd_bf16(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_k_dev, runs_k_dev, tiles_all_dev,
+                  runs_all_dev, dq, dk, dv, stream=None) -> None:
+    """hsap_attn_bwd_bf16: final bf16 gradients over every chunk (MAJOR_K and MAJOR_Q_ALL lists)."""
+    s = desc.shard
+    n = s.total_tokens // s.sp_degree
+    hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
+    _dev(q, "bfloat16", "q", n * hq * d)
+    _dev(k, "bfloat16", "k", P * n * hkv * d)
+    _dev(v, "bfloat16", "v", P * n * hkv * d)
+    _dev(d_o, "bfloat16", "d_o", n * hq * d)
+    _dev(lse, "float32", "lse", hq * n)
+    _dev(delta, "float32", "delta", hq * n)
+    _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
+    for t, name in ((tiles_k_dev, "tiles_k"), (runs_k_dev, "runs_k"), (tiles_all_dev, "tiles_all"),
+                    (runs_all_dev, "runs_all")):
+        _dev(t, "int32", name)
+    _dev(dq, "bfloat16", "dq", n * hq * d)
+    _dev(dk, "bfloat16", "dk", P * n * hkv * d)
+    _dev(dv, "bfloat16", "dv", P * n * hkv * d)
+    _check(lib().hsap_attn_bwd_bf16(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(d_o), _ptr(lse), _ptr(delta),
+                                    _ptr(doc_start_dev), _ptr(tiles_k_dev), _ptr(runs_k_dev), runs_k_dev.numel() // 4,
+                                    _ptr(tiles_all_dev), _ptr(runs_all_dev), runs_all_dev.numel() // 4, _ptr(dq),
+                                    _ptr(dk), _ptr(dv), _stream(stream)))
 
 
 def convert_f32_bf16(src, dst, stream=None) -> None:

@@ -35,9 +35,12 @@ struct BwdArgs {
   const int32_t* doc_start;
   const hsap_tile* tiles;
   const hsap_run* runs;
-  float* dq;
+  float* dq;       // fp32 accumulators (+=), or
   float* dk;
   float* dv;
+  __bf16* dq16;    // final bf16 gradients (written once)
+  __bf16* dk16;
+  __bf16* dv16;
   Geom geom;
   int32_t shard;
   int32_t hq;
@@ -48,7 +51,7 @@ struct BwdArgs {
   float scale_log2;
 };
 
-template <int D, int WAVES>
+template <int D, int WAVES, bool BF16OUT>
 __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a) {
   constexpr int BN = 32 * WAVES;
   constexpr int NT = 64 * WAVES;
@@ -112,10 +115,39 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   const int nsub = a.bm / SUB;
   const int per_head = run.count * nsub;
   const int total = a.group * per_head;
-  // sub-tile `it`: query head, tile of the run, 64-row slice of the tile
+  // The run's q-tiles, packed one per lane (q_tile | kind << 31) in windows of 64 tiles, read
+  // with v_readlane: the next sub-tile's address never waits on a memory load.  Window v lives
+  // in win0 (v even) or win1 (v odd); sub-tiles visit the run's tiles in order once per query
+  // head, so the window is reloaded when the tile index leaves it.
+  uint32_t win0 = 0u, win1 = 0u;
+  int win_lo = 0, win_hi = -1;  // windows held: win_lo (and win_lo + 1 when win_hi > win_lo)
+  auto load_window = [&](int v) {
+    const int i = 64 * v + lane;
+    uint32_t p = 0;
+    if (i < run.count) {
+      const hsap_tile t = a.tiles[run.first + i];
+      p = (uint32_t)t.q_tile | ((uint32_t)t.kind << 31);
+    }
+    if (v & 1) win1 = p;
+    else win0 = p;
+  };
+  auto ensure_window = [&](int v) {  // v is the window of the next tile index needed
+    if (v >= win_lo && v <= win_hi) return;
+    load_window(v);
+    if (v == win_hi + 1 && v - 1 >= win_lo) win_lo = v - 1;
+    else win_lo = v;
+    win_hi = v;
+  };
+  // sub-tile `it`: query head, tile of the run (packed), 64-row slice of the tile
   auto head_of = [&](int it) { return g * a.group + it / per_head; };
-  auto tile_of = [&](int it) { return a.tiles[run.first + (it % per_head) / nsub]; };
-  auto q0_of = [&](const hsap_tile& t, int it) { return (int64_t)t.q_tile * a.bm + ((it % per_head) % nsub) * SUB; };
+  auto tile_of = [&](int it) -> uint32_t {
+    const int idx = (it % per_head) / nsub;
+    return __builtin_amdgcn_readlane(((idx >> 6) & 1) ? win1 : win0, idx & 63);
+  };
+  auto q0_of = [&](uint32_t t, int it) {
+    return (int64_t)(t & 0x7FFFFFFFu) * a.bm + ((it % per_head) % nsub) * SUB;
+  };
+  ensure_window(0);
 
   // staging of one sub-tile: Q and dO rows, and the per-row LSE, delta and document start
   int32_t soff[PER_T], loff[PER_T];
@@ -130,7 +162,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   int32_t sreg = 0;
   auto load_sub = [&](int it) {
     const int h = head_of(it);
-    const hsap_tile t = tile_of(it);
+    ensure_window(((it % per_head) / nsub) >> 6);
+    const uint32_t t = tile_of(it);
     const int64_t q0 = q0_of(t, it);
     const int64_t base = (q0 * a.hq + h) * D;
 #pragma unroll
@@ -164,10 +197,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   for (int it = 0; it < total; ++it) {
     const int buf = it & 1;
     const int h = head_of(it);
-    const hsap_tile tile = tile_of(it);
+    const uint32_t tile = tile_of(it);
     const int64_t q0 = q0_of(tile, it);
     const int32_t gq0 = (int32_t)global_pos(a.geom, a.shard, q0);
-    const bool masked = tile.kind == HSAP_TILE_MASKED;
+    const bool masked = (tile >> 31) != 0;
     if (it + 1 < total) load_sub(it + 1);
     const __bf16* Q = Qs[buf];
     const __bf16* O = dOs[buf];
@@ -228,13 +261,19 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   }
 
   // this workgroup owns rows [krow0, krow0 + BN) of chunk c for K/V head g: plain read-add-write
+  // of the fp32 accumulators, or a store of the final bf16 values
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int64_t idx = ((kvrow + 32 * w + c_row(j, hi)) * a.hkv + g) * D + 32 * mb + l32;
-      a.dk[idx] += dk[mb][j] * a.scale;
-      a.dv[idx] += dv[mb][j];
+      if (BF16OUT) {
+        a.dk16[idx] = (__bf16)(dk[mb][j] * a.scale);
+        a.dv16[idx] = (__bf16)dv[mb][j];
+      } else {
+        a.dk[idx] += dk[mb][j] * a.scale;
+        a.dv[idx] += dv[mb][j];
+      }
     }
 }
 
@@ -245,10 +284,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
 // are scalars of the lane.  Per step of 64 keys:
 //   P^T = exp2(S^T * scale*log2e - LSE*log2e), dS^T = P^T o (dP^T - delta),
 //   dQ^T += K^T dS^T (K^T read transposed from the [key][d] tile).
-// dQ stays in registers for the whole run and is added to dq_acc once at the
-// end (a q-tile meets one run per chunk, so at most P adds per element).
+// A run may span several chunks (tile by tile), so one run per q-tile covers
+// every chunk; dQ stays in registers for the whole run and is written once at
+// the end, by the q-tile's only run: a plain read-add-write of the fp32
+// accumulator, or a store of the final bf16 value.
 // ---------------------------------------------------------------------------
-template <int D, int BN, int WAVES>
+template <int D, int BN, int WAVES, bool BF16OUT>
 __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
   constexpr int KB = 64;                     // keys per step
   constexpr int SUBS = BN / KB;
@@ -268,11 +309,17 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
   const int run_idx = blockIdx.x / a.hq;
   const int h = blockIdx.x - run_idx * a.hq;
   const hsap_run run = a.runs[run_idx];
-  if (run.count == 0) return;
-  const int c = a.tiles[run.first].chunk;  // all tiles of a run belong to one chunk
   const int g = h / a.group;
   const int64_t n = a.geom.n;
   const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;
+  if (run.count == 0) {  // no key for this q-tile: dQ = 0
+    if (BF16OUT) {
+      bf16x4* dst = (bf16x4*)(a.dq16 + (qrow * a.hq + h) * D + 4 * hi);
+#pragma unroll
+      for (int e = 0; e < D / 8; ++e) dst[2 * e] = bf16x4{};
+    }
+    return;
+  }
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
   const int32_t qstart = a.doc_start[gq];
   const uint32_t span = (uint32_t)(gq - qstart);
@@ -299,8 +346,6 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
     for (int k = 0; k < 2; ++k) troff[mb][k] = swz<CPR>(8 * k + tr_row, 32 * mb + tr_col) - 8 * k * D;
 
   const int64_t rstride = (int64_t)a.hkv * D;
-  const __bf16* kbase = a.k + ((int64_t)c * n * a.hkv + g) * D;
-  const __bf16* vbase = a.v + ((int64_t)c * n * a.hkv + g) * D;
   const int total = run.count * SUBS;
   int32_t goff[PER_T], loff[PER_T];
 #pragma unroll
@@ -311,9 +356,11 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
   }
   bf16x8 kreg[PER_T], vreg[PER_T];
   auto step_row0 = [&](const hsap_tile& t, int s) { return (int64_t)t.k_tile * BN + (s % SUBS) * KB; };
-  auto load_step = [&](int64_t row0) {
-    const __bf16* kb = kbase + row0 * rstride;
-    const __bf16* vb = vbase + row0 * rstride;
+  // the step's rows in the sharded K/V buffers: chunk t.chunk, K/V head g
+  auto load_step = [&](const hsap_tile& t, int s) {
+    const int64_t off = (((int64_t)t.chunk * n + step_row0(t, s)) * a.hkv + g) * D;
+    const __bf16* kb = a.k + off;
+    const __bf16* vb = a.v + off;
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
       kreg[i] = *(const bf16x8*)(kb + goff[i]);
@@ -333,7 +380,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
   for (int mb = 0; mb < MB; ++mb) dq[mb] = f32x16{};
 
   hsap_tile cur = a.tiles[run.first];
-  load_step(step_row0(cur, 0));
+  load_step(cur, 0);
   store_step(0);
   hsap_tile nxt = cur;
   if (run.count > 1) nxt = a.tiles[run.first + 1];
@@ -347,12 +394,12 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
         cur = nxt;
         if ((s + 1) / SUBS + 1 < run.count) nxt = a.tiles[run.first + (s + 1) / SUBS + 1];
       }
-      load_step(step_row0(cur, s + 1));
+      load_step(cur, s + 1);
     }
     const __bf16* K = Ks[buf];
     const __bf16* V = Vs[buf];
     const bool masked = tile.kind == HSAP_TILE_MASKED;
-    const int32_t rel0 = masked ? (int32_t)global_pos(a.geom, c, step_row0(tile, s)) - qstart : 0;
+    const int32_t rel0 = masked ? (int32_t)global_pos(a.geom, tile.chunk, step_row0(tile, s)) - qstart : 0;
 #pragma unroll
     for (int nb = 0; nb < KB / 32; ++nb) {
       f32x16 st{}, dpt{};
@@ -383,31 +430,121 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
     __syncthreads();
   }
 
-  // dQ^T: this lane's query, d = 32 mb + c_row(j, hi); four consecutive d per register group
-  float* dst = a.dq + (qrow * a.hq + h) * D + 4 * hi;
+  // dQ^T: this lane's query, d = 32 mb + 8 grp + 4 hi + e for register j = 4 grp + e
+  const int64_t base = (qrow * a.hq + h) * D + 4 * hi;
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) unsafeAtomicAdd(dst + 32 * mb + 8 * (j >> 2) + (j & 3), dq[mb][j] * a.scale);
+    for (int grp = 0; grp < 4; ++grp) {
+      const f32x4 val{dq[mb][4 * grp] * a.scale, dq[mb][4 * grp + 1] * a.scale, dq[mb][4 * grp + 2] * a.scale,
+                      dq[mb][4 * grp + 3] * a.scale};
+      if (BF16OUT) {
+        *(bf16x4*)(a.dq16 + base + 32 * mb + 8 * grp) = bf16x4{(__bf16)val[0], (__bf16)val[1], (__bf16)val[2],
+                                                               (__bf16)val[3]};
+      } else {
+        f32x4* dst = (f32x4*)(a.dq + base + 32 * mb + 8 * grp);
+        *dst = *dst + val;
+      }
+    }
 }
 
-template <int D, int WAVES>
+template <int D, int WAVES, bool BF16OUT>
 static hsap_status launch_dkdv(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hkv;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, WAVES>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, WAVES, BF16OUT>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream,
+                     a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_bwd_dkdv launch: %s", hipGetErrorString(e));
   return HSAP_OK;
 }
 
-template <int D, int BN, int WAVES>
+template <int D, int BN, int WAVES, bool BF16OUT>
 static hsap_status launch_dq(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, BN, WAVES>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, BN, WAVES, BF16OUT>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream,
+                     a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_bwd_dq launch: %s", hipGetErrorString(e));
+  return HSAP_OK;
+}
+
+
+// shared checks and dispatch of the fp32-accumulating and the bf16-storing backward
+template <bool BF16OUT>
+static hsap_status backward(const hsap_attn_desc* desc, const void* q, const void* k, const void* v, const void* d_o,
+                            const float* lse, const float* delta, const int32_t* doc_start, const hsap_tile* tiles_k,
+                            const hsap_run* runs_k, int64_t num_runs_k, const hsap_tile* tiles_q,
+                            const hsap_run* runs_q, int64_t num_runs_q, void* dq, void* dk, void* dv,
+                            hipStream_t s) {
+  Geom geom;
+  hsap_status st = check_attn(desc, &geom);
+  if (st != HSAP_OK) return st;
+  if (num_runs_k < 0 || num_runs_q < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "negative run count");
+  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
+  if (bm % 64) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "backward needs BM a multiple of 64 (BM=%d)", bm);
+  const bool dkdv_ok = (d == 128 && (bn == 128 || bn == 64)) || (d == 64 && bn == 64);
+  const bool dq_ok = (bm == 128 || bm == 64) && (bn == 128 || bn == 64);
+  if (!dkdv_ok || !dq_ok)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no backward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
+  if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
+  if (num_runs_k == 0 && num_runs_q == 0) return HSAP_OK;
+  if (!q || !k || !v || !d_o || !lse || !delta || !doc_start || !dq || !dk || !dv ||
+      (num_runs_k > 0 && (!tiles_k || !runs_k)) || (num_runs_q > 0 && (!tiles_q || !runs_q)))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)d_o) & 15)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k, v and d_o must be 16-byte aligned");
+  if ((uintptr_t)dq & (BF16OUT ? 7 : 15))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "dq must be %d-byte aligned", BF16OUT ? 8 : 16);
+  BwdArgs a = {};
+  a.q = (const __bf16*)q;
+  a.k = (const __bf16*)k;
+  a.v = (const __bf16*)v;
+  a.d_o = (const __bf16*)d_o;
+  a.lse = lse;
+  a.delta = delta;
+  a.doc_start = doc_start;
+  if (BF16OUT) {
+    a.dq16 = (__bf16*)dq;
+    a.dk16 = (__bf16*)dk;
+    a.dv16 = (__bf16*)dv;
+  } else {
+    a.dq = (float*)dq;
+    a.dk = (float*)dk;
+    a.dv = (float*)dv;
+  }
+  a.geom = geom;
+  a.shard = desc->shard.shard_id;
+  a.hq = desc->heads_q;
+  a.hkv = desc->heads_kv;
+  a.group = desc->heads_q / desc->heads_kv;
+  a.bm = bm;
+  a.scale = desc->softmax_scale;
+  a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
+  if (num_runs_k > 0) {
+    a.tiles = tiles_k;
+    a.runs = runs_k;
+    if (d == 128 && bn == 128) st = launch_dkdv<128, 4, BF16OUT>(a, num_runs_k, s);
+    else if (d == 128) st = launch_dkdv<128, 2, BF16OUT>(a, num_runs_k, s);
+    else st = launch_dkdv<64, 2, BF16OUT>(a, num_runs_k, s);
+    if (st != HSAP_OK) return st;
+  }
+  if (num_runs_q > 0) {
+    a.tiles = tiles_q;
+    a.runs = runs_q;
+#define HSAP_DQ_CASE(D_, BN_, W_) \
+  if (d == D_ && bn == BN_ && bm == 32 * W_) return launch_dq<D_, BN_, W_, BF16OUT>(a, num_runs_q, s);
+    HSAP_DQ_CASE(128, 128, 4)
+    HSAP_DQ_CASE(128, 64, 4)
+    HSAP_DQ_CASE(128, 128, 2)
+    HSAP_DQ_CASE(128, 64, 2)
+    HSAP_DQ_CASE(64, 128, 4)
+    HSAP_DQ_CASE(64, 64, 4)
+    HSAP_DQ_CASE(64, 128, 2)
+    HSAP_DQ_CASE(64, 64, 2)
+#undef HSAP_DQ_CASE
+  }
   return HSAP_OK;
 }
 
@@ -422,65 +559,16 @@ extern "C" hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const v
                                              const hsap_run* runs_q, int64_t num_runs_q, float* dq_acc,
                                              float* dk_acc, float* dv_acc, void* hip_stream) {
   clear_error();
-  Geom geom;
-  hsap_status st = check_attn(desc, &geom);
-  if (st != HSAP_OK) return st;
-  if (num_runs_k < 0 || num_runs_q < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "negative run count");
-  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
-  if (bm % 64) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "backward needs BM a multiple of 64 (BM=%d)", bm);
-  const bool dkdv_ok = (d == 128 && (bn == 128 || bn == 64)) || (d == 64 && bn == 64);
-  const bool dq_ok = (bm == 128 || bm == 64) && (bn == 128 || bn == 64);
-  if (!dkdv_ok || !dq_ok)
-    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no backward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
-  if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
-  if (num_runs_k == 0 && num_runs_q == 0) return HSAP_OK;
-  if (!q || !k || !v || !d_o || !lse || !delta || !doc_start || !dq_acc || !dk_acc || !dv_acc ||
-      (num_runs_k > 0 && (!tiles_k || !runs_k)) || (num_runs_q > 0 && (!tiles_q || !runs_q)))
-    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
-  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)d_o) & 15)
-    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k, v and d_o must be 16-byte aligned");
-  BwdArgs a;
-  a.q = (const __bf16*)q;
-  a.k = (const __bf16*)k;
-  a.v = (const __bf16*)v;
-  a.d_o = (const __bf16*)d_o;
-  a.lse = lse;
-  a.delta = delta;
-  a.doc_start = doc_start;
-  a.dq = dq_acc;
-  a.dk = dk_acc;
-  a.dv = dv_acc;
-  a.geom = geom;
-  a.shard = desc->shard.shard_id;
-  a.hq = desc->heads_q;
-  a.hkv = desc->heads_kv;
-  a.group = desc->heads_q / desc->heads_kv;
-  a.bm = bm;
-  a.scale = desc->softmax_scale;
-  a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
-  hipStream_t s = (hipStream_t)hip_stream;
-  if (num_runs_k > 0) {
-    a.tiles = tiles_k;
-    a.runs = runs_k;
-    if (d == 128 && bn == 128) st = launch_dkdv<128, 4>(a, num_runs_k, s);
-    else if (d == 128) st = launch_dkdv<128, 2>(a, num_runs_k, s);
-    else st = launch_dkdv<64, 2>(a, num_runs_k, s);
-    if (st != HSAP_OK) return st;
-  }
-  if (num_runs_q > 0) {
-    a.tiles = tiles_q;
-    a.runs = runs_q;
-#define HSAP_DQ_CASE(D_, BN_, W_) \
-  if (d == D_ && bn == BN_ && bm == 32 * W_) return launch_dq<D_, BN_, W_>(a, num_runs_q, s);
-    HSAP_DQ_CASE(128, 128, 4)
-    HSAP_DQ_CASE(128, 64, 4)
-    HSAP_DQ_CASE(128, 128, 2)
-    HSAP_DQ_CASE(128, 64, 2)
-    HSAP_DQ_CASE(64, 128, 4)
-    HSAP_DQ_CASE(64, 64, 4)
-    HSAP_DQ_CASE(64, 128, 2)
-    HSAP_DQ_CASE(64, 64, 2)
-#undef HSAP_DQ_CASE
-  }
-  return HSAP_OK;
+  return backward<false>(desc, q, k, v, d_o, lse, delta, doc_start, tiles_k, runs_k, num_runs_k, tiles_q, runs_q,
+                         num_runs_q, dq_acc, dk_acc, dv_acc, (hipStream_t)hip_stream);
+}
+
+extern "C" hsap_status hsap_attn_bwd_bf16(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                          const void* d_o, const float* lse, const float* delta,
+                                          const int32_t* doc_start, const hsap_tile* tiles_k, const hsap_run* runs_k,
+                                          int64_t num_runs_k, const hsap_tile* tiles_q, const hsap_run* runs_q,
+                                          int64_t num_runs_q, void* dq, void* dk, void* dv, void* hip_stream) {
+  clear_error();
+  return backward<true>(desc, q, k, v, d_o, lse, delta, doc_start, tiles_k, runs_k, num_runs_k, tiles_q, runs_q,
+                        num_runs_q, dq, dk, dv, (hipStream_t)hip_stream);
 }

@@ -58,9 +58,6 @@ struct hsap_executor {
   int32_t* doc_start = nullptr;
   DevBuf o_part, lse_part;
   float* delta = nullptr;
-  float* dq_acc = nullptr;
-  float* dk_acc = nullptr;
-  float* dv_acc = nullptr;
 
   // current plan
   bool planned = false;
@@ -119,8 +116,7 @@ void release(hsap_executor* ex) {
     if (ex->pinned[i].p) hipHostFree(ex->pinned[i].p);
     if (ex->uploaded[i]) hipEventDestroy(ex->uploaded[i]);
   }
-  void* dev[] = {ex->lists.p, ex->doc_start, ex->o_part.p, ex->lse_part.p, ex->delta, ex->dq_acc, ex->dk_acc,
-                 ex->dv_acc};
+  void* dev[] = {ex->lists.p, ex->doc_start, ex->o_part.p, ex->lse_part.p, ex->delta};
   for (void* p : dev)
     if (p) hipFree(p);
   delete ex;
@@ -175,13 +171,8 @@ hsap_status hsap_executor_create(const hsap_attn_desc* desc, int32_t options, in
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ex->device);
   for (int i = 0; e == hipSuccess && i < 2; ++i) e = hipEventCreateWithFlags(&ex->uploaded[i], hipEventDisableTiming);
   if (e == hipSuccess) e = hipMalloc((void**)&ex->doc_start, (size_t)g.N * sizeof(int32_t));
-  if (e == hipSuccess && (options & HSAP_EXEC_BACKWARD)) {
-    const size_t rows_q = (size_t)g.n * desc->heads_q, rows_kv = (size_t)g.P * g.n * desc->heads_kv;
-    e = hipMalloc((void**)&ex->delta, rows_q * sizeof(float));
-    if (e == hipSuccess) e = hipMalloc((void**)&ex->dq_acc, rows_q * desc->head_dim * sizeof(float));
-    if (e == hipSuccess) e = hipMalloc((void**)&ex->dk_acc, rows_kv * desc->head_dim * sizeof(float));
-    if (e == hipSuccess) e = hipMalloc((void**)&ex->dv_acc, rows_kv * desc->head_dim * sizeof(float));
-  }
+  if (e == hipSuccess && (options & HSAP_EXEC_BACKWARD))
+    e = hipMalloc((void**)&ex->delta, (size_t)g.n * desc->heads_q * sizeof(float));
   if (e != hipSuccess) {
     release(ex);
     return hip_fail("create", e);
@@ -262,7 +253,7 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
     st = runs_for(ex, HSAP_MAJOR_K, 0, ex->sorted_k, ex->runs_k, &RK, nullptr);
     if (st != HSAP_OK) return st;
   }
-  if (ex->options & HSAP_EXEC_FUSED) {
+  if (ex->options & (HSAP_EXEC_FUSED | HSAP_EXEC_BACKWARD)) {  // fused forward and the backward's dQ
     st = runs_for(ex, HSAP_MAJOR_Q_ALL, 0, ex->sorted_all, ex->runs_all, &RA, nullptr);
     if (st != HSAP_OK) return st;
   }
@@ -384,31 +375,16 @@ hsap_status hsap_executor_backward(hsap_executor* ex, const void* q, const void*
   if (!q || !k || !v || !d_o || !o || !lse || !dq || !dk || !dv)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   const hipStream_t stream = (hipStream_t)hip_stream;
-  const int64_t n = ex->geom.n, hq = ex->desc.heads_q, hkv = ex->desc.heads_kv, d = ex->desc.head_dim;
-  const int64_t chunk_elems = n * hkv * d;
-  hsap_status st = zero_fill(ex->dq_acc, n * hq * d * (int64_t)sizeof(float), stream);
-  for (int32_t c = 0; st == HSAP_OK && c < ex->geom.P; ++c)
-    if (ex->chunk_has_tiles[(size_t)c]) {
-      st = zero_fill(ex->dk_acc + c * chunk_elems, chunk_elems * (int64_t)sizeof(float), stream);
-      if (st == HSAP_OK) st = zero_fill(ex->dv_acc + c * chunk_elems, chunk_elems * (int64_t)sizeof(float), stream);
-    }
+  const int64_t n = ex->geom.n, hq = ex->desc.heads_q, d = ex->desc.head_dim;
+  // dK/dV rows that no k-major run owns (chunks without tiles, k-tiles no query reaches) are zero
+  const int64_t kv_bytes = (int64_t)ex->geom.P * n * ex->desc.heads_kv * d * 2;
+  hsap_status st = zero_fill(dk, kv_bytes, stream);
+  if (st == HSAP_OK) st = zero_fill(dv, kv_bytes, stream);
   if (st == HSAP_OK) st = hsap_attn_bwd_preprocess(o, d_o, n, (int32_t)hq, (int32_t)d, ex->delta, hip_stream);
   if (st == HSAP_OK)
-    st = hsap_partial_attn_bwd(&ex->desc, q, k, v, d_o, lse, ex->delta, ex->doc_start, ex->d_tiles_k, ex->d_runs_k,
-                               ex->info.num_runs_k, ex->d_tiles_q, ex->d_runs_q, ex->info.num_runs_q, ex->dq_acc,
-                               ex->dk_acc, ex->dv_acc, hip_stream);
-  if (st == HSAP_OK) st = hsap_convert_f32_bf16(ex->dq_acc, dq, n * hq * d, hip_stream);
-  for (int32_t c = 0; st == HSAP_OK && c < ex->geom.P; ++c) {
-    __bf16* dkc = (__bf16*)dk + c * chunk_elems;
-    __bf16* dvc = (__bf16*)dv + c * chunk_elems;
-    if (ex->chunk_has_tiles[(size_t)c]) {
-      st = hsap_convert_f32_bf16(ex->dk_acc + c * chunk_elems, dkc, chunk_elems, hip_stream);
-      if (st == HSAP_OK) st = hsap_convert_f32_bf16(ex->dv_acc + c * chunk_elems, dvc, chunk_elems, hip_stream);
-    } else {
-      st = zero_fill(dkc, chunk_elems * 2, stream);
-      if (st == HSAP_OK) st = zero_fill(dvc, chunk_elems * 2, stream);
-    }
-  }
+    st = hsap_attn_bwd_bf16(&ex->desc, q, k, v, d_o, lse, ex->delta, ex->doc_start, ex->d_tiles_k, ex->d_runs_k,
+                            ex->info.num_runs_k, ex->d_tiles_all, ex->d_runs_all, ex->info.num_runs_all, dq, dk, dv,
+                            hip_stream);
   return st;
 }
 

@@ -11,8 +11,8 @@ per stage); every step of the path runs inside the library:
             the runs wrote; or hsap_attn_fwd_fused, one pass over every chunk
             per q-tile without partials
   backward  hsap_attn_bwd_preprocess, hsap_partial_attn_bwd (dK/dV over the
-            k-major runs, dQ over the forward's q-major runs), and
-            hsap_convert_f32_bf16 for the gradients
+            k-major runs, dQ over one run per q-tile across every chunk),
+            and hsap_convert_f32_bf16 for the gradients
 
 Tensors follow the library's layouts: the shard's q / dO are [n, Hq, d] in
 its local row order; k / v and the dK / dV accumulators are in sharded order
@@ -172,8 +172,9 @@ class ShardAttention:
                 bufs["dk_acc"][c].zero_()
                 bufs["dv_acc"][c].zero_()
         L.attn_bwd_preprocess(fwd["o"], d_o, self.n, self.hq, self.d, bufs["delta"])
+        # dQ over the one-run-per-q-tile lists (every chunk), so each q-tile has one owner
         L.partial_attn_bwd(self.desc, q, k, v, d_o, fwd["lse"], bufs["delta"], self.doc_start, self.tiles_k,
-                           self.runs_k, self.tiles_q, self.runs_q, bufs["dq_acc"], bufs["dk_acc"], bufs["dv_acc"])
+                           self.runs_k, self.tiles_all, self.runs_all, bufs["dq_acc"], bufs["dk_acc"], bufs["dv_acc"])
         L.convert_f32_bf16(bufs["dq_acc"], bufs["dq"])
         # only chunks with tiles receive gradient; the others are zero
         for c in range(self.P):

@@ -169,6 +169,24 @@ def test_backward_validates_before_launch():
     assert st == L.HSAP_ERR_INVALID_ARG
 
 
+def test_bf16_backward_validates_before_launch():
+    lib = L.lib()
+    fake = ctypes.c_void_p(4096)
+    d = _attn_desc(block_m=32, total_tokens=64 * 2, block_n=32)
+    st = lib.hsap_attn_bwd_bf16(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
+                                fake, 1, fake, fake, fake, None)
+    assert st == L.HSAP_ERR_UNSUPPORTED
+    d = _attn_desc()
+    st = lib.hsap_attn_bwd_bf16(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, None, None, 1, fake,
+                                fake, 1, fake, fake, fake, None)
+    assert st == L.HSAP_ERR_INVALID_ARG
+    st = lib.hsap_attn_bwd_bf16(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
+                                fake, 1, ctypes.c_void_p(4098), fake, fake, None)
+    assert st == L.HSAP_ERR_INVALID_ARG                          # dq not 8-byte aligned
+    assert lib.hsap_attn_bwd_bf16(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 0, fake,
+                                  fake, 0, fake, fake, fake, None) == L.HSAP_OK   # nothing to do
+
+
 def test_merge_and_helpers_validate():
     lib = L.lib()
     fake = ctypes.c_void_p(4096)

@@ -14,7 +14,8 @@ import numpy as np
 import pytest
 import torch
 
-from _harness import Case, compare_backward, compare_forward, max_abs
+from _harness import Case, compare_backward, compare_forward, max_abs, rel_max
+from paper_2606_30460_amd.shard_attention import to_sharded
 from workloads import make_workload
 
 pytestmark = pytest.mark.gpu
@@ -212,6 +213,40 @@ def test_backward_small(case):
         compare_forward(gpu, ref["fwd"])
         rep = compare_backward(gpu, ref)
         _say(case, r, rep)
+
+
+def test_backward_ring_steps_accumulate():
+    """dQ accumulated over one call per ring step (each chunk's unsplit q-major runs), dK/dV per
+    chunk, equals the one-pass result within rounding and meets the oracle."""
+    from paper_2606_30460_amd import _lib as L
+    N, P, layout, hq, hkv, d, bm, bn = 4096, 4, "contiguous", 4, 2, 128, 128, 128
+    cu = np.array([0, 700, 2600, 2601, 4096], dtype=np.int32)
+    r = 3
+    c = Case(cu, N, P, layout, r, hq, hkv, d, bm, bn, seed=5, backward=True)
+    gpu = c.run_gpu()
+    ref = c.run_oracle()
+    sa = gpu["sa"]
+    dev = torch.device("cuda")
+    q = to_sharded(sa.shard, c.q.to(dev))[r].contiguous()
+    k, v = to_sharded(sa.shard, c.k.to(dev)), to_sharded(sa.shard, c.v.to(dev))
+    d_o = to_sharded(sa.shard, c.do.to(dev))[r].contiguous()
+    fwd = sa.alloc_forward()
+    sa.forward(q, k, v, fwd)
+    bwd = sa.alloc_backward()
+    L.attn_bwd_preprocess(fwd["o"], d_o, sa.n, hq, d, bwd["delta"])
+    tiles_q, runs_q, _ = L.plan_runs(sa.shard, sa.tiles, L.MAJOR_Q, 0)
+    tq = torch.from_numpy(tiles_q.reshape(-1)).to(dev)
+    for chunk in sa.chunks:
+        sel = runs_q[runs_q[:, 0] == chunk]
+        if len(sel):
+            L.partial_attn_bwd(sa.desc, q, k, v, d_o, fwd["lse"], bwd["delta"], sa.doc_start, None, None, tq,
+                               torch.from_numpy(np.ascontiguousarray(sel).reshape(-1)).to(dev), bwd["dq_acc"],
+                               bwd["dk_acc"], bwd["dv_acc"])
+    torch.cuda.synchronize()
+    dq = bwd["dq_acc"].cpu().numpy()
+    rep = {"dq_vs_onepass": rel_max(dq, gpu["dq"]), "dq_vs_oracle": rel_max(dq, ref["dq"])}
+    _say(rep)
+    assert rep["dq_vs_onepass"] <= 1e-5 and rep["dq_vs_oracle"] <= 3e-2, rep
 
 
 @pytest.mark.parametrize("name", ["c5", "c5m"])
