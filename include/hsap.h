@@ -392,6 +392,7 @@ typedef struct {
   int32_t split_length;     /* max_run_tiles used for the q-major runs (0: none) */
   int32_t chunks_with_tiles;
   int32_t reserved;
+  uint64_t chunk_mask;      /* bit c set: chunk c has tiles (P <= 64)        */
 } hsap_exec_info;
 
 /*
@@ -453,14 +454,16 @@ hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, 
 
 /*
  * hsap_executor_backward -- gradients of the forward for the current plan
- * (needs HSAP_EXEC_BACKWARD): zeroes dk and dv, then
- * hsap_attn_bwd_preprocess and hsap_attn_bwd_bf16 over the k-major and
- * MAJOR_Q_ALL runs.
+ * (needs HSAP_EXEC_BACKWARD): zeroes the dk and dv rows of the chunks with
+ * tiles, then hsap_attn_bwd_preprocess and hsap_attn_bwd_bf16 over the
+ * k-major and MAJOR_Q_ALL runs.
  *   q, k, v  as for the forward;  d_o, o  device bf16 [n, Hq, d] (o: the
  *            forward's output);  lse  device fp32 [Hq, n] (the forward's).
  *   dq       device bf16 [n, Hq, d].
- *   dk, dv   device bf16 [P, n, Hkv, d], sharded order: chunks without tiles
- *            receive zeros.
+ *   dk, dv   device bf16 [P, n, Hkv, d], sharded order: the rows of every
+ *            chunk in hsap_exec_info.chunk_mask are written; the rows of a
+ *            chunk without tiles are left untouched (this shard sends it no
+ *            gradient: its contribution is zero).
  */
 hsap_status hsap_executor_backward(hsap_executor* ex, const void* q, const void* k, const void* v, const void* d_o,
                                    const void* o, const float* lse, void* dq, void* dk, void* dv, void* hip_stream);

@@ -65,7 +65,7 @@ class ExecInfo(ctypes.Structure):
     _fields_ = [("num_tiles", ctypes.c_int64), ("num_full_tiles", ctypes.c_int64), ("useful_pairs", ctypes.c_int64),
                 ("num_runs_q", ctypes.c_int64), ("num_runs_k", ctypes.c_int64), ("num_runs_all", ctypes.c_int64),
                 ("num_parts", ctypes.c_int32), ("split_length", ctypes.c_int32),
-                ("chunks_with_tiles", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("chunks_with_tiles", ctypes.c_int32), ("reserved", ctypes.c_int32), ("chunk_mask", ctypes.c_uint64)]
 
 
 _lib: Optional[ctypes.CDLL] = None

@@ -25,6 +25,8 @@
 
 namespace hsap {
 
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
 struct BwdArgs {
   const __bf16* q;
   const __bf16* k;
@@ -64,9 +66,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   constexpr float LOG2E = 1.44269504088896340736f;
   __shared__ __attribute__((aligned(16))) __bf16 Qs[2][SUB * D];
   __shared__ __attribute__((aligned(16))) __bf16 dOs[2][SUB * D];
-  __shared__ float lse_s[2][SUB];
-  __shared__ float delta_s[2][SUB];
-  __shared__ int32_t start_s[2][SUB];
+  __shared__ __attribute__((aligned(16))) float lse_s[2][SUB];
+  __shared__ __attribute__((aligned(16))) float delta_s[2][SUB];
+  __shared__ __attribute__((aligned(16))) int32_t start_s[2][SUB];
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
@@ -221,22 +223,34 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
         sacc = mfma32(qa[kk], kf[kk], sacc);
         dpacc = mfma32(oa[kk], vf[kk], dpacc);
       }
+      // P for the block (register j = 4 grp + e holds query q4 + e, q4 = 32 qb + 8 grp + 4 hi),
+      // masked in one uniform branch, then P and dS = P (dP - delta) as bf16
+      float p[16];
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const f32x4 l4 = *(const f32x4*)(&lse_s[buf][32 * qb + 8 * grp + 4 * hi]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) p[4 * grp + e] = fast_exp2(__builtin_fmaf(sacc[4 * grp + e], a.scale_log2, -l4[e]));
+      }
+      if (masked) {
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+          const int q4 = 32 * qb + 8 * grp + 4 * hi;
+          const i32x4 s4 = *(const i32x4*)(&start_s[buf][q4]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if ((uint32_t)(gk - s4[e]) > (uint32_t)(gq0 + q4 + e - s4[e])) p[4 * grp + e] = 0.f;
+        }
+      }
       bf16x8 pb[2], sb[2];
 #pragma unroll
       for (int grp = 0; grp < 4; ++grp) {
-        const int q4 = 32 * qb + 8 * grp + 4 * hi;  // four consecutive queries
-        const f32x4 l4 = *(const f32x4*)(&lse_s[buf][q4]);
-        const f32x4 d4 = *(const f32x4*)(&delta_s[buf][q4]);
+        const f32x4 d4 = *(const f32x4*)(&delta_s[buf][32 * qb + 8 * grp + 4 * hi]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int j = 4 * grp + e;
-          float p = fast_exp2(__builtin_fmaf(sacc[j], a.scale_log2, -l4[e]));
-          if (masked) {
-            const int32_t st = start_s[buf][q4 + e];
-            if ((uint32_t)(gk - st) > (uint32_t)(gq0 + q4 + e - st)) p = 0.f;
-          }
-          pb[j >> 3][j & 7] = (__bf16)p;
-          sb[j >> 3][j & 7] = (__bf16)(p * (dpacc[j] - d4[e]));
+          pb[j >> 3][j & 7] = (__bf16)p[j];
+          sb[j >> 3][j & 7] = (__bf16)(p[j] * (dpacc[j] - d4[e]));
         }
       }
 #pragma unroll

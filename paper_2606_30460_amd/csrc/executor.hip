@@ -245,7 +245,11 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   ex->info.num_runs_q = RQ;
   ex->info.num_parts = parts;
   ex->info.split_length = split;
-  for (uint8_t c : ex->chunk_has_tiles) ex->info.chunks_with_tiles += c;
+  for (int32_t c = 0; c < P; ++c)
+    if (ex->chunk_has_tiles[(size_t)c]) {
+      ++ex->info.chunks_with_tiles;
+      ex->info.chunk_mask |= 1ull << c;
+    }
 
   // 3. k-major and fused runs
   int64_t RK = 0, RA = 0;
@@ -376,10 +380,14 @@ hsap_status hsap_executor_backward(hsap_executor* ex, const void* q, const void*
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   const hipStream_t stream = (hipStream_t)hip_stream;
   const int64_t n = ex->geom.n, hq = ex->desc.heads_q, d = ex->desc.head_dim;
-  // dK/dV rows that no k-major run owns (chunks without tiles, k-tiles no query reaches) are zero
-  const int64_t kv_bytes = (int64_t)ex->geom.P * n * ex->desc.heads_kv * d * 2;
-  hsap_status st = zero_fill(dk, kv_bytes, stream);
-  if (st == HSAP_OK) st = zero_fill(dv, kv_bytes, stream);
+  // in a chunk with tiles, dK/dV rows of k-tiles that no query reaches have no owning run: zero first
+  const int64_t chunk_bytes = n * ex->desc.heads_kv * d * 2;
+  hsap_status st = HSAP_OK;
+  for (int32_t c = 0; st == HSAP_OK && c < ex->geom.P; ++c)
+    if (ex->chunk_has_tiles[(size_t)c]) {
+      st = zero_fill((char*)dk + c * chunk_bytes, chunk_bytes, stream);
+      if (st == HSAP_OK) st = zero_fill((char*)dv + c * chunk_bytes, chunk_bytes, stream);
+    }
   if (st == HSAP_OK) st = hsap_attn_bwd_preprocess(o, d_o, n, (int32_t)hq, (int32_t)d, ex->delta, hip_stream);
   if (st == HSAP_OK)
     st = hsap_attn_bwd_bf16(&ex->desc, q, k, v, d_o, lse, ex->delta, ex->doc_start, ex->d_tiles_k, ex->d_runs_k,

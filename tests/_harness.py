@@ -106,8 +106,14 @@ class Case:
                    "o_staged": os_.float().cpu().numpy(), "lse_staged": lses.cpu().numpy()}
             if self.backward:
                 do_sh = to_sharded(s, self.do.to(dev))[self.shard].contiguous()
+                # chunks without tiles are not written: the caller's zeros stay (their gradient is zero)
                 dq = torch.full_like(q_sh, float("nan"))
-                dk, dv = torch.full_like(k_sh, float("nan")), torch.full_like(v_sh, float("nan"))
+                dk, dv = torch.zeros_like(k_sh), torch.zeros_like(v_sh)
+                mask = ex.info()["chunk_mask"]
+                for chunk in range(self.P):
+                    if mask >> chunk & 1:
+                        dk[chunk].fill_(float("nan"))
+                        dv[chunk].fill_(float("nan"))
                 ex.backward(q_sh, k_sh, v_sh, do_sh, o, lse, dq, dk, dv)
                 out.update({"dq": dq.float().cpu().numpy(), "dk": dk.float().cpu().numpy(),
                             "dv": dv.float().cpu().numpy()})

@@ -205,7 +205,7 @@ def test_merge_and_helpers_validate():
 
 
 def test_executor_struct_layout():
-    assert ctypes.sizeof(L.ExecInfo) == 64
+    assert ctypes.sizeof(L.ExecInfo) == 72
 
 
 def test_executor_validates_before_touching_the_device():
