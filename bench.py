@@ -50,11 +50,41 @@ def _critical_shard(L, w):
     return best_r
 
 
+def _positions(N: int, P: int, layout: int, x: int, local: np.ndarray) -> np.ndarray:
+    """Global positions of local rows of shard (or chunk) x."""
+    n = N // P
+    if layout == 0:
+        return x * n + local
+    m = n // 2
+    return np.where(local < m, x * m + local, (2 * P - 1 - x) * m + (local - m))
+
+
+def _finite_partial_rows(L, cu, sd, split: int) -> int:
+    """(part, query row) pairs whose partial LSE is finite, from the plan on the host: a row of a
+    q-major run has an allowed key iff some tile of the run holds a key j with start(i) <= j <= i."""
+    tiles = L.plan(cu, sd)["tiles"]
+    sorted_tiles, runs, _ = L.plan_runs(sd, tiles, L.MAJOR_Q, split)
+    N, P, bm, bn = sd.total_tokens, sd.sp_degree, sd.block_m, sd.block_n
+    starts = np.repeat(cu[:-1].astype(np.int64), np.diff(cu))
+    count = 0
+    for _, t, first, cnt in runs:
+        if cnt == 0:
+            continue
+        gi = _positions(N, P, sd.layout, sd.shard_id, np.arange(t * bm, (t + 1) * bm))
+        si = starts[gi]
+        ok = np.zeros(bm, dtype=bool)
+        for c, _, kt, _ in sorted_tiles[first:first + cnt]:
+            k0 = int(_positions(N, P, sd.layout, int(c), np.array([kt * bn]))[0])  # a tile's keys are contiguous
+            ok |= (k0 <= gi) & (k0 + bn - 1 >= si)
+        count += int(ok.sum())
+    return count
+
+
 def measure(name: str, steps: int, warmup: int, backward=None):
     """Time `steps` steps of one workload through the step executor; returns a result dict (GPU side only)."""
     import torch
     from paper_2606_30460_amd import _lib as L
-    from paper_2606_30460_amd.shard_attention import ShardAttention, to_sharded
+    from paper_2606_30460_amd.shard_attention import to_sharded
     from workloads import make_workload
 
     w = make_workload(name)
@@ -131,22 +161,8 @@ def measure(name: str, steps: int, warmup: int, backward=None):
         L.plan(cu, sd)
     plan_ms = (time.perf_counter() - t1) / reps * 1e3
 
-    # algorithmic merge bytes: every part's LSE row, the O row of parts whose LSE is finite, the outputs.
-    # The finite rows are counted on the same parts computed through the entry points.
-    sa = ShardAttention(cu, w.total_tokens, w.sp_degree, w.layout, shard, w.heads_q, w.heads_kv, w.head_dim,
-                        w.block_m, w.block_n, max_run_tiles=info["split_length"])
-    sa.plan()
-    part = {"o_part": torch.empty(len(sa.present), n, w.heads_q, w.head_dim, dtype=torch.float32, device=dev)}
-    part["lse_part"] = torch.empty(len(sa.present), w.heads_q, n, dtype=torch.float32, device=dev)
-    finite_rows = 0
-    for i, slot in enumerate(sa.present):
-        sel = sa.runs_q_host[sa.runs_q_host[:, 0] == slot].copy()
-        sel[:, 0] = 0
-        L.partial_attn_fwd(sa.desc, q, k, v, sa.doc_start, sa.tiles_q, torch.from_numpy(sel.reshape(-1)).to(dev),
-                           part["o_part"][i], part["lse_part"][i])
-        finite_rows += int(torch.isfinite(part["lse_part"][i]).sum().item())
-    assert len(sa.present) == info["num_parts"]
-    del part, sa
+    # algorithmic merge bytes: every part's LSE row, the O row of parts whose LSE is finite, the outputs
+    finite_rows = _finite_partial_rows(L, cu, sd, info["split_length"]) * w.heads_q
     merge_bytes = (info["num_parts"] * w.heads_q * n * 4 + finite_rows * w.head_dim * 4
                    + n * w.heads_q * (2 * w.head_dim + 4))
 
