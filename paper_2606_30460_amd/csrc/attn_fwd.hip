@@ -281,6 +281,263 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS forward for d = 128, BM = 256: eight waves (wave w owns query
+// rows 32w..32w+31), one workgroup per CU.  K and V steps go from global
+// memory straight into LDS (global_load_lds, no staging registers) in a
+// three-slot ring of unpadded XOR-swizzled [64][128] tiles: K three steps
+// ahead of its use in the scores, V two steps ahead of its use in PV, so a
+// load has two steps to arrive.  Each wave moves 128 of a tile's 1024
+// 16-byte chunks per tile, 64 per instruction; a lane's source chunk is the
+// one the swizzle places at its destination.
+// ---------------------------------------------------------------------------
+template <int BN, bool FUSED>
+__global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
+  constexpr int D = 128, KB = 64, SUBS = BN / KB, CPR = D / 8, NSLOT = 3, TILE = KB * D;
+  constexpr float NEG_INF = -__builtin_inff();
+  constexpr float RESCALE_SLACK = 8.f;
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[NSLOT][TILE];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[NSLOT][TILE];
+  typedef __attribute__((address_space(3))) void* lds_void;
+  typedef __attribute__((address_space(1))) void* glb_void;
+
+  const int tid = threadIdx.x;
+  const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
+  const int run_idx = blockIdx.x / a.hq;
+  const int h = blockIdx.x - run_idx * a.hq;
+  const hsap_run run = a.runs[run_idx];
+  const int slot = run.slot;
+  if (!FUSED && (slot < 0 || slot >= a.num_slots)) return;
+  const int g = h / a.group;
+  const int64_t n = a.geom.n;
+  const int64_t qrow = (int64_t)run.tile * 256 + 32 * w + l32;
+
+  if (run.count == 0) {
+    if (FUSED) {
+      bf16x4* op = (bf16x4*)(a.o_out + (qrow * a.hq + h) * D + 4 * hi);
+#pragma unroll
+      for (int e = 0; e < D / 8; ++e) op[2 * e] = bf16x4{};
+      if (hi == 0) a.lse_out[(int64_t)h * n + qrow] = NEG_INF;
+    } else if (hi == 0) {
+      a.lse_part[((int64_t)slot * a.hq + h) * n + qrow] = NEG_INF;
+    }
+    return;
+  }
+
+  const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
+  const int32_t qstart = a.doc_start[gq];
+  const uint32_t span = (uint32_t)(gq - qstart);
+  bf16x8 qf[D / 16];
+  {
+    const __bf16* qp = a.q + (qrow * a.hq + h) * D + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
+  }
+  const int64_t rstride = (int64_t)a.hkv * D;
+  const int total = run.count * SUBS;
+  // The run's tile descriptors, packed one per lane (k_tile | chunk << 23 | kind << 31) in
+  // windows of 64 tiles (window v in win0 or win1 by parity), read with v_readlane: no memory
+  // access for descriptors inside the loop (a vector load there would wait for every
+  // transfer in flight).
+  uint32_t win0 = 0u, win1 = 0u;
+  int win_hi = -1;
+  auto load_window = [&](int v) {
+    const int i = 64 * v + lane;
+    uint32_t p = 0;
+    if (i < run.count) {
+      const hsap_tile t = a.tiles[run.first + i];
+      p = (uint32_t)t.k_tile | ((uint32_t)t.chunk << 23) | ((uint32_t)t.kind << 31);
+    }
+    if (v & 1) win1 = p;
+    else win0 = p;
+    win_hi = v;
+  };
+  auto tile_at = [&](int s) -> uint32_t {
+    const int idx = s / SUBS;
+    return __builtin_amdgcn_readlane(((idx >> 6) & 1) ? win1 : win0, idx & 63);
+  };
+  auto chunk_of = [](uint32_t p) { return (int32_t)((p >> 23) & 0xFFu); };
+  auto step_row0 = [&](uint32_t p, int s) { return (int64_t)(p & 0x7FFFFFu) * BN + (s % SUBS) * KB; };
+  load_window(0);
+  const int64_t run_base = FUSED ? 0 : (((int64_t)chunk_of(tile_at(0)) * n) * a.hkv + g) * D;
+  auto step_off = [&](uint32_t p, int s) {
+    if (FUSED) return (((int64_t)chunk_of(p) * n + step_row0(p, s)) * a.hkv + g) * D;
+    return run_base + step_row0(p, s) * rstride;
+  };
+
+  // direct staging: instruction u of wave w fills chunk positions p = 128 w + 64 u + lane
+  int32_t gsrc[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int p = 128 * w + 64 * u + lane, row = p >> 4;
+    gsrc[u] = (int32_t)(row * rstride + swz_chunk<CPR>(row, p & 15) * 8);
+  }
+  // issued from asm: the transfers are ordered by the explicit vmcnt waits of the ring below (the
+  // compiler would otherwise wait for each one before any later LDS read).  No memory clobber:
+  // volatile asm keeps its order against the ring's barriers (which do clobber memory), and the
+  // tile descriptors stay scalar loads.
+  auto stage = [&](const __bf16* src, __bf16* dst) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const uint32_t m0v = (uint32_t)(uintptr_t)(dst + (128 * w + 64 * u) * 8);
+      const __bf16* gp = src + gsrc[u];
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(m0v)),
+                   "v"(gp)
+                   : "m0");
+    }
+  };
+  // operand offsets in a swizzled tile: K rows (row l32 of a 32-row block, chunk 2 kk + hi) and
+  // V transpose reads (rows 8 k + tr_row of a 16-row block, columns 32 mb + tr_col)
+  const int tr_row = 4 * hi + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int rowoff[D / 16], troff[D / 32][2];
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) rowoff[kk] = swz<CPR>(l32, 16 * kk + 8 * hi);
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+    for (int k = 0; k < 2; ++k) troff[mb][k] = swz<CPR>(8 * k + tr_row, 32 * mb + tr_col) - 8 * k * D;
+
+  auto scores = [&](const __bf16* K, f32x16 (&sc)[KB / 32]) {
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb) {
+      bf16x8 kf[D / 16];
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(K + 32 * nb * D + rowoff[kk]);
+      sc[nb] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) sc[nb] = mfma32(kf[kk], qf[kk], sc[nb]);
+    }
+  };
+
+  float m_run = NEG_INF, l_run = 0.f;
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
+
+  // prologue: K(0..2) and V(0..1) in flight, wait for all, scores of step 0
+  {
+    const uint32_t t0 = tile_at(0);
+    stage(a.k + step_off(t0, 0), Ks[0]);
+    stage(a.v + step_off(t0, 0), Vs[0]);
+    if (total > 1) {
+      const uint32_t t1 = tile_at(1);
+      stage(a.k + step_off(t1, 1), Ks[1]);
+      stage(a.v + step_off(t1, 1), Vs[1]);
+    }
+    if (total > 2) stage(a.k + step_off(tile_at(2), 2), Ks[2]);
+  }
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  f32x16 sc[KB / 32];
+  scores(Ks[0], sc);
+  hsap_lds_barrier();  // every wave has read K slot 0 before step 0 refills it
+
+  int sk = 0;  // s % 3
+  for (int s = 0; s < total; ++s) {
+    // the window of tile (s + 3) / SUBS is needed now (rare vector load: every 64 tiles)
+    if (s + 3 < total && ((s + 3) / SUBS) >> 6 > win_hi) load_window(win_hi + 1);
+    const uint32_t tile = tile_at(s);
+    const int s1 = sk == 2 ? 0 : sk + 1, s2 = s1 == 2 ? 0 : s1 + 1;  // (s + 1) % 3, (s + 2) % 3
+    const bool ldk = s + 3 < total, ldv = s + 2 < total;
+    if (ldk) stage(a.k + step_off(tile_at(s + 3), s + 3), Ks[sk]);
+    if (ldv) stage(a.v + step_off(tile_at(s + 2), s + 2), Vs[s2]);
+    f32x16 sn[KB / 32];
+    if (s + 1 < total) scores(Ks[s1], sn);
+
+    if (tile >> 31) {  // MASKED
+      const int32_t rel0 = (int32_t)global_pos(a.geom, chunk_of(tile), step_row0(tile, s)) - qstart;
+#pragma unroll
+      for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if ((uint32_t)(rel0 + 32 * nb + c_row(j, hi)) > span) sc[nb][j] = NEG_INF;
+    }
+    float mx = sc[0][0];
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
+    const float m_new = fmaxf(m_run, pair_max(mx) * a.scale_log2);
+    if (__builtin_amdgcn_ballot_w64(m_new > m_run + RESCALE_SLACK) != 0) {
+      const float alpha = fast_exp2(m_run - (m_new == NEG_INF ? 0.f : m_new));
+      l_run *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = m_run == NEG_INF ? 0.f : m_run;
+    float rs = 0.f;
+    bf16x8 pb[KB / 32][2];
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const float p = fast_exp2(__builtin_fmaf(sc[nb][j], a.scale_log2, -m_use));
+        rs += p;
+        pb[nb][j >> 3][j & 7] = (__bf16)p;
+      }
+    l_run += rs;
+
+    const __bf16* V = Vs[sk];
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int rb = (32 * nb + 16 * half) * D;
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb) {
+          const bf16x8 av = cat4(ds_read_tr16(V + rb + troff[mb][0]), ds_read_tr16(V + rb + 8 * D + troff[mb][1]));
+          o[mb] = mfma32(av, pb[nb][half], o[mb]);
+        }
+      }
+    // the loads issued one step ago (K(s + 2), V(s + 1)) must have landed before the next step;
+    // this step's own loads stay in flight
+    if (ldk && ldv) asm volatile("s_waitcnt vmcnt(4)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else if (ldk || ldv) asm volatile("s_waitcnt vmcnt(2)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#pragma unroll
+    for (int nb = 0; nb < KB / 32; ++nb) sc[nb] = sn[nb];
+    sk = s1;
+  }
+
+  l_run = pair_sum(l_run);
+  const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+  const float lse = l_run > 0.f ? (m_run + __log2f(l_run)) * 0.69314718055994530942f : NEG_INF;
+  if (FUSED) {
+    __bf16* op = a.o_out + (qrow * a.hq + h) * D + 4 * hi;
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const bf16x4 val{(__bf16)(o[mb][4 * grp] * inv), (__bf16)(o[mb][4 * grp + 1] * inv),
+                         (__bf16)(o[mb][4 * grp + 2] * inv), (__bf16)(o[mb][4 * grp + 3] * inv)};
+        *(bf16x4*)(op + 32 * mb + 8 * grp) = val;
+      }
+    if (hi == 0) a.lse_out[(int64_t)h * n + qrow] = lse;
+  } else {
+    float* op = a.o_part + (((int64_t)slot * n + qrow) * a.hq + h) * D + 4 * hi;
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const f32x4 val{o[mb][4 * grp] * inv, o[mb][4 * grp + 1] * inv, o[mb][4 * grp + 2] * inv,
+                        o[mb][4 * grp + 3] * inv};
+        *(f32x4*)(op + 32 * mb + 8 * grp) = val;
+      }
+    if (hi == 0) a.lse_part[((int64_t)slot * a.hq + h) * n + qrow] = lse;
+  }
+}
+
+template <int BN, bool FUSED>
+static hsap_status launch_dl(const FwdArgs& a, int64_t num_runs, hipStream_t stream) {
+  const int64_t blocks = num_runs * a.hq;
+  if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
+  hipLaunchKernelGGL((attn_fwd_dl_kernel<BN, FUSED>), dim3((unsigned)blocks), dim3(512), 0, stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
+  return HSAP_OK;
+}
+
 template <int D, int BN, int WAVES, bool FUSED>
 static hsap_status launch(const FwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
@@ -326,8 +583,7 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
 #define HSAP_FWD_CASE(D_, BN_, W_) \
   if (d == D_ && bn == BN_ && bm == 32 * W_) return launch<D_, BN_, W_, FUSED>(a, num_runs, s);
-  HSAP_FWD_CASE(128, 128, 8)
-  HSAP_FWD_CASE(128, 64, 8)
+  if (d == 128 && bm == 256) return bn == 128 ? launch_dl<128, FUSED>(a, num_runs, s) : launch_dl<64, FUSED>(a, num_runs, s);
   HSAP_FWD_CASE(128, 128, 4)
   HSAP_FWD_CASE(128, 64, 4)
   HSAP_FWD_CASE(128, 128, 2)
