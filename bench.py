@@ -2,12 +2,12 @@
 """Useful document-masked attention TFLOP/s for one sequence-parallel shard on one MI355X.
 
 One step is one pass of the whole path for one packed batch, inputs resident
-in HBM:
-  host planner (tile list and runs, C++) -> async upload -> document starts
-  -> partial attention of the shard against every K/V chunk -> LSE merge
-  (and, for a forward+backward workload, the backward preprocess, partial
-  attention backward and gradient conversion).
-The planner of step i+1 runs on the host while the GPU executes step i.
+in HBM, driven by the step executor (hsap_executor_*):
+  host planner (tile list and runs, C++) -> one async upload of the lists
+  -> document starts -> partial attention of the shard against every K/V
+  chunk -> LSE merge (and, for a forward+backward workload, the backward
+  preprocess and the partial attention backward, which stores the final bf16
+  dQ/dK/dV from its registers).
 
 Default workload: 32768-token packed sequence, log-normal documents, 32
 heads of 128, sequence-parallel degree 8 (contiguous), shard 3, forward.

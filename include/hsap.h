@@ -213,8 +213,8 @@ hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, voi
  * equation of the inter-group SP section restricted to the packing mask).
  *
  *   desc       shard layout (N, P, layout, r, BM, BN) and heads / head_dim /
- *              softmax scale.  Supported: d in {64, 128}; BM in {64, 128};
- *              BN in {64, 128}; Hq % Hkv == 0.
+ *              softmax scale.  Supported: d in {64, 128}; BM in {64, 128},
+ *              or 256 with d = 128; BN in {64, 128}; Hq % Hkv == 0.
  *   q          device bf16 [n, Hq, d]: shard r's queries, local row order.
  *   k, v       device bf16 [P, n, Hkv, d]: every chunk, sharded order.
  *   doc_start  device int32 [N] from hsap_doc_start.

@@ -107,6 +107,12 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError("libhsap.so is not built (%s); run __graft_entry__.build() or "
                                "python -m paper_2606_30460_amd.build" % LIB_PATH)
+        # torch ships its own HIP runtime; loading torch first makes this library bind to that
+        # one (loading ours first would leave torch with a runtime that sees no GPU)
+        try:
+            import torch  # noqa: F401
+        except ImportError:  # pragma: no cover - host-only use of the planner
+            pass
         handle = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in _SIG.items():
             fn = getattr(handle, name)
