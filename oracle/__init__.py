@@ -29,6 +29,9 @@ What it computes, with the passages it follows (HSAP paper, arxiv 2606.30460):
   balancing in the compile-algorithm section).
 * ``plan`` -- the per-shard tile classification that the compile step's block
   partition performs (compile step 1 of the SAP section), at tile granularity.
+* ``balance`` -- the per-(shard, chunk) block sizes of every shard and the
+  Q-transfer rebalance of the blocks over ranks (compile step 2, and the
+  balancing of InterSP groups by transferring Q blocks).
 
 Parity status: every function above is pinned by ``tests/test_oracle_pins.py``
 against brute force, closed forms, library routines or invariants; none is
@@ -50,3 +53,4 @@ from .plan import (  # noqa: F401
     tile_pair_counts_bruteforce,
     useful_pairs_all_shards,
 )
+from .balance import load_matrix, q_transfer_balance  # noqa: F401

@@ -472,3 +472,80 @@ def test_p12_neg_inf_structure(layout):
             for h in range(H):
                 assert np.array_equal(np.isneginf(lse_c[h]), none)
         assert np.all(np.isfinite(fwd["lse"]))        # the diagonal is always allowed
+
+
+# ---------------------------------------------------------------------------
+# Block loads of every shard and the Q-transfer rebalance
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("layout", ["contiguous", "zigzag"])
+@pytest.mark.parametrize("seed", range(3))
+def test_load_matrix_counts_dense_mask(layout, seed):
+    # every block's pair count is the number of allowed (query, key) pairs of the dense mask;
+    # each shard's row sums to the closed form sum_i (i - start(i) + 1); tiles exist iff pairs do
+    rng = np.random.default_rng(300 + seed)
+    P, bm, bn = 4, 8, 4
+    N = 2 * P * 16
+    cu = _rand_cu(rng, N)
+    tiles, pairs = oracle.load_matrix(cu, N, P, layout, bm, bn)
+    for r in range(P):
+        qp = oracle.shard_positions(N, P, layout, r)
+        for c in range(P):
+            kp = oracle.shard_positions(N, P, layout, c)
+            assert pairs[r, c] == int(oracle.allowed_mask_dense(cu, qp, kp).sum())
+            assert (tiles[r, c] > 0) == (pairs[r, c] > 0)
+            assert pairs[r, c] <= tiles[r, c] * bm * bn
+    assert np.array_equal(pairs.sum(axis=1), oracle.useful_pairs_all_shards(cu, N, P, layout))
+
+
+def _check_assignment(cost, exec_rank, load):
+    P = cost.shape[0]
+    expect = np.zeros(P, dtype=np.int64)
+    for r in range(P):
+        assert exec_rank[r, r] == r
+        for c in range(P):
+            assert exec_rank[r, c] in (r, c)
+            if cost[r, c] == 0:
+                assert exec_rank[r, c] == r
+            expect[exec_rank[r, c]] += cost[r, c]
+    assert np.array_equal(load, expect)
+    assert int(load.sum()) == int(cost.sum())
+
+
+def _best_max_load(cost):
+    """Smallest achievable maximum load, by trying every assignment of the movable blocks."""
+    P = cost.shape[0]
+    movable = [(r, c) for r in range(P) for c in range(P) if r != c and cost[r, c] > 0]
+    best = None
+    for bits in range(1 << len(movable)):
+        load = np.diag(cost).astype(np.int64).copy()
+        for i, (r, c) in enumerate(movable):
+            load[c if bits >> i & 1 else r] += cost[r, c]
+        best = int(load.max()) if best is None else min(best, int(load.max()))
+    return best, len(movable)
+
+
+def test_q_transfer_balance_worked_example():
+    # Lower-triangular costs (causal, contiguous).  Diagonal loads start at [4, 3, 2].  The
+    # off-diagonal blocks by decreasing cost: (2, 1) w 7 -- rank 2 (load 2) is not above rank 1
+    # (load 3), stays: [4, 3, 9]; (1, 0) w 6 -- rank 1 (3) is below rank 0 (4), stays:
+    # [4, 9, 9]; (2, 0) w 5 -- rank 0 (4) is below rank 2 (9), moves to 0: [9, 9, 9].
+    cost = np.array([[4, 0, 0], [6, 3, 0], [5, 7, 2]])
+    exec_rank, load = oracle.q_transfer_balance(cost)
+    assert load.tolist() == [9, 9, 9]
+    assert exec_rank.tolist() == [[0, 0, 0], [1, 1, 1], [0, 2, 2]]   # empty blocks keep their row
+    _check_assignment(cost, exec_rank, load)
+    assert _best_max_load(cost)[0] == 9
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_q_transfer_balance_against_every_assignment(seed):
+    rng = np.random.default_rng(900 + seed)
+    P = int(rng.integers(1, 5))
+    cost = rng.integers(0, 20, size=(P, P)) * (rng.random((P, P)) < 0.6)
+    exec_rank, load = oracle.q_transfer_balance(cost)
+    _check_assignment(cost, exec_rank, load)
+    best, movable = _best_max_load(cost)
+    assert best <= int(load.max()) <= int(cost.sum())
+    if movable <= 1:   # one decision: taking the less loaded rank is optimal
+        assert int(load.max()) == best
