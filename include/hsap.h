@@ -189,6 +189,40 @@ int32_t hsap_split_length(const hsap_shard_desc* shard, int64_t num_tiles, int32
                           int32_t resident_workgroups);
 
 /*
+ * hsap_load_matrix -- the size of every rank block of the packed sequence
+ * (host): for each shard r (query rows) and chunk c (key rows), the number of
+ * non-empty tiles and of allowed (query, key) pairs per head that hsap_plan
+ * finds for shard r in chunk c.  These are the blocks of compile step 1 of
+ * the SAP section, over all ranks; their sizes are what compile step 2
+ * balances.
+ *   cu_seqlens  host int32 [num_docs + 1] (rules of hsap_plan).
+ *   shard       N, P, layout, BM, BN; shard_id is ignored (every shard).
+ *   tiles       host int64 [P * P] or NULL: tiles[r * P + c].
+ *   pairs       host int64 [P * P] or NULL: pairs[r * P + c]; each row sums
+ *               to sum over shard r's queries i of (i - start(i) + 1).
+ *   At least one of tiles and pairs must be given.
+ */
+hsap_status hsap_load_matrix(const int32_t* cu_seqlens, int32_t num_docs, const hsap_shard_desc* shard,
+                             int64_t* tiles, int64_t* pairs);
+
+/*
+ * hsap_balance -- the Q-transfer rebalance of rank blocks over ranks (host).
+ * The workload balancing of compile step 2 (SAP section) follows LightSeq's
+ * scheduling, and HSAP balances InterSP groups by additionally transferring
+ * Q blocks; this is one concrete rule for it.  Block (r, c), r != c, runs
+ * either on rank r once chunk c's K/V reach it (the ring) or on rank c, the
+ * chunk's owner, once Q_r reaches it (its partial O and LSE then go back to
+ * r for the merge).  Diagonal and empty blocks stay on r.  The other blocks
+ * are taken longest first (equal costs: lower r, then lower c), each going
+ * to whichever of r and c carries the smaller load so far (equal loads: r).
+ *   cost       host int64 [P * P], >= 0: cost[r * P + c] of block (r, c),
+ *              e.g. its tiles from hsap_load_matrix.
+ *   exec_rank  host int32 [P * P] out: r or c, the rank computing the block.
+ *   load       host int64 [P] out or NULL: the summed cost per rank.
+ */
+hsap_status hsap_balance(int32_t sp_degree, const int64_t* cost, int32_t* exec_rank, int64_t* load);
+
+/*
  * hsap_doc_start -- device int32 [N]: start(t) for every position t.
  *   cu_seqlens  device int32 [num_docs + 1] (same rules as hsap_plan; the
  *               device copy is not re-validated).

@@ -34,7 +34,8 @@ MAX_MERGE_PARTS = 64
 
 # Every symbol include/hsap.h declares.
 EXPORTED = (
-    "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_doc_start",
+    "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_load_matrix",
+    "hsap_balance", "hsap_doc_start",
     "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
     "hsap_partial_attn_bwd", "hsap_attn_bwd_bf16", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
     "hsap_executor_plan", "hsap_executor_info", "hsap_executor_forward", "hsap_executor_partial_forward",
@@ -79,6 +80,8 @@ _SIG = {
     "hsap_plan": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _P, _P]),
     "hsap_plan_runs": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P, _I64, _P, _P]),
     "hsap_split_length": (ctypes.c_int32, [_P, _I64, _I32, _I32]),
+    "hsap_load_matrix": (ctypes.c_int, [_P, _I32, _P, _P, _P]),
+    "hsap_balance": (ctypes.c_int, [_I32, _P, _P, _P]),
     "hsap_doc_start": (ctypes.c_int, [_P, _I32, _I64, _P, _P]),
     "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
     "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
@@ -236,6 +239,28 @@ def plan_into(cu_seqlens: np.ndarray, shard: ShardDesc, tiles_out: np.ndarray, s
     _check(lib().hsap_plan(_ptr(cu_seqlens), len(cu_seqlens) - 1, ctypes.byref(shard), _ptr(tiles_out),
                            tiles_out.shape[0], ctypes.byref(num), _ptr(step_offsets_out), _ptr(useful_pairs_out)))
     return num.value
+
+
+def load_matrix(cu_seqlens, shard: ShardDesc):
+    """hsap_load_matrix: (tiles, pairs), int64 [P, P] indexed [shard r, chunk c]."""
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    P = shard.sp_degree
+    tiles = np.zeros((P, P), dtype=np.int64)
+    pairs = np.zeros((P, P), dtype=np.int64)
+    _check(lib().hsap_load_matrix(_ptr(cu), len(cu) - 1, ctypes.byref(shard), _ptr(tiles), _ptr(pairs)))
+    return tiles, pairs
+
+
+def balance(cost):
+    """hsap_balance: (exec_rank int32 [P, P], load int64 [P]) for block costs [P, P]."""
+    cost = np.ascontiguousarray(cost, dtype=np.int64)
+    if cost.ndim != 2 or cost.shape[0] != cost.shape[1]:
+        raise ValueError("cost must be a square [P, P] matrix")
+    P = cost.shape[0]
+    exec_rank = np.zeros((P, P), dtype=np.int32)
+    load = np.zeros(P, dtype=np.int64)
+    _check(lib().hsap_balance(int(P), _ptr(cost), _ptr(exec_rank), _ptr(load)))
+    return exec_rank, load
 
 
 def plan_runs_into(shard: ShardDesc, tiles: np.ndarray, num_tiles: int, major: int, max_run_tiles: int,

@@ -125,45 +125,25 @@ int64_t tile_pairs(const int32_t* cu, int64_t dq, int64_t qa, int64_t qb, int64_
   return total;
 }
 
-}  // namespace
-}  // namespace hsap
-
-using namespace hsap;
-
-extern "C" {
-
-const char* hsap_status_string(hsap_status status) {
-  switch (status) {
-    case HSAP_OK: return "HSAP_OK";
-    case HSAP_ERR_INVALID_ARG: return "HSAP_ERR_INVALID_ARG";
-    case HSAP_ERR_CAPACITY: return "HSAP_ERR_CAPACITY";
-    case HSAP_ERR_UNSUPPORTED: return "HSAP_ERR_UNSUPPORTED";
-    case HSAP_ERR_HIP: return "HSAP_ERR_HIP";
-  }
-  return "HSAP_ERR_UNKNOWN";
-}
-
-const char* hsap_last_error(void) { return g_last_error.c_str(); }
-
-hsap_status hsap_plan(const int32_t* cu, int32_t num_docs, const hsap_shard_desc* shard, hsap_tile* tiles,
-                      int64_t capacity, int64_t* num_tiles, int64_t* step_offsets, int64_t* useful_pairs) {
-  clear_error();
-  Geom g;
-  hsap_status st = check_shard(shard, &g);
-  if (st != HSAP_OK) return st;
+// cu_seqlens: 0 = cu[0] <= ... <= cu[num_docs] = N
+hsap_status check_cu(const int32_t* cu, int32_t num_docs, const Geom& g) {
   if (!cu) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens is NULL");
-  if (!num_tiles) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_tiles is NULL");
   if (num_docs < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_docs %d < 1", num_docs);
-  if (capacity < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "capacity < 0");
   if (cu[0] != 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens[0] = %d, expected 0", cu[0]);
   for (int32_t i = 0; i < num_docs; ++i)
     if (cu[i + 1] < cu[i]) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens decreases at %d", i + 1);
   if ((int64_t)cu[num_docs] != g.N)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens[%d] = %d, expected total_tokens %lld", num_docs, cu[num_docs],
               (long long)g.N);
+  return HSAP_OK;
+}
 
-  const int32_t P = g.P, r = shard->shard_id;
-  const int64_t BM = shard->block_m, BN = shard->block_n;
+// The non-empty tiles of one shard (validated geometry and cu_seqlens) in canonical order: stores
+// the first `capacity` of them when `tiles` is not NULL and returns how many there are.
+int64_t plan_shard(const int32_t* cu, int32_t num_docs, const Geom& g, const hsap_shard_desc& shard, hsap_tile* tiles,
+                   int64_t capacity, int64_t* step_offsets, int64_t* useful_pairs) {
+  const int32_t P = g.P, r = shard.shard_id;
+  const int64_t BM = shard.block_m, BN = shard.block_n;
   const int64_t full = BM * BN;
   Piece qp[2], kp[2];
   const int nq_pieces = shard_pieces(g, r, qp);
@@ -202,9 +182,107 @@ hsap_status hsap_plan(const int32_t* cu, int32_t num_docs, const hsap_shard_desc
     if (step_offsets) step_offsets[step + 1] = count;
     if (useful_pairs) useful_pairs[step] = step_pairs;
   }
+  return count;
+}
+
+}  // namespace
+}  // namespace hsap
+
+using namespace hsap;
+
+extern "C" {
+
+const char* hsap_status_string(hsap_status status) {
+  switch (status) {
+    case HSAP_OK: return "HSAP_OK";
+    case HSAP_ERR_INVALID_ARG: return "HSAP_ERR_INVALID_ARG";
+    case HSAP_ERR_CAPACITY: return "HSAP_ERR_CAPACITY";
+    case HSAP_ERR_UNSUPPORTED: return "HSAP_ERR_UNSUPPORTED";
+    case HSAP_ERR_HIP: return "HSAP_ERR_HIP";
+  }
+  return "HSAP_ERR_UNKNOWN";
+}
+
+const char* hsap_last_error(void) { return g_last_error.c_str(); }
+
+hsap_status hsap_plan(const int32_t* cu, int32_t num_docs, const hsap_shard_desc* shard, hsap_tile* tiles,
+                      int64_t capacity, int64_t* num_tiles, int64_t* step_offsets, int64_t* useful_pairs) {
+  clear_error();
+  Geom g;
+  hsap_status st = check_shard(shard, &g);
+  if (st != HSAP_OK) return st;
+  if (!num_tiles) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_tiles is NULL");
+  if (capacity < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "capacity < 0");
+  st = check_cu(cu, num_docs, g);
+  if (st != HSAP_OK) return st;
+  const int64_t count = plan_shard(cu, num_docs, g, *shard, tiles, capacity, step_offsets, useful_pairs);
   *num_tiles = count;
-  if (!store || count > capacity)
+  if (!tiles || count > capacity)
     HSAP_FAIL(HSAP_ERR_CAPACITY, "tile list needs %lld entries, capacity %lld", (long long)count, (long long)capacity);
+  return HSAP_OK;
+}
+
+hsap_status hsap_load_matrix(const int32_t* cu, int32_t num_docs, const hsap_shard_desc* shard, int64_t* tiles,
+                             int64_t* pairs) {
+  clear_error();
+  if (!shard) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "shard descriptor is NULL");
+  if (!tiles && !pairs) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "tiles and pairs are both NULL");
+  hsap_shard_desc sd = *shard;
+  sd.shard_id = 0;  // every shard is planned; only the geometry of the descriptor is used
+  Geom g;
+  hsap_status st = check_shard(&sd, &g);
+  if (st != HSAP_OK) return st;
+  st = check_cu(cu, num_docs, g);
+  if (st != HSAP_OK) return st;
+  const int32_t P = g.P;
+  std::vector<int64_t> offs((size_t)P + 1), step_pairs((size_t)P);
+  for (int32_t r = 0; r < P; ++r) {
+    sd.shard_id = r;
+    plan_shard(cu, num_docs, g, sd, nullptr, 0, offs.data(), step_pairs.data());
+    for (int32_t step = 0; step < P; ++step) {
+      const int32_t c = ((r - step) % P + P) % P;
+      if (tiles) tiles[(int64_t)r * P + c] = offs[(size_t)step + 1] - offs[(size_t)step];
+      if (pairs) pairs[(int64_t)r * P + c] = step_pairs[(size_t)step];
+    }
+  }
+  return HSAP_OK;
+}
+
+hsap_status hsap_balance(int32_t sp_degree, const int64_t* cost, int32_t* exec_rank, int64_t* load) {
+  clear_error();
+  if (sp_degree < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "sp_degree %d < 1", sp_degree);
+  if (!cost || !exec_rank) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL cost or exec_rank");
+  const int64_t P = sp_degree;
+  for (int64_t i = 0; i < P * P; ++i)
+    if (cost[i] < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cost[%lld] < 0", (long long)i);
+  struct Block {
+    int64_t w;
+    int32_t r, c;
+  };
+  std::vector<Block> blocks;
+  std::vector<int64_t> ld((size_t)P);
+  for (int32_t r = 0; r < P; ++r) {
+    ld[(size_t)r] = cost[r * P + r];
+    for (int32_t c = 0; c < P; ++c) {
+      exec_rank[r * P + c] = r;
+      if (c != r && cost[r * P + c] > 0) blocks.push_back(Block{cost[r * P + c], r, c});
+    }
+  }
+  // longest first; equal costs by shard, then chunk
+  std::sort(blocks.begin(), blocks.end(), [](const Block& a, const Block& b) {
+    if (a.w != b.w) return a.w > b.w;
+    if (a.r != b.r) return a.r < b.r;
+    return a.c < b.c;
+  });
+  for (const Block& b : blocks) {
+    if (ld[(size_t)b.c] < ld[(size_t)b.r]) {  // the chunk's owner computes it: Q_r moves, not K/V of c
+      exec_rank[b.r * P + b.c] = b.c;
+      ld[(size_t)b.c] += b.w;
+    } else {
+      ld[(size_t)b.r] += b.w;
+    }
+  }
+  if (load) std::copy(ld.begin(), ld.end(), load);
   return HSAP_OK;
 }
 

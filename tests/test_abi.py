@@ -204,6 +204,25 @@ def test_merge_and_helpers_validate():
     assert lib.hsap_shard_gather(ctypes.byref(d), fake, fake, 12, None) == L.HSAP_ERR_INVALID_ARG
 
 
+def test_load_matrix_and_balance_validate():
+    lib = L.lib()
+    cu = np.asarray([0, 1024], dtype=np.int32)
+    out = np.zeros(4, dtype=np.int64)
+    s = L.shard_desc(1024, 2, "contiguous", 0, 128, 128)
+    assert lib.hsap_load_matrix(cu.ctypes.data, 1, ctypes.byref(s), None, None) == L.HSAP_ERR_INVALID_ARG
+    bad = np.asarray([0, 1000], dtype=np.int32)               # does not end at N
+    assert lib.hsap_load_matrix(bad.ctypes.data, 1, ctypes.byref(s), out.ctypes.data, None) == L.HSAP_ERR_INVALID_ARG
+    odd = L.shard_desc(1000, 2, "contiguous", 0, 128, 128)    # BM does not divide n
+    assert lib.hsap_load_matrix(cu.ctypes.data, 1, ctypes.byref(odd), out.ctypes.data, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_load_matrix(cu.ctypes.data, 1, ctypes.byref(s), out.ctypes.data, None) == 0
+    assert out.tolist() == [10, 0, 16, 10]      # one causal document: 4 x 4 tiles per block, 10 on or below the diagonal
+    cost = np.asarray([1, -1, 0, 1], dtype=np.int64)
+    ex = np.zeros(4, dtype=np.int32)
+    assert lib.hsap_balance(2, cost.ctypes.data, ex.ctypes.data, None) == L.HSAP_ERR_INVALID_ARG   # negative cost
+    assert lib.hsap_balance(0, cost.ctypes.data, ex.ctypes.data, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_balance(2, None, ex.ctypes.data, None) == L.HSAP_ERR_INVALID_ARG
+
+
 def test_executor_struct_layout():
     assert ctypes.sizeof(L.ExecInfo) == 72
 

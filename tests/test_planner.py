@@ -155,3 +155,59 @@ def test_split_length():
     assert L.split_length(d, 10, 1, 512) == 8                   # floor: a quarter of a chunk's k-tiles
     with pytest.raises(L.HsapError):
         L.split_length(d, 10, 0, 512)
+
+
+# ---------------------------------------------------------------------------
+# block loads of every shard (hsap_load_matrix) and the Q-transfer rebalance (hsap_balance)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(16))
+def test_load_matrix_against_oracle(seed):
+    rng = np.random.default_rng(2000 + seed)
+    P = int(rng.choice([1, 2, 4, 8]))
+    layout = str(rng.choice(["contiguous", "zigzag"]))
+    bm, bn = int(rng.choice([16, 32, 64])), int(rng.choice([16, 32, 64]))
+    split = 2 * P if layout == "zigzag" else P
+    N = split * max(bm, bn) * int(rng.integers(1, 3))
+    cu = _rand_cu(rng, N)
+    tiles, pairs = L.load_matrix(cu, L.shard_desc(N, P, layout, 0, bm, bn))
+    ref_tiles, ref_pairs = oracle.load_matrix(cu, N, P, layout, bm, bn)
+    assert np.array_equal(tiles, ref_tiles) and np.array_equal(pairs, ref_pairs)
+
+
+@pytest.mark.parametrize("name", ["c2", "c5"])
+def test_load_matrix_workloads(name):
+    w = make_workload(name)
+    s = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, 0, w.block_m, w.block_n)
+    tiles, pairs = L.load_matrix(w.cu_seqlens, s)
+    for r in range(w.sp_degree):   # each row is shard r's plan, ring step s at chunk (r - s) mod P
+        p = L.plan(w.cu_seqlens, L.shard_desc(w.total_tokens, w.sp_degree, w.layout, r, w.block_m, w.block_n))
+        for step in range(w.sp_degree):
+            c = (r - step) % w.sp_degree
+            assert tiles[r, c] == p["step_offsets"][step + 1] - p["step_offsets"][step]
+            assert pairs[r, c] == p["useful_pairs"][step]
+    lengths = np.diff(w.cu_seqlens).astype(np.int64)
+    assert int(pairs.sum()) == int(np.sum(lengths * (lengths + 1) // 2))
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_balance_against_oracle(seed):
+    rng = np.random.default_rng(3000 + seed)
+    P = int(rng.integers(1, 17))
+    cost = (rng.integers(0, 50, size=(P, P)) * (rng.random((P, P)) < 0.5)).astype(np.int64)
+    if seed % 4 == 0:
+        cost[:] = rng.integers(0, 3, size=(P, P))      # many equal costs: the tie rules decide
+    exec_rank, load = L.balance(cost)
+    ref_exec, ref_load = oracle.q_transfer_balance(cost)
+    assert np.array_equal(exec_rank, ref_exec) and np.array_equal(load, ref_load)
+
+
+@pytest.mark.parametrize("layout", ["contiguous", "zigzag"])
+def test_balance_of_workload_loads(layout):
+    w = make_workload("c2")
+    tiles, _ = L.load_matrix(w.cu_seqlens, L.shard_desc(w.total_tokens, w.sp_degree, layout, 0, w.block_m,
+                                                       w.block_n))
+    exec_rank, load = L.balance(tiles)
+    ref_exec, ref_load = oracle.q_transfer_balance(tiles)
+    assert np.array_equal(exec_rank, ref_exec) and np.array_equal(load, ref_load)
+    assert int(load.sum()) == int(tiles.sum())
