@@ -212,9 +212,13 @@ hsap_status hsap_load_matrix(const int32_t* cu_seqlens, int32_t num_docs, const 
  * Q blocks; this is one concrete rule for it.  Block (r, c), r != c, runs
  * either on rank r once chunk c's K/V reach it (the ring) or on rank c, the
  * chunk's owner, once Q_r reaches it (its partial O and LSE then go back to
- * r for the merge).  Diagonal and empty blocks stay on r.  The other blocks
- * are taken longest first (equal costs: lower r, then lower c), each going
- * to whichever of r and c carries the smaller load so far (equal loads: r).
+ * r for the merge).  Diagonal and empty blocks stay on r.  Starting from the
+ * ring (every block on r), the most loaded rank (lowest index among equals)
+ * hands one of its blocks to the block's other eligible rank while the
+ * receiver stays below the giver's load, choosing the move that leaves the
+ * smaller maximum of the two loads (equal: lower r, then lower c); it stops
+ * when the most loaded rank has no such move.  The result is never worse
+ * than the ring.
  *   cost       host int64 [P * P], >= 0: cost[r * P + c] of block (r, c),
  *              e.g. its tiles from hsap_load_matrix.
  *   exec_rank  host int32 [P * P] out: r or c, the rank computing the block.

@@ -8,16 +8,20 @@ path imports this module.
   chunk c (key rows), the number of non-empty BM x BN tiles and of allowed
   (query, key) pairs, taken from the per-shard plan of ``plan.plan_shard``.
 * ``q_transfer_balance`` -- the workload balancing of compile step 2, which the
-  paper bases on LightSeq's scheduling, and the balancing of InterSP groups by
-  additionally transferring Q blocks (memory and communication section).  The
-  paper gives no algorithm; the reading used here: a block (r, c) with r != c
-  runs either on rank r once chunk c's K/V reach it (the ring), or on rank c,
-  the owner of chunk c, once Q_r reaches it (its partial O and LSE then travel
-  back to r for the merge).  Diagonal blocks stay on their rank.  Off-diagonal
-  non-empty blocks are taken by decreasing cost (ties: lower r, then lower c)
-  and each goes to whichever of r and c carries the smaller load so far (ties:
-  r, i.e. no transfer) -- list scheduling, longest first, with two eligible
-  ranks per block.
+  paper bases on LightSeq's scheduling and which it states as balancing the
+  number of attention blocks each rank computes, together with the balancing
+  of InterSP groups by additionally transferring Q blocks (memory and
+  communication section).  The paper gives no algorithm; the reading used
+  here: a block (r, c) with r != c runs either on rank r once chunk c's K/V
+  reach it (the ring), or on rank c, the owner of chunk c, once Q_r reaches it
+  (its partial O and LSE then travel back to r for the merge).  Diagonal
+  blocks stay on their rank.  Starting from the ring assignment, the most
+  loaded rank (lowest index among equals) hands one of its blocks to that
+  block's other eligible rank, as long as the receiver stays below the giver's
+  current load; among such moves the one leaving the smaller of the two new
+  loads' maximum is taken (equal: lower r, then lower c).  It stops when the
+  most loaded rank has no such move.  Every move lowers the sum of squared
+  loads, so it ends.
 
 Pins (``tests/test_oracle_pins.py``): pair counts against the dense mask and
 the closed-form per-shard total; the assignment against brute force over every
@@ -58,13 +62,25 @@ def q_transfer_balance(cost) -> Tuple[np.ndarray, np.ndarray]:
     cost = np.asarray(cost, dtype=np.int64)
     P = cost.shape[0]
     exec_rank = np.repeat(np.arange(P, dtype=np.int32)[:, None], P, axis=1)
-    load = np.array([int(cost[r, r]) for r in range(P)], dtype=np.int64)
-    blocks = [(int(cost[r, c]), r, c) for r in range(P) for c in range(P) if r != c and cost[r, c] > 0]
-    blocks.sort(key=lambda b: (-b[0], b[1], b[2]))
-    for w, r, c in blocks:
-        if load[c] < load[r]:
-            exec_rank[r, c] = c
-            load[c] += w
-        else:
-            load[r] += w
-    return exec_rank, load
+    load = [int(cost[r].sum()) for r in range(P)]
+    while True:
+        giver = max(range(P), key=lambda e: (load[e], -e))      # most loaded, lowest index among equals
+        best = None
+        for r in range(P):
+            for c in range(P):
+                w = int(cost[r, c])
+                if r == c or w == 0 or giver not in (r, c) or exec_rank[r, c] != giver:
+                    continue
+                taker = c if giver == r else r
+                if load[taker] + w >= load[giver]:
+                    continue
+                key = (max(load[giver] - w, load[taker] + w), r, c)
+                if best is None or key < best[0]:
+                    best = (key, r, c, taker, w)
+        if best is None:
+            break
+        _, r, c, taker, w = best
+        exec_rank[r, c] = taker
+        load[giver] -= w
+        load[taker] += w
+    return exec_rank, np.asarray(load, dtype=np.int64)

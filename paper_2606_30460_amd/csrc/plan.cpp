@@ -255,32 +255,49 @@ hsap_status hsap_balance(int32_t sp_degree, const int64_t* cost, int32_t* exec_r
   const int64_t P = sp_degree;
   for (int64_t i = 0; i < P * P; ++i)
     if (cost[i] < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cost[%lld] < 0", (long long)i);
-  struct Block {
-    int64_t w;
-    int32_t r, c;
-  };
-  std::vector<Block> blocks;
-  std::vector<int64_t> ld((size_t)P);
-  for (int32_t r = 0; r < P; ++r) {
-    ld[(size_t)r] = cost[r * P + r];
+  // ring assignment: every block on its shard's rank
+  std::vector<int64_t> ld((size_t)P, 0);
+  for (int32_t r = 0; r < P; ++r)
     for (int32_t c = 0; c < P; ++c) {
       exec_rank[r * P + c] = r;
-      if (c != r && cost[r * P + c] > 0) blocks.push_back(Block{cost[r * P + c], r, c});
+      ld[(size_t)r] += cost[r * P + c];
     }
-  }
-  // longest first; equal costs by shard, then chunk
-  std::sort(blocks.begin(), blocks.end(), [](const Block& a, const Block& b) {
-    if (a.w != b.w) return a.w > b.w;
-    if (a.r != b.r) return a.r < b.r;
-    return a.c < b.c;
-  });
-  for (const Block& b : blocks) {
-    if (ld[(size_t)b.c] < ld[(size_t)b.r]) {  // the chunk's owner computes it: Q_r moves, not K/V of c
-      exec_rank[b.r * P + b.c] = b.c;
-      ld[(size_t)b.c] += b.w;
-    } else {
-      ld[(size_t)b.r] += b.w;
+  // The most loaded rank (lowest index among equals) hands one block to the block's other
+  // eligible rank while the receiver stays below the giver's load; the move leaving the smaller
+  // maximum of the two loads wins (equal: lower r, then lower c).  Each move lowers the sum of
+  // squared loads, so the loop ends.
+  for (;;) {
+    int32_t g = 0;
+    for (int32_t e = 1; e < P; ++e)
+      if (ld[(size_t)e] > ld[(size_t)g]) g = e;
+    int64_t best_key = -1;
+    int32_t best_r = -1, best_c = -1, best_t = -1;
+    auto consider = [&](int32_t r, int32_t c) {
+      const int64_t w = cost[r * P + c];
+      if (r == c || w == 0 || exec_rank[r * P + c] != g) return;
+      const int32_t t = g == r ? c : r;
+      if (ld[(size_t)t] + w >= ld[(size_t)g]) return;
+      const int64_t key = std::max(ld[(size_t)g] - w, ld[(size_t)t] + w);
+      // (key, r, c) lexicographic; candidates arrive in increasing (r, c) order below
+      if (best_key < 0 || key < best_key) {
+        best_key = key;
+        best_r = r;
+        best_c = c;
+        best_t = t;
+      }
+    };
+    // blocks rank g may hold: its own row (g, c) and transferred blocks (r, g), in (r, c) order
+    for (int32_t r = 0; r < P; ++r) {
+      if (r == g)
+        for (int32_t c = 0; c < P; ++c) consider(g, c);
+      else
+        consider(r, g);
     }
+    if (best_key < 0) break;
+    const int64_t w = cost[best_r * P + best_c];
+    exec_rank[best_r * P + best_c] = best_t;
+    ld[(size_t)g] -= w;
+    ld[(size_t)best_t] += w;
   }
   if (load) std::copy(ld.begin(), ld.end(), load);
   return HSAP_OK;

@@ -526,16 +526,29 @@ def _best_max_load(cost):
 
 
 def test_q_transfer_balance_worked_example():
-    # Lower-triangular costs (causal, contiguous).  Diagonal loads start at [4, 3, 2].  The
-    # off-diagonal blocks by decreasing cost: (2, 1) w 7 -- rank 2 (load 2) is not above rank 1
-    # (load 3), stays: [4, 3, 9]; (1, 0) w 6 -- rank 1 (3) is below rank 0 (4), stays:
-    # [4, 9, 9]; (2, 0) w 5 -- rank 0 (4) is below rank 2 (9), moves to 0: [9, 9, 9].
+    # Lower-triangular costs (causal, contiguous).  Ring loads [4, 9, 14].  Rank 2 gives: (2, 0)
+    # w 5 to rank 0 leaves max(9, 9) = 9, (2, 1) w 7 to rank 1 would leave max(7, 16): take (2, 0)
+    # -> [9, 9, 9].  Rank 0 (lowest of the equals) holds (2, 0) w 5; back to rank 2: 9 + 5 is
+    # not below 9, so it stops.
     cost = np.array([[4, 0, 0], [6, 3, 0], [5, 7, 2]])
     exec_rank, load = oracle.q_transfer_balance(cost)
     assert load.tolist() == [9, 9, 9]
     assert exec_rank.tolist() == [[0, 0, 0], [1, 1, 1], [0, 2, 2]]   # empty blocks keep their row
     _check_assignment(cost, exec_rank, load)
     assert _best_max_load(cost)[0] == 9
+
+
+def test_q_transfer_balance_one_causal_document():
+    # one document over four contiguous shards of 8 x 8 tiles: diagonal blocks 36, below 64.
+    # Ring loads [36, 100, 164, 228]; rank 3 gives (3, 0) to rank 0 (max(164, 100) = 164, the
+    # same as (3, 1) -> rank 1 but lower c): [100, 100, 164, 164]; rank 2 then has no move
+    # (100 + 64 is not below 164).  Six equal blocks on four ranks: 164 is the optimum.
+    cost = np.array([[36, 0, 0, 0], [64, 36, 0, 0], [64, 64, 36, 0], [64, 64, 64, 36]])
+    exec_rank, load = oracle.q_transfer_balance(cost)
+    assert load.tolist() == [100, 100, 164, 164]
+    assert exec_rank[3].tolist() == [0, 3, 3, 3] and exec_rank[2].tolist() == [2, 2, 2, 2]
+    _check_assignment(cost, exec_rank, load)
+    assert _best_max_load(cost)[0] == 164
 
 
 @pytest.mark.parametrize("seed", range(40))
@@ -546,6 +559,6 @@ def test_q_transfer_balance_against_every_assignment(seed):
     exec_rank, load = oracle.q_transfer_balance(cost)
     _check_assignment(cost, exec_rank, load)
     best, movable = _best_max_load(cost)
-    assert best <= int(load.max()) <= int(cost.sum())
-    if movable <= 1:   # one decision: taking the less loaded rank is optimal
+    assert best <= int(load.max()) <= int(cost.sum(axis=1).max())   # never worse than the ring
+    if movable <= 1:   # one decision: the search finds the better side
         assert int(load.max()) == best
