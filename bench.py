@@ -252,6 +252,58 @@ def cpu_baseline(name: str, budget_s: float):
             "cpu": cpu_model, "affinity_cores": cores}
 
 
+def all_shards_analysis(name: str, layouts=None, reps: int = 5) -> dict:
+    """Every shard of the workload's packed sequence on this GPU, ring and balanced schedules
+    (hsap_load_matrix, hsap_balance): per-rank tiles and milliseconds (blocks + merge, median of
+    ``reps``), the critical path, and the whole sequence's useful TFLOP/s at that critical path,
+    i.e. what a group of P GPUs would reach if each ran its rank's work alone, without transfers."""
+    import torch
+    from paper_2606_30460_amd import _lib as L
+    from paper_2606_30460_amd.all_shards import AllShards
+    from paper_2606_30460_amd.shard_attention import to_sharded
+    from workloads import make_workload, random_bf16
+
+    w = make_workload(name)
+    dev = torch.device("cuda")
+    N, P = w.total_tokens, w.sp_degree
+    q = random_bf16((N, w.heads_q, w.head_dim), w.seed + 1).to(dev)
+    k = random_bf16((N, w.heads_kv, w.head_dim), w.seed + 2).to(dev)
+    v = random_bf16((N, w.heads_kv, w.head_dim), w.seed + 3).to(dev)
+    lengths = np.diff(w.cu_seqlens).astype(np.int64)
+    flops = 4.0 * w.head_dim * w.heads_q * float(np.sum(lengths * (lengths + 1) // 2))
+    out = {}
+    for layout in (layouts or [w.layout]):
+        s = L.shard_desc(N, P, layout, 0, w.block_m, w.block_n)
+        qs, ks, vs = to_sharded(s, q), to_sharded(s, k), to_sharded(s, v)
+        res = {}
+        for balanced in (False, True):
+            a = AllShards(w.cu_seqlens, N, P, layout, w.heads_q, w.heads_kv, w.head_dim, w.block_m, w.block_n,
+                          balance=balanced)
+            a.plan()
+            bufs = a.alloc()
+            for _ in range(2):
+                a.forward(qs, ks, vs, bufs)
+            times = [a.forward(qs, ks, vs, bufs, timed=True) for _ in range(reps)]
+            rank_ms = (np.median([t["blocks_ms"] for t in times], axis=0)
+                       + np.median([t["merge_ms"] for t in times], axis=0))
+            sched = a.schedule()
+            crit = float(rank_ms.max())
+            res["balanced" if balanced else "ring"] = {
+                "rank_tiles": sched["rank_tiles"], "tile_imbalance": round(sched["tile_imbalance"], 3),
+                "moved_blocks": sched["moved_blocks"], "rank_ms": [round(x, 4) for x in rank_ms.tolist()],
+                "critical_ms": round(crit, 4), "rank_ms_mean": round(float(rank_ms.mean()), 4),
+                "sequence_tflops_at_critical_path": round(flops / (crit * 1e-3) / 1e12, 1),
+                "kv_bytes_moved": sched["kv_bytes_moved"], "q_o_bytes_moved": sched["q_o_bytes_moved"]}
+            del bufs, a
+            torch.cuda.empty_cache()
+        log("[bench] all shards %s %s: critical path ring %.3f ms, balanced %.3f ms" % (
+            name, layout, res["ring"]["critical_ms"], res["balanced"]["critical_ms"]))
+        out[layout] = res
+    del q, k, v
+    torch.cuda.empty_cache()
+    return out
+
+
 FWD_SOURCES = ("paper_2606_30460_amd/csrc/attn_fwd.hip", "paper_2606_30460_amd/csrc/mfma.h",
                "paper_2606_30460_amd/csrc/hsap_internal.h")
 TRAFFIC_SUMMARY = "profiles/attn_fwd_hbm_traffic.md"
@@ -310,6 +362,10 @@ def main():
     ap.add_argument("--workload", default="c2")
     ap.add_argument("--extra", default="c3,c4,c5", help="other workloads reported under 'extra' ('' for none)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle budget for the CPU baseline (0: skip)")
+    ap.add_argument("--no-all-shards", action="store_true",
+                    help="skip the all-shard load analysis of the main workload (e.g. under a kernel trace)")
+    ap.add_argument("--all-shards", default="", metavar="WORKLOADS",
+                    help="only run the all-shard load analysis (both layouts) of these workloads and print it")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter calibration) and exit")
     args = ap.parse_args()
@@ -326,6 +382,10 @@ def main():
         sys.exit(1)
     from paper_2606_30460_amd import _lib as L
     L.lib()
+    if args.all_shards:
+        print(json.dumps({name: all_shards_analysis(name, ["contiguous", "zigzag"])
+                          for name in args.all_shards.split(",") if name}), flush=True)
+        return
 
     main_res = measure(args.workload, args.steps, args.warmup)
     extra = {}
@@ -333,6 +393,8 @@ def main():
         r = measure(name, min(args.steps, 20), min(args.warmup, 3))
         r.pop("_fwd_flops", None)
         extra[name] = r
+    if not args.no_all_shards:
+        main_res["all_shards"] = all_shards_analysis(args.workload)
     cpu = None
     if args.cpu_seconds > 0:
         log("[bench] CPU baseline (oracle) on %s, ~%.0f s" % (args.workload, args.cpu_seconds))
