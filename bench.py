@@ -129,11 +129,16 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     for _ in range(warmup):
         one_step(None)
     torch.cuda.synchronize()
+    # the step rate, timed with nothing between the launches; then the same steps again with
+    # events around each stage for the per-kernel breakdown (event markers add small gaps)
     t0 = time.perf_counter()
+    for i in range(steps):
+        one_step(None)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
     for i in range(steps):
         one_step(events[i])
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     info = ex.info()
 
     fwd_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
