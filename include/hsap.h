@@ -226,6 +226,62 @@ hsap_status hsap_load_matrix(const int32_t* cu_seqlens, int32_t num_docs, const 
  */
 hsap_status hsap_balance(int32_t sp_degree, const int64_t* cost, int32_t* exec_rank, int64_t* load);
 
+/* Instruction set of the per-rank programs (instruction table of the SAP
+ * section): send / receive of a tensor to / from a peer, computing one rank
+ * block, and the copy-and-rescale of partial outputs (one merge of all of a
+ * shard's parts). */
+typedef enum { HSAP_OP_SEND = 0, HSAP_OP_RECV = 1, HSAP_OP_COMPUTE = 2, HSAP_OP_MERGE = 3 } hsap_op_kind;
+typedef enum { HSAP_T_NONE = -1, HSAP_T_Q = 0, HSAP_T_KV = 1, HSAP_T_O = 2 } hsap_tensor_kind;
+
+/* One instruction, 32-byte POD.  Buffers of a rank: its own Q shard and K/V
+ * chunk; two receive slots each for Q and K/V; two result slots for the
+ * partials it computes for other shards; one part slot per chunk with tiles
+ * of its own shard (part index = that chunk's rank among them).
+ *   SEND     tensor (Q: shard; KV: chunk; O: shard and chunk) to `peer`;
+ *            in_slot = result slot for O, -1 for the own Q / K/V.
+ *   RECV     the matching tensor from `peer` into out_slot (receive slot for
+ *            Q and K/V, part index for O).
+ *   COMPUTE  block (shard, chunk): Q is the own shard or receive slot
+ *            in_slot, K/V the own chunk or receive slot in_slot (-1 when
+ *            both are local); the partial goes to part out_slot (own shard)
+ *            or result slot out_slot (another shard's).
+ *   MERGE    the out_slot parts of the own shard into its output. */
+typedef struct {
+  int32_t op;        /* hsap_op_kind */
+  int32_t tensor;    /* hsap_tensor_kind (SEND, RECV) */
+  int32_t peer;      /* SEND: destination rank; RECV: source rank; else -1 */
+  int32_t stage;
+  int32_t shard;     /* query shard of the block, Q or O; -1 for K/V */
+  int32_t chunk;     /* chunk of the block, K/V or O; -1 for Q */
+  int32_t in_slot;
+  int32_t out_slot;
+} hsap_op;
+
+/*
+ * hsap_emit_forward -- the per-rank instruction lists of the forward pass
+ * (host), the jitted code generation of the SAP section: each rank computes
+ * the non-empty blocks assigned to it one per stage -- its diagonal block
+ * first, then by ring step (r - c) mod P, shard, chunk (a rank without a
+ * diagonal block starts at stage 1).  Inputs arrive one stage ahead straight
+ * from their owner into receive slot (stage % 2); a block computed for another
+ * shard returns its partial one stage later; the last stage returns the last
+ * partials and merges.  Within a stage a rank lists its sends and receives
+ * (ordered by peer, send before receive, tensor, shard, chunk), then its
+ * computation, then the merge.  Every SEND has the matching RECV at the same
+ * stage of the peer's list, so each stage's transfers form one batched
+ * point-to-point group.
+ *   block_tiles   host int64 [P * P]: non-empty tiles of block (r, c)
+ *                 (hsap_load_matrix); empty blocks are not computed.
+ *   exec_rank     host int32 [P * P]: r or c for every non-empty block
+ *                 (hsap_balance, or r everywhere for the plain ring).
+ *   ops           host [capacity] or NULL: rank e's instructions are
+ *                 ops[rank_offsets[e] .. rank_offsets[e+1]-1], by stage.
+ *   rank_offsets  host int64 [P + 1] out (also on HSAP_ERR_CAPACITY).
+ *   num_stages    out: stages of the program (compute stages + 1).
+ */
+hsap_status hsap_emit_forward(int32_t sp_degree, const int64_t* block_tiles, const int32_t* exec_rank, hsap_op* ops,
+                              int64_t capacity, int64_t* rank_offsets, int32_t* num_stages);
+
 /*
  * hsap_doc_start -- device int32 [N]: start(t) for every position t.
  *   cu_seqlens  device int32 [num_docs + 1] (same rules as hsap_plan; the

@@ -32,6 +32,9 @@ What it computes, with the passages it follows (HSAP paper, arxiv 2606.30460):
 * ``balance`` -- the per-(shard, chunk) block sizes of every shard and the
   Q-transfer rebalance of the blocks over ranks (compile step 2, and the
   balancing of InterSP groups by transferring Q blocks).
+* ``schedule`` -- the per-rank instruction lists of the forward pass (the
+  jitted code generation of the SAP section, with the paper's instruction
+  set), arranged in stages with matched sends and receives.
 
 Parity status: every function above is pinned by ``tests/test_oracle_pins.py``
 against brute force, closed forms, library routines or invariants; none is
@@ -54,3 +57,4 @@ from .plan import (  # noqa: F401
     useful_pairs_all_shards,
 )
 from .balance import load_matrix, q_transfer_balance  # noqa: F401
+from .schedule import forward_program  # noqa: F401

@@ -35,7 +35,7 @@ MAX_MERGE_PARTS = 64
 # Every symbol include/hsap.h declares.
 EXPORTED = (
     "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_load_matrix",
-    "hsap_balance", "hsap_doc_start",
+    "hsap_balance", "hsap_emit_forward", "hsap_doc_start",
     "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
     "hsap_partial_attn_bwd", "hsap_attn_bwd_bf16", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
     "hsap_executor_plan", "hsap_executor_info", "hsap_executor_forward", "hsap_executor_partial_forward",
@@ -82,6 +82,7 @@ _SIG = {
     "hsap_split_length": (ctypes.c_int32, [_P, _I64, _I32, _I32]),
     "hsap_load_matrix": (ctypes.c_int, [_P, _I32, _P, _P, _P]),
     "hsap_balance": (ctypes.c_int, [_I32, _P, _P, _P]),
+    "hsap_emit_forward": (ctypes.c_int, [_I32, _P, _P, _P, _I64, _P, _P]),
     "hsap_doc_start": (ctypes.c_int, [_P, _I32, _I64, _P, _P]),
     "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
     "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
@@ -261,6 +262,27 @@ def balance(cost):
     load = np.zeros(P, dtype=np.int64)
     _check(lib().hsap_balance(int(P), _ptr(cost), _ptr(exec_rank), _ptr(load)))
     return exec_rank, load
+
+
+OP_SEND, OP_RECV, OP_COMPUTE, OP_MERGE = 0, 1, 2, 3
+T_NONE, T_Q, T_KV, T_O = -1, 0, 1, 2
+
+
+def emit_forward(block_tiles, exec_rank):
+    """hsap_emit_forward with the two-call pattern: (list of int32 [ops_e, 8] arrays per rank --
+    fields op, tensor, peer, stage, shard, chunk, in_slot, out_slot -- and the number of stages)."""
+    tiles = np.ascontiguousarray(block_tiles, dtype=np.int64)
+    ex = np.ascontiguousarray(exec_rank, dtype=np.int32)
+    P = tiles.shape[0]
+    offs = np.zeros(P + 1, dtype=np.int64)
+    stages = ctypes.c_int32(0)
+    st = lib().hsap_emit_forward(int(P), _ptr(tiles), _ptr(ex), None, 0, _ptr(offs), ctypes.byref(stages))
+    if st != HSAP_ERR_CAPACITY:
+        _check(st)
+    ops = np.zeros((max(int(offs[P]), 1), 8), dtype=np.int32)
+    _check(lib().hsap_emit_forward(int(P), _ptr(tiles), _ptr(ex), _ptr(ops), int(offs[P]), _ptr(offs),
+                                   ctypes.byref(stages)))
+    return [ops[offs[e]:offs[e + 1]] for e in range(P)], int(stages.value)
 
 
 def plan_runs_into(shard: ShardDesc, tiles: np.ndarray, num_tiles: int, major: int, max_run_tiles: int,
