@@ -261,10 +261,14 @@ def all_shards_analysis(name: str, layouts=None, reps: int = 5) -> dict:
     """Every shard of the workload's packed sequence on this GPU, ring and balanced schedules
     (hsap_load_matrix, hsap_balance): per-rank tiles and milliseconds (blocks + merge, median of
     ``reps``), the critical path, and the whole sequence's useful TFLOP/s at that critical path,
-    i.e. what a group of P GPUs would reach if each ran its rank's work alone, without transfers."""
+    i.e. what a group of P GPUs would reach if each ran its rank's work alone, without transfers.
+    The same assignment also runs as per-rank instruction lists (hsap_emit_forward) with every
+    rank's stream on this one GPU: its stages, instruction count and wall time (all ranks' work
+    plus the transfers as device copies, on one GPU)."""
     import torch
     from paper_2606_30460_amd import _lib as L
     from paper_2606_30460_amd.all_shards import AllShards
+    from paper_2606_30460_amd.sap_program import SapProgram
     from paper_2606_30460_amd.shard_attention import to_sharded
     from workloads import make_workload, random_bf16
 
@@ -293,14 +297,26 @@ def all_shards_analysis(name: str, layouts=None, reps: int = 5) -> dict:
                        + np.median([t["merge_ms"] for t in times], axis=0))
             sched = a.schedule()
             crit = float(rank_ms.max())
+            del bufs, a
+            torch.cuda.empty_cache()
+            # the same assignment as per-rank instruction lists (hsap_emit_forward), all ranks' streams on this GPU
+            prog = SapProgram(w.cu_seqlens, N, P, layout, w.heads_q, w.heads_kv, w.head_dim, w.block_m, w.block_n,
+                              balance=balanced)
+            prog.plan()
+            pbufs = prog.alloc()
+            prog.run(qs, ks, vs, pbufs)
+            prog_ms = float(np.median([prog.run(qs, ks, vs, pbufs, timed=True) for _ in range(reps)]))
+            n_ops = int(sum(len(x) for x in prog.ops))
+            n_stages = prog.num_stages
+            del pbufs, prog
+            torch.cuda.empty_cache()
             res["balanced" if balanced else "ring"] = {
                 "rank_tiles": sched["rank_tiles"], "tile_imbalance": round(sched["tile_imbalance"], 3),
                 "moved_blocks": sched["moved_blocks"], "rank_ms": [round(x, 4) for x in rank_ms.tolist()],
                 "critical_ms": round(crit, 4), "rank_ms_mean": round(float(rank_ms.mean()), 4),
                 "sequence_tflops_at_critical_path": round(flops / (crit * 1e-3) / 1e12, 1),
-                "kv_bytes_moved": sched["kv_bytes_moved"], "q_o_bytes_moved": sched["q_o_bytes_moved"]}
-            del bufs, a
-            torch.cuda.empty_cache()
+                "kv_bytes_moved": sched["kv_bytes_moved"], "q_o_bytes_moved": sched["q_o_bytes_moved"],
+                "program_stages": n_stages, "program_ops": n_ops, "program_one_gpu_ms": round(prog_ms, 4)}
         log("[bench] all shards %s %s: critical path ring %.3f ms, balanced %.3f ms" % (
             name, layout, res["ring"]["critical_ms"], res["balanced"]["critical_ms"]))
         out[layout] = res

@@ -1,0 +1,158 @@
+"""The per-rank instruction lists of one packed sequence's forward pass (hsap_emit_forward),
+executed on one GPU with one HIP stream standing in for each rank.
+
+Every rank gets the buffers the lists name: its own Q shard and K/V chunk (views of the
+sharded inputs), two receive slots for Q and for K/V, two result slots for partials it
+computes for other shards, and one part slot per chunk with tiles of its own shard.  A
+stage runs on every rank's stream after all ranks finished the previous stage (the batched
+point-to-point group of a stage); within it a rank's receives are device copies from the
+peer's buffer, its computation is hsap_partial_attn_fwd over that block's q-major runs, and
+its merge is hsap_lse_merge.  Sends need no action here: the receiving rank's copy reads
+the sender's buffer, which the stage order keeps unchanged until then.
+
+This sequences library calls and device copies only; all arithmetic runs in libhsap.
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+import torch
+
+from . import _lib as L
+
+
+class SapProgram:
+    """Emit and run the forward program of all P ranks (ring or balanced assignment)."""
+
+    def __init__(self, cu_seqlens, total_tokens: int, sp_degree: int, layout, heads_q: int, heads_kv: int,
+                 head_dim: int, block_m: int = 128, block_n: int = 128, softmax_scale: Optional[float] = None,
+                 balance: bool = False, device: str = "cuda"):
+        self.device = torch.device(device)
+        self.cu_host = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+        self.N, self.P = int(total_tokens), int(sp_degree)
+        self.n = self.N // self.P
+        self.layout = layout
+        self.hq, self.hkv, self.d = int(heads_q), int(heads_kv), int(head_dim)
+        self.bm, self.bn = int(block_m), int(block_n)
+        self.scale = float(softmax_scale) if softmax_scale is not None else 1.0 / math.sqrt(head_dim)
+        self.balance = bool(balance)
+        self.planned = False
+
+    def plan(self) -> None:
+        P, dev = self.P, self.device
+        base = L.shard_desc(self.N, P, self.layout, 0, self.bm, self.bn)
+        self.block_tiles, _ = L.load_matrix(self.cu_host, base)
+        if self.balance:
+            self.exec_rank = L.balance(self.block_tiles)[0]
+        else:
+            self.exec_rank = np.repeat(np.arange(P, dtype=np.int32)[:, None], P, axis=1)
+        self.ops, self.num_stages = L.emit_forward(self.block_tiles, self.exec_rank)
+        self.cu_dev = torch.from_numpy(self.cu_host).to(dev)
+        self.doc_start = torch.empty(self.N, dtype=torch.int32, device=dev)
+        L.doc_start(self.cu_dev, self.N, self.doc_start)
+        self.descs, self.tiles_dev, self.runs_host = [], [], []
+        for r in range(P):
+            shard = L.shard_desc(self.N, P, self.layout, r, self.bm, self.bn)
+            self.descs.append(L.attn_desc(shard, self.hq, self.hkv, self.d, self.scale))
+            tiles = L.plan(self.cu_host, shard)["tiles"]
+            sorted_tiles, runs, _ = L.plan_runs(shard, tiles, L.MAJOR_Q, 0)   # unsplit: slot = chunk
+            self.tiles_dev.append(torch.from_numpy(np.ascontiguousarray(sorted_tiles).reshape(-1)).to(dev))
+            self.runs_host.append(runs)
+        self._runs_dev: Dict[Tuple[int, int, int], torch.Tensor] = {}
+        self.parts = [int((self.block_tiles[r] > 0).sum()) for r in range(P)]
+        self.planned = True
+
+    def _runs(self, r: int, c: int, slot: int) -> torch.Tensor:
+        """Block (r, c)'s runs on the device, writing partial slot ``slot`` of the buffer they get."""
+        key = (r, c, slot)
+        if key not in self._runs_dev:
+            runs = self.runs_host[r]
+            sel = np.ascontiguousarray(runs[runs[:, 0] == c])
+            sel[:, 0] = slot
+            self._runs_dev[key] = torch.from_numpy(sel.reshape(-1)).to(self.device)
+        return self._runs_dev[key]
+
+    def alloc(self) -> Dict[str, list]:
+        P, n, dev = self.P, self.n, self.device
+        bf, f32 = torch.bfloat16, torch.float32
+        return {
+            "q_recv": [torch.empty(2, n, self.hq, self.d, dtype=bf, device=dev) for _ in range(P)],
+            # receive slots hold one chunk each, in the [P, n, Hkv, d] layout the kernel indexes by chunk
+            "k_recv": [torch.empty(2, P, n, self.hkv, self.d, dtype=bf, device=dev) for _ in range(P)],
+            "v_recv": [torch.empty(2, P, n, self.hkv, self.d, dtype=bf, device=dev) for _ in range(P)],
+            "o_res": [torch.empty(2, n, self.hq, self.d, dtype=f32, device=dev) for _ in range(P)],
+            "lse_res": [torch.empty(2, self.hq, n, dtype=f32, device=dev) for _ in range(P)],
+            "o_part": [torch.empty(max(p, 1), n, self.hq, self.d, dtype=f32, device=dev) for p in self.parts],
+            "lse_part": [torch.empty(max(p, 1), self.hq, n, dtype=f32, device=dev) for p in self.parts],
+            "o": torch.empty(P, n, self.hq, self.d, dtype=bf, device=dev),
+            "lse": torch.empty(P, self.hq, n, dtype=f32, device=dev),
+        }
+
+    def run(self, q, k, v, bufs: Dict[str, list], timed: bool = False) -> Optional[float]:
+        """q [P, n, Hq, d], k / v [P, n, Hkv, d] (every rank's own data, sharded order) ->
+        bufs["o"] [P, n, Hq, d], bufs["lse"] [P, Hq, n].  Returns the milliseconds of the whole
+        program when ``timed``."""
+        if not self.planned:
+            raise RuntimeError("call plan() first")
+        P = self.P
+        main = torch.cuda.current_stream()
+        streams = [torch.cuda.Stream(device=self.device) for _ in range(P)]
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(main)
+        done = [start] * P      # the event each rank's stream must pass before the next stage
+        by_stage = [[[] for _ in range(self.num_stages)] for _ in range(P)]
+        for e in range(P):
+            for o in self.ops[e]:
+                by_stage[e][int(o[3])].append([int(x) for x in o])
+        for t in range(self.num_stages):
+            stage_done = []
+            for e in range(P):
+                s = streams[e]
+                for ev in set(done):
+                    s.wait_event(ev)
+                with torch.cuda.stream(s):
+                    for op, tensor, peer, _, shard, chunk, in_slot, out_slot in by_stage[e][t]:
+                        if op == L.OP_RECV:
+                            if tensor == L.T_Q:
+                                bufs["q_recv"][e][out_slot].copy_(q[peer])
+                            elif tensor == L.T_KV:
+                                bufs["k_recv"][e][out_slot][peer].copy_(k[peer])
+                                bufs["v_recv"][e][out_slot][peer].copy_(v[peer])
+                            else:
+                                src = self._send_slot(peer, e, t, shard, chunk)
+                                bufs["o_part"][e][out_slot].copy_(bufs["o_res"][peer][src])
+                                bufs["lse_part"][e][out_slot].copy_(bufs["lse_res"][peer][src])
+                        elif op == L.OP_COMPUTE:
+                            qq = q[e] if shard == e else bufs["q_recv"][e][in_slot]
+                            kk, vv = (k, v) if chunk == e else (bufs["k_recv"][e][in_slot], bufs["v_recv"][e][in_slot])
+                            if shard == e:
+                                ob, lb = bufs["o_part"][e], bufs["lse_part"][e]
+                            else:
+                                ob, lb = bufs["o_res"][e], bufs["lse_res"][e]
+                            L.partial_attn_fwd(self.descs[shard], qq, kk, vv, self.doc_start, self.tiles_dev[shard],
+                                               self._runs(shard, chunk, out_slot), ob, lb, stream=s)
+                        elif op == L.OP_MERGE:
+                            parts = out_slot
+                            L.lse_merge([bufs["o_part"][e][i] for i in range(parts)],
+                                        [bufs["lse_part"][e][i] for i in range(parts)], self.n, self.hq, self.d,
+                                        bufs["o"][e], bufs["lse"][e], stream=s)
+                ev = torch.cuda.Event()
+                ev.record(s)
+                stage_done.append(ev)
+            done = stage_done
+        for ev in done:
+            main.wait_event(ev)
+        end.record(main)
+        if not timed:
+            return None
+        end.synchronize()
+        return start.elapsed_time(end)
+
+    def _send_slot(self, sender: int, receiver: int, stage: int, shard: int, chunk: int) -> int:
+        for o in self.ops[sender]:
+            if (int(o[0]) == L.OP_SEND and int(o[1]) == L.T_O and int(o[2]) == receiver and int(o[3]) == stage
+                    and int(o[4]) == shard and int(o[5]) == chunk):
+                return int(o[6])
+        raise RuntimeError("no matching send for a receive of o")
