@@ -43,7 +43,7 @@ def log(*a):
 def _critical_shard(L, w):
     best, best_r = -1, 0
     for r in range(w.sp_degree):
-        d = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, r, w.block_m, w.block_n)
+        d = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, r, w.block_m, w.block_n, batch=w.batch)
         pairs = int(L.plan(w.cu_seqlens, d)["useful_pairs"].sum())
         if pairs > best:
             best, best_r = pairs, r
@@ -51,12 +51,14 @@ def _critical_shard(L, w):
 
 
 def _positions(N: int, P: int, layout: int, x: int, local: np.ndarray) -> np.ndarray:
-    """Global positions of local rows of shard (or chunk) x."""
+    """Global positions of local rows of shard (or chunk) x; row b*n + l is row l of sequence b of
+    N tokens (a batch of concatenated sequences)."""
     n = N // P
+    b, local = local // n, local % n
     if layout == 0:
-        return x * n + local
+        return b * N + x * n + local
     m = n // 2
-    return np.where(local < m, x * m + local, (2 * P - 1 - x) * m + (local - m))
+    return b * N + np.where(local < m, x * m + local, (2 * P - 1 - x) * m + (local - m))
 
 
 def _finite_partial_rows(L, cu, sd, split: int) -> int:
@@ -93,7 +95,7 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     log("[bench] %s: generating inputs (shard %d)" % (w.name, shard))
     t = w.tensors(backward=bwd)
     dev = torch.device("cuda")
-    sd = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, shard, w.block_m, w.block_n)
+    sd = L.shard_desc(w.total_tokens, w.sp_degree, w.layout, shard, w.block_m, w.block_n, batch=w.batch)
     desc = L.attn_desc(sd, w.heads_q, w.heads_kv, w.head_dim, 1.0 / math.sqrt(w.head_dim))
     ex = L.Executor(desc, backward=bwd, fused=True)
     q = to_sharded(sd, t["q"].to(dev))[shard].contiguous()
@@ -101,7 +103,7 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     v = to_sharded(sd, t["v"].to(dev))
     d_o = to_sharded(sd, t["do"].to(dev))[shard].contiguous() if bwd else None
     del t
-    n = w.total_tokens // w.sp_degree
+    n = sd.rows
     o = torch.empty(n, w.heads_q, w.head_dim, dtype=torch.bfloat16, device=dev)
     lse = torch.empty(w.heads_q, n, dtype=torch.float32, device=dev)
     if bwd:
@@ -177,7 +179,7 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     bwd_flops = 10.0 * w.head_dim * w.heads_q * pairs if bwd else 0.0
     ms_step = wall / steps * 1e3
     res = {
-        "workload": w.name, "shard": shard, "tokens": w.total_tokens, "sp_degree": w.sp_degree,
+        "workload": w.name, "shard": shard, "tokens": w.total_tokens, "batch": w.batch, "sp_degree": w.sp_degree,
         "layout": w.layout, "heads_q": w.heads_q, "heads_kv": w.heads_kv, "head_dim": w.head_dim,
         "block_m": w.block_m, "block_n": w.block_n, "backward": bool(bwd), "docs": w.num_docs,
         "useful_pairs": pairs, "tiles": tiles, "full_tiles": info["num_full_tiles"],
@@ -381,7 +383,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c2")
-    ap.add_argument("--extra", default="c3,c4,c5", help="other workloads reported under 'extra' ('' for none)")
+    ap.add_argument("--extra", default="c3,c4,c5,c6", help="other workloads reported under 'extra' ('' for none)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle budget for the CPU baseline (0: skip)")
     ap.add_argument("--no-all-shards", action="store_true",
                     help="skip the all-shard load analysis of the main workload (e.g. under a kernel trace)")

@@ -94,13 +94,22 @@ typedef struct {
 } hsap_run;
 
 typedef struct {
-  int64_t total_tokens;  /* N                                               */
+  int64_t total_tokens;  /* N: tokens of one packed sequence                */
   int32_t sp_degree;     /* P >= 1                                          */
   int32_t layout;        /* hsap_layout                                     */
   int32_t shard_id;      /* r in [0, P)                                     */
   int32_t block_m;       /* BM: query rows per tile                         */
   int32_t block_n;       /* BN: key rows per tile                           */
+  int32_t batch;         /* B >= 1 packed sequences per call (0 reads as 1) */
 } hsap_shard_desc;
+
+/* Batches.  B packed sequences of N tokens are concatenated: sequence b holds
+ * positions b*N .. b*N+N-1, and cu_seqlens covers all B*N positions with a
+ * document boundary at every b*N.  Each sequence is split P ways by the
+ * layout; shard (or chunk) x holds n = N/P positions of every sequence, and
+ * its local rows are b*n + l (row l of sequence b).  Every per-shard array
+ * below therefore has B*n rows, doc_start has B*N entries, and no tile pairs
+ * rows of two sequences.  With B = 1 this is the single packed sequence. */
 
 typedef struct {
   hsap_shard_desc shard;
@@ -283,7 +292,8 @@ hsap_status hsap_emit_forward(int32_t sp_degree, const int64_t* block_tiles, con
                               int64_t capacity, int64_t* rank_offsets, int32_t* num_stages);
 
 /*
- * hsap_doc_start -- device int32 [N]: start(t) for every position t.
+ * hsap_doc_start -- device int32 [total_tokens]: start(t) for every position
+ * t (total_tokens = B*N for a batch).
  *   cu_seqlens  device int32 [num_docs + 1] (same rules as hsap_plan; the
  *               device copy is not re-validated).
  */
@@ -293,9 +303,10 @@ hsap_status hsap_doc_start(const int32_t* cu_seqlens, int32_t num_docs, int64_t 
 /*
  * hsap_shard_gather -- place a global-order tensor into sharded order (the
  * in-memory stand-in for scattering a sequence over P ranks).
- *   src  device [N rows] in global token order; dst device [P, n rows].
+ *   src  device [B*N rows] in global token order; dst device [P, B*n rows].
  *   row_bytes  bytes per token row, a multiple of 16; src and dst 16-byte
- *              aligned.  Uses shard->total_tokens, sp_degree and layout only.
+ *              aligned.  Uses shard->total_tokens, sp_degree, layout and
+ *              batch only.
  */
 hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, void* dst,
                               int64_t row_bytes, void* hip_stream);

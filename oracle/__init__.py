@@ -32,6 +32,8 @@ What it computes, with the passages it follows (HSAP paper, arxiv 2606.30460):
 * ``balance`` -- the per-(shard, chunk) block sizes of every shard and the
   Q-transfer rebalance of the blocks over ranks (compile step 2, and the
   balancing of InterSP groups by transferring Q blocks).
+* ``batch`` -- batches of packed sequences (each sharded the same way, never
+  attending across sequences), computed one sequence at a time.
 * ``schedule`` -- the per-rank instruction lists of the forward pass (the
   jitted code generation of the SAP section, with the paper's instruction
   set), arranged in stages with matched sends and receives.
@@ -58,3 +60,4 @@ from .plan import (  # noqa: F401
 )
 from .balance import load_matrix, q_transfer_balance  # noqa: F401
 from .schedule import forward_program  # noqa: F401
+from .batch import batch_plan_shard, batch_shard_backward, batch_shard_forward, split_batch  # noqa: F401

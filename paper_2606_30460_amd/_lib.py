@@ -54,7 +54,22 @@ class HsapError(RuntimeError):
 
 class ShardDesc(ctypes.Structure):
     _fields_ = [("total_tokens", ctypes.c_int64), ("sp_degree", ctypes.c_int32), ("layout", ctypes.c_int32),
-                ("shard_id", ctypes.c_int32), ("block_m", ctypes.c_int32), ("block_n", ctypes.c_int32)]
+                ("shard_id", ctypes.c_int32), ("block_m", ctypes.c_int32), ("block_n", ctypes.c_int32),
+                ("batch", ctypes.c_int32)]
+
+    @property
+    def sequences(self) -> int:
+        return max(int(self.batch), 1)
+
+    @property
+    def rows(self) -> int:
+        """Local rows of one shard over the batch (B * N / P)."""
+        return self.sequences * (self.total_tokens // self.sp_degree)
+
+    @property
+    def positions(self) -> int:
+        """Positions over the batch (B * N)."""
+        return self.sequences * self.total_tokens
 
 
 class AttnDesc(ctypes.Structure):
@@ -144,8 +159,12 @@ def layout_code(layout) -> int:
     return int(layout)
 
 
-def shard_desc(total_tokens: int, sp_degree: int, layout, shard_id: int, block_m: int, block_n: int) -> ShardDesc:
-    return ShardDesc(int(total_tokens), int(sp_degree), layout_code(layout), int(shard_id), int(block_m), int(block_n))
+def shard_desc(total_tokens: int, sp_degree: int, layout, shard_id: int, block_m: int, block_n: int,
+               batch: int = 1) -> ShardDesc:
+    """Shard descriptor; ``total_tokens`` is one packed sequence's length, ``batch`` the number of
+    such sequences per call (concatenated)."""
+    return ShardDesc(int(total_tokens), int(sp_degree), layout_code(layout), int(shard_id), int(block_m), int(block_n),
+                     int(batch))
 
 
 def attn_desc(shard: ShardDesc, heads_q: int, heads_kv: int, head_dim: int, softmax_scale: float) -> AttnDesc:
@@ -311,8 +330,8 @@ def shard_gather(shard: ShardDesc, src, dst, stream=None) -> None:
     import torch
     if src.shape != dst.shape or src.dtype != dst.dtype or not (src.is_cuda and dst.is_cuda):
         raise ValueError("src and dst must be device tensors of one shape and dtype")
-    if not (src.is_contiguous() and dst.is_contiguous()) or src.shape[0] != shard.total_tokens:
-        raise ValueError("src and dst must be contiguous with total_tokens rows")
+    if not (src.is_contiguous() and dst.is_contiguous()) or src.shape[0] != shard.positions:
+        raise ValueError("src and dst must be contiguous with total_tokens x batch rows")
     row_bytes = src[0].numel() * src.element_size() if src.shape[0] else 0
     del torch
     _check(lib().hsap_shard_gather(ctypes.byref(shard), _ptr(src), _ptr(dst), int(row_bytes), _stream(stream)))
@@ -321,12 +340,12 @@ def shard_gather(shard: ShardDesc, src, dst, stream=None) -> None:
 def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev, o_part, lse_part,
                      stream=None) -> None:
     s = desc.shard
-    n = s.total_tokens // s.sp_degree
+    n = s.rows
     hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
     _dev(q, "bfloat16", "q", n * hq * d)
     _dev(k, "bfloat16", "k", P * n * hkv * d)
     _dev(v, "bfloat16", "v", P * n * hkv * d)
-    _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
+    _dev(doc_start_dev, "int32", "doc_start", s.positions)
     _dev(tiles_dev, "int32", "tiles")
     _dev(runs_dev, "int32", "runs")
     _dev(o_part, "float32", "o_part")
@@ -342,12 +361,12 @@ def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev
 def attn_fwd_fused(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev, o_out, lse_out, stream=None) -> None:
     """hsap_attn_fwd_fused over MAJOR_Q_ALL runs: final bf16 O and LSE in one pass."""
     s = desc.shard
-    n = s.total_tokens // s.sp_degree
+    n = s.rows
     hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
     _dev(q, "bfloat16", "q", n * hq * d)
     _dev(k, "bfloat16", "k", P * n * hkv * d)
     _dev(v, "bfloat16", "v", P * n * hkv * d)
-    _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
+    _dev(doc_start_dev, "int32", "doc_start", s.positions)
     _dev(tiles_dev, "int32", "tiles")
     _dev(runs_dev, "int32", "runs")
     _dev(o_out, "bfloat16", "o_out", n * hq * d)
@@ -385,7 +404,7 @@ def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, ti
                      runs_q_dev, dq_acc, dk_acc, dv_acc, stream=None) -> None:
     """hsap_partial_attn_bwd.  Either run list may be None to skip its kernel."""
     s = desc.shard
-    n = s.total_tokens // s.sp_degree
+    n = s.rows
     hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
     _dev(q, "bfloat16", "q", n * hq * d)
     _dev(k, "bfloat16", "k", P * n * hkv * d)
@@ -393,7 +412,7 @@ def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, ti
     _dev(d_o, "bfloat16", "d_o", n * hq * d)
     _dev(lse, "float32", "lse", hq * n)
     _dev(delta, "float32", "delta", hq * n)
-    _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
+    _dev(doc_start_dev, "int32", "doc_start", s.positions)
     for t, name in ((tiles_k_dev, "tiles_k"), (runs_k_dev, "runs_k"), (tiles_q_dev, "tiles_q"), (runs_q_dev, "runs_q")):
         if t is not None:
             _dev(t, "int32", name)
@@ -412,7 +431,7 @@ def attn_bwd_bf16(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles
                   runs_all_dev, dq, dk, dv, stream=None) -> None:
     """hsap_attn_bwd_bf16: final bf16 gradients over every chunk (MAJOR_K and MAJOR_Q_ALL lists)."""
     s = desc.shard
-    n = s.total_tokens // s.sp_degree
+    n = s.rows
     hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
     _dev(q, "bfloat16", "q", n * hq * d)
     _dev(k, "bfloat16", "k", P * n * hkv * d)
@@ -420,7 +439,7 @@ def attn_bwd_bf16(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles
     _dev(d_o, "bfloat16", "d_o", n * hq * d)
     _dev(lse, "float32", "lse", hq * n)
     _dev(delta, "float32", "delta", hq * n)
-    _dev(doc_start_dev, "int32", "doc_start", s.total_tokens)
+    _dev(doc_start_dev, "int32", "doc_start", s.positions)
     for t, name in ((tiles_k_dev, "tiles_k"), (runs_k_dev, "runs_k"), (tiles_all_dev, "tiles_all"),
                     (runs_all_dev, "runs_all")):
         _dev(t, "int32", name)
@@ -455,7 +474,7 @@ class Executor:
     def __init__(self, desc: AttnDesc, backward: bool = False, fused: bool = False, max_run_tiles: int = -1):
         self.desc = desc
         s = desc.shard
-        self.n = s.total_tokens // s.sp_degree
+        self.n = s.rows
         self.P = s.sp_degree
         self._q_numel = self.n * desc.heads_q * desc.head_dim
         self._kv_numel = self.P * self.n * desc.heads_kv * desc.head_dim

@@ -31,22 +31,33 @@ void clear_error();
 // ---------------------------------------------------------------------------
 // shard geometry
 //
-// Shard (or chunk) x of a sequence of N tokens split P ways holds n = N/P
-// positions.  CONTIGUOUS: x*n + l.  ZIGZAG: the sequence is cut into 2P
-// pieces of m = N/(2P); local rows 0..m-1 are piece x, rows m..2m-1 are
+// A batch of B packed sequences of Ns tokens each, concatenated (sequence b
+// holds positions b*Ns .. b*Ns+Ns-1), every sequence split P ways.  Shard
+// (or chunk) x holds ns = Ns/P positions of each sequence; its local rows are
+// b*ns + l.  CONTIGUOUS: position b*Ns + x*ns + l.  ZIGZAG: each sequence is
+// cut into 2P pieces of m = Ns/(2P); rows l < m are piece x, rows m..2m-1 are
 // piece 2P-1-x.
 // ---------------------------------------------------------------------------
 struct Geom {
-  int64_t N;
-  int64_t n;  // rows per shard
-  int64_t m;  // rows per piece (n for CONTIGUOUS, n/2 for ZIGZAG)
+  int64_t N;   // positions over the batch (B * Ns)
+  int64_t n;   // rows per shard over the batch (B * ns)
+  int64_t m;   // rows per piece of one sequence (ns for CONTIGUOUS, ns/2 for ZIGZAG)
+  int64_t Ns;  // tokens per sequence
+  int64_t ns;  // rows per shard of one sequence
   int32_t P;
   int32_t layout;
+  int32_t B;
 };
 
 HSAP_HD inline int64_t global_pos(const Geom& g, int32_t shard, int64_t local) {
-  if (g.layout == HSAP_LAYOUT_CONTIGUOUS) return (int64_t)shard * g.n + local;
-  return local < g.m ? (int64_t)shard * g.m + local : (int64_t)(2 * g.P - 1 - shard) * g.m + (local - g.m);
+  int64_t base = 0;
+  if (g.B > 1) {  // rows and positions stay below 2^31 (checked with the descriptor)
+    const uint32_t b = (uint32_t)local / (uint32_t)g.ns;
+    base = (int64_t)b * g.Ns;
+    local -= (int64_t)b * g.ns;
+  }
+  if (g.layout == HSAP_LAYOUT_CONTIGUOUS) return base + (int64_t)shard * g.ns + local;
+  return base + (local < g.m ? (int64_t)shard * g.m + local : (int64_t)(2 * g.P - 1 - shard) * g.m + (local - g.m));
 }
 
 // Validates N, P, layout, shard id and tile sizes; fills `g`.

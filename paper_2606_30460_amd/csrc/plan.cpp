@@ -41,8 +41,10 @@ void clear_error() { g_last_error.clear(); }
 
 hsap_status check_shard(const hsap_shard_desc* d, Geom* g) {
   if (!d) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "shard descriptor is NULL");
-  if (d->total_tokens <= 0 || d->total_tokens > INT32_MAX)
-    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "total_tokens %lld outside 1..2^31-1", (long long)d->total_tokens);
+  const int32_t B = d->batch <= 0 ? 1 : d->batch;
+  if (d->batch < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "batch %d < 0", d->batch);
+  if (d->total_tokens <= 0 || d->total_tokens * B > INT32_MAX)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "total_tokens %lld x batch %d outside 1..2^31-1", (long long)d->total_tokens, B);
   if (d->sp_degree < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "sp_degree %d < 1", d->sp_degree);
   if (d->shard_id < 0 || d->shard_id >= d->sp_degree)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "shard_id %d outside 0..%d", d->shard_id, d->sp_degree - 1);
@@ -58,11 +60,14 @@ hsap_status check_shard(const hsap_shard_desc* d, Geom* g) {
   if (piece % d->block_m || piece % d->block_n)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "BM=%d and BN=%d must divide the %s length %lld", d->block_m, d->block_n,
               d->layout == HSAP_LAYOUT_ZIGZAG ? "zigzag piece" : "shard", (long long)piece);
-  g->N = N;
-  g->n = N / P;
+  g->Ns = N;
+  g->ns = N / P;
+  g->N = N * B;
+  g->n = (N / P) * B;
   g->m = piece;
   g->P = (int32_t)P;
   g->layout = d->layout;
+  g->B = B;
   return HSAP_OK;
 }
 
@@ -82,19 +87,25 @@ hsap_status check_attn(const hsap_attn_desc* d, Geom* g) {
 
 namespace {
 
-// Positions of shard x's local rows, as (global start, local start, length) pieces.
+// Positions of shard x's local rows, as (global start, local start, length) pieces, one or two
+// per sequence of the batch; piece i belongs to sequence i / (pieces per sequence).
 struct Piece {
   int64_t global0, local0, len;
 };
 
-int shard_pieces(const Geom& g, int32_t x, Piece out[2]) {
-  if (g.layout == HSAP_LAYOUT_CONTIGUOUS) {
-    out[0] = {(int64_t)x * g.n, 0, g.n};
-    return 1;
+int pieces_per_sequence(const Geom& g) { return g.layout == HSAP_LAYOUT_CONTIGUOUS ? 1 : 2; }
+
+void shard_pieces(const Geom& g, int32_t x, std::vector<Piece>& out) {
+  out.clear();
+  for (int32_t b = 0; b < g.B; ++b) {
+    const int64_t gb = (int64_t)b * g.Ns, lb = (int64_t)b * g.ns;
+    if (g.layout == HSAP_LAYOUT_CONTIGUOUS) {
+      out.push_back({gb + (int64_t)x * g.ns, lb, g.ns});
+    } else {
+      out.push_back({gb + (int64_t)x * g.m, lb, g.m});
+      out.push_back({gb + (int64_t)(2 * g.P - 1 - x) * g.m, lb + g.m, g.m});
+    }
   }
-  out[0] = {(int64_t)x * g.m, 0, g.m};
-  out[1] = {(int64_t)(2 * g.P - 1 - x) * g.m, g.m, g.m};
-  return 2;
 }
 
 // Index of the document holding position t (the last k with cu[k] <= t).
@@ -133,8 +144,13 @@ hsap_status check_cu(const int32_t* cu, int32_t num_docs, const Geom& g) {
   for (int32_t i = 0; i < num_docs; ++i)
     if (cu[i + 1] < cu[i]) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens decreases at %d", i + 1);
   if ((int64_t)cu[num_docs] != g.N)
-    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens[%d] = %d, expected total_tokens %lld", num_docs, cu[num_docs],
-              (long long)g.N);
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "cu_seqlens[%d] = %d, expected total_tokens x batch = %lld", num_docs,
+              cu[num_docs], (long long)g.N);
+  // documents stay inside their sequence: every sequence start is a document boundary
+  for (int32_t b = 1; b < g.B; ++b)
+    if (!std::binary_search(cu, cu + num_docs + 1, (int32_t)(b * g.Ns)))
+      HSAP_FAIL(HSAP_ERR_INVALID_ARG, "sequence %d starts at %lld, which is not a document boundary", b,
+                (long long)(b * g.Ns));
   return HSAP_OK;
 }
 
@@ -145,23 +161,25 @@ int64_t plan_shard(const int32_t* cu, int32_t num_docs, const Geom& g, const hsa
   const int32_t P = g.P, r = shard.shard_id;
   const int64_t BM = shard.block_m, BN = shard.block_n;
   const int64_t full = BM * BN;
-  Piece qp[2], kp[2];
-  const int nq_pieces = shard_pieces(g, r, qp);
+  std::vector<Piece> qp, kp;
+  shard_pieces(g, r, qp);
+  const int pps = pieces_per_sequence(g);
   const bool store = tiles != nullptr;
   int64_t count = 0;
   if (step_offsets) step_offsets[0] = 0;
   for (int32_t step = 0; step < P; ++step) {
     const int32_t c = ((r - step) % P + P) % P;
-    const int nk_pieces = shard_pieces(g, c, kp);
+    shard_pieces(g, c, kp);
     int64_t step_pairs = 0;
-    for (int qi = 0; qi < nq_pieces; ++qi) {
+    for (int qi = 0; qi < (int)qp.size(); ++qi) {
       for (int64_t l0 = 0; l0 < qp[qi].len; l0 += BM) {
         const int64_t qa = qp[qi].global0 + l0, qb = qa + BM - 1;
         const int64_t q_tile = (qp[qi].local0 + l0) / BM;
         const int64_t dq = doc_of(cu, num_docs, qa);
         const int64_t s_first = cu[dq];
         const int64_t s_last = cu[doc_of(cu, num_docs, qb)];
-        for (int ki = 0; ki < nk_pieces; ++ki) {
+        const int seq = qi / pps;  // keys of other sequences are never allowed
+        for (int ki = seq * pps; ki < (seq + 1) * pps; ++ki) {
           const int64_t pa = kp[ki].global0, pb = pa + kp[ki].len - 1;
           const int64_t x = std::max(s_first, pa), y = std::min(qb, pb);
           if (x > y) continue;
@@ -432,7 +450,7 @@ int32_t hsap_split_length(const hsap_shard_desc* shard, int64_t num_tiles, int32
     set_error("bad num_tiles, heads_q or resident_workgroups");
     return -1;
   }
-  const int64_t nk = g.n / shard->block_n;
+  const int64_t nk = g.ns / shard->block_n;  // a run never leaves its sequence
   const int64_t avg = (num_tiles * heads_q + resident_workgroups - 1) / resident_workgroups;
   if (nk <= avg) return 0;  // no run can exceed the average load
   const int64_t len = std::max<int64_t>({avg, 4, (nk + 3) / 4});

@@ -562,3 +562,66 @@ def test_q_transfer_balance_against_every_assignment(seed):
     assert best <= int(load.max()) <= int(cost.sum(axis=1).max())   # never worse than the ring
     if movable <= 1:   # one decision: the search finds the better side
         assert int(load.max()) == best
+
+
+# ---------------------------------------------------------------------------
+# Batches of packed sequences
+# ---------------------------------------------------------------------------
+
+def test_batch_of_one_is_the_single_sequence():
+    rng = np.random.default_rng(77)
+    P, N, H, d = 4, 64, 2, 4
+    cu = _rand_cu(rng, N)
+    q, k, v, do = (_rand(rng, N, H, d) for _ in range(4))
+    for layout in ("contiguous", "zigzag"):
+        for r in range(P):
+            one = oracle.shard_forward(q, k, v, cu, N, P, layout, r)
+            bat = oracle.batch_shard_forward(q, k, v, cu, N, 1, P, layout, r)
+            assert np.array_equal(bat["o"], one["o"]) and np.array_equal(bat["lse"], one["lse"])
+            p1, pb = plan_shard(cu, N, P, layout, r, 8, 4), oracle.batch_plan_shard(cu, N, 1, P, layout, r, 8, 4)
+            assert np.array_equal(p1["tiles"], pb["tiles"]) and np.array_equal(p1["step_offsets"], pb["step_offsets"])
+        g1 = oracle.shard_backward(q, k, v, do, cu, N, P, layout, 1)
+        gb = oracle.batch_shard_backward(q, k, v, do, cu, N, 1, P, layout, 1)
+        assert all(np.array_equal(g1[x], gb[x]) for x in ("dq", "dk", "dv"))
+
+
+def test_batch_of_copies_gives_copies():
+    rng = np.random.default_rng(78)
+    P, N, H, d = 2, 32, 2, 4
+    cu = _rand_cu(rng, N)
+    q, k, v = (_rand(rng, N, H, d) for _ in range(3))
+    cu2 = np.concatenate([cu, cu[1:] + N])
+    q2, k2, v2 = (np.concatenate([x, x]) for x in (q, k, v))
+    n = N // P
+    for layout in ("contiguous", "zigzag"):
+        for r in range(P):
+            res = oracle.batch_shard_forward(q2, k2, v2, cu2, N, 2, P, layout, r)
+            assert np.array_equal(res["o"][:n], res["o"][n:]) and np.array_equal(res["lse"][:, :n], res["lse"][:, n:])
+
+
+@pytest.mark.parametrize("layout", ["contiguous", "zigzag"])
+def test_batch_tiles_bruteforce(layout):
+    # the batch's tiles classify the concatenated sequence's allowed pairs over the batched row maps
+    rng = np.random.default_rng(79)
+    P, N, B, bm, bn = 2, 64, 3, 8, 4
+    cus = [_rand_cu(rng, N) for _ in range(B)]
+    cu = np.concatenate([cus[0]] + [c[1:] + b * N for b, c in enumerate(cus) if b > 0])
+    n = N // P
+
+    def rows(x):      # global positions of local rows b*n + l of shard x
+        return np.concatenate([oracle.shard_positions(N, P, layout, x) + b * N for b in range(B)])
+
+    for r in range(P):
+        plan = oracle.batch_plan_shard(cu, N, B, P, layout, r, bm, bn)
+        got = {(int(t[0]), int(t[1]), int(t[2])): int(t[3]) for t in plan["tiles"]}
+        expect = {}
+        qp = rows(r)
+        for c in range(P):
+            kp = rows(c)
+            mask = oracle.allowed_mask_dense(cu, qp, kp)
+            for t in range(B * n // bm):
+                for u in range(B * n // bn):
+                    cnt = int(mask[t * bm:(t + 1) * bm, u * bn:(u + 1) * bn].sum())
+                    if cnt:
+                        expect[(c, t, u)] = KIND_FULL if cnt == bm * bn else KIND_MASKED
+        assert got == expect

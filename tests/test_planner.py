@@ -211,3 +211,45 @@ def test_balance_of_workload_loads(layout):
     ref_exec, ref_load = oracle.q_transfer_balance(tiles)
     assert np.array_equal(exec_rank, ref_exec) and np.array_equal(load, ref_load)
     assert int(load.sum()) == int(tiles.sum())
+
+
+# ---------------------------------------------------------------------------
+# batches of packed sequences
+# ---------------------------------------------------------------------------
+
+def _batch_cu(rng, N, B):
+    cus = [_rand_cu(rng, N) for _ in range(B)]
+    return np.concatenate([cus[0]] + [c[1:] + b * N for b, c in enumerate(cus) if b > 0]).astype(np.int32)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_batch_plan_against_oracle(seed):
+    rng = np.random.default_rng(4000 + seed)
+    P = int(rng.choice([1, 2, 4, 8]))
+    B = int(rng.integers(1, 5))
+    layout = str(rng.choice(["contiguous", "zigzag"]))
+    bm, bn = int(rng.choice([16, 32, 64])), int(rng.choice([16, 32, 64]))
+    split = 2 * P if layout == "zigzag" else P
+    N = split * max(bm, bn) * int(rng.integers(1, 3))
+    cu = _batch_cu(rng, N, B)
+    r = int(rng.integers(0, P))
+    got = L.plan(cu, L.shard_desc(N, P, layout, r, bm, bn, batch=B))
+    ref = oracle.batch_plan_shard(cu, N, B, P, layout, r, bm, bn)
+    assert np.array_equal(got["tiles"], ref["tiles"])
+    assert np.array_equal(got["step_offsets"], ref["step_offsets"])
+    assert np.array_equal(got["useful_pairs"], ref["useful_pairs"])
+    tiles, pairs = L.load_matrix(cu, L.shard_desc(N, P, layout, 0, bm, bn, batch=B))
+    lengths = np.diff(cu).astype(np.int64)
+    assert int(pairs.sum()) == int(np.sum(lengths * (lengths + 1) // 2))
+
+
+def test_batch_rejects_documents_across_sequences():
+    N, P = 256, 2
+    s = L.shard_desc(N, P, "contiguous", 0, 32, 32, batch=2)
+    with pytest.raises(L.HsapError):
+        L.plan(np.array([0, 100, 300, 512], dtype=np.int32), s)     # a document over 256
+    with pytest.raises(L.HsapError):
+        L.plan(np.array([0, 256], dtype=np.int32), s)                # covers one sequence only
+    L.plan(np.array([0, 100, 256, 300, 512], dtype=np.int32), s)
+    with pytest.raises(L.HsapError):                                 # B * N beyond 2^31 - 1
+        L.plan(np.array([0, 1 << 30], dtype=np.int32), L.shard_desc(1 << 30, 1, "contiguous", 0, 64, 64, batch=2))

@@ -15,10 +15,11 @@ def test_uniform_partition_seed0():
 @pytest.mark.parametrize("name", list(CONFIGS))
 def test_workloads_cover_total(name):
     w = make_workload(name)
-    assert sum(w.lengths) == w.total_tokens
+    assert sum(w.lengths) == w.total_tokens * w.batch
     assert all(x > 0 for x in w.lengths)
     cu = w.cu_seqlens
-    assert cu.dtype == np.int32 and cu[0] == 0 and cu[-1] == w.total_tokens
+    assert cu.dtype == np.int32 and cu[0] == 0 and cu[-1] == w.total_tokens * w.batch
+    assert all(b * w.total_tokens in cu for b in range(w.batch))   # every sequence starts a document
     assert w.total_tokens % (w.sp_degree * (2 if w.layout == "zigzag" else 1)) == 0
     n = w.total_tokens // w.sp_degree
     assert n % w.block_m == 0 and n % w.block_n == 0

@@ -153,6 +153,10 @@ class Workload:
     useful (unmasked) query-key pairs" -- the slowest rank, which sets the step
     time of a sequence-parallel group.  Picking it needs the mask, so the
     caller resolves it with its own planner.
+
+    ``batch`` packed sequences of ``total_tokens`` tokens each are concatenated
+    (``lengths`` lists every sequence's documents in turn, each sequence's
+    summing to ``total_tokens``); tensors then have batch * total_tokens rows.
     """
     name: str
     total_tokens: int
@@ -167,6 +171,7 @@ class Workload:
     block_n: int
     backward: bool
     seed: int = 0
+    batch: int = 1
 
     @property
     def cu_seqlens(self) -> np.ndarray:
@@ -177,9 +182,9 @@ class Workload:
         return len(self.lengths)
 
     def tensors(self, backward: Optional[bool] = None) -> Dict[str, torch.Tensor]:
-        """Q [N, Hq, d], K and V [N, Hkv, d] (and dO [N, Hq, d]) in global token order."""
+        """Q [B*N, Hq, d], K and V [B*N, Hkv, d] (and dO [B*N, Hq, d]) in global token order."""
         bwd = self.backward if backward is None else backward
-        N, hq, hkv, d = self.total_tokens, self.heads_q, self.heads_kv, self.head_dim
+        N, hq, hkv, d = self.total_tokens * self.batch, self.heads_q, self.heads_kv, self.head_dim
         out = {
             "q": random_bf16((N, hq, d), self.seed + 1),
             "k": random_bf16((N, hkv, d), self.seed + 2),
@@ -226,8 +231,17 @@ def _c5m(seed: int) -> Workload:
                     8, "contiguous", 0, 128, 128, True, seed)
 
 
+def _c6(seed: int) -> Workload:
+    # four packed sequences of the log-normal mix (each with its own documents) in one call
+    lengths: List[int] = []
+    for b in range(4):
+        lengths += doc_lengths_lognormal(32768, 2048.0, 1.0, 128, 16384, seed + 1000 * b)
+    return Workload("c6_4x32k_lognormal_h32_d128_sp8_shard3", 32768, lengths, 32, 32, 128,
+                    8, "contiguous", 3, 128, 128, False, seed, batch=4)
+
+
 CONFIGS: Dict[str, Callable[[int], Workload]] = {
-    "c1": _c1, "c2": _c2, "c3": _c3, "c4": _c4, "c5": _c5, "c5m": _c5m,
+    "c1": _c1, "c2": _c2, "c3": _c3, "c4": _c4, "c5": _c5, "c5m": _c5m, "c6": _c6,
 }
 
 
