@@ -625,3 +625,50 @@ def test_batch_tiles_bruteforce(layout):
                     if cnt:
                         expect[(c, t, u)] = KIND_FULL if cnt == bm * bn else KIND_MASKED
         assert got == expect
+
+
+# ---------------------------------------------------------------------------
+# fp8 (e4m3) quantisation of Q and K
+# ---------------------------------------------------------------------------
+
+def test_fp8_worked_example():
+    # amax 3 -> inv = 448 / 3 = 149.33: 1 -> 149.33 -> nearest e4m3 144 = 2^7 * 1.125 -> 0 1110 001;
+    # -0.5 -> -74.67 -> -72 = -(2^6 * 1.125) -> 1 1101 001; 0.25 -> 37.33 -> 36 = 2^5 * 1.125 -> 0 1100 001;
+    # 3 -> 448 = 2^8 * 1.75 -> 0 1111 110
+    x = np.array([1.0, -0.5, 0.25, 3.0], dtype=np.float32).reshape(1, 4, 1, 1)
+    codes, scale = oracle.quantize_fp8(x)
+    assert codes.ravel().tolist() == [0x71, 0xE9, 0x61, 0x7E]
+    assert scale[0, 0] == np.float32(3.0) / np.float32(448.0)
+
+
+def test_fp8_decode_every_code():
+    # e4m3 (bias 7, 3 mantissa bits): normal 2^(e-7) (1 + m/8), subnormal 2^-6 m/8; 0x7F / 0xFF are NaN
+    codes = np.arange(256, dtype=np.uint8)
+    got = oracle.decode_fp8(codes)
+    for c in range(256):
+        s, e, m = c >> 7, (c >> 3) & 15, c & 7
+        if e == 15 and m == 7:
+            assert np.isnan(got[c])
+            continue
+        mag = 2.0 ** (e - 7) * (1 + m / 8) if e else 2.0 ** -6 * (m / 8)
+        assert got[c] == (-mag if s else mag)
+
+
+def test_fp8_round_trip_and_amax():
+    rng = np.random.default_rng(81)
+    x = (rng.standard_normal((3, 40, 2, 16)) * np.array([1e-3, 5.0])[None, None, :, None]).astype(np.float32)
+    x[1, :, 0, :] = 0.0                                   # a group with amax 0
+    codes, scale = oracle.quantize_fp8(x)
+    deq = oracle.dequantize_fp8(codes, scale)
+    assert np.all(codes[1, :, 0, :] == 0) and scale[1, 0] == 0
+    for g in range(3):
+        for h in range(2):
+            a = np.abs(x[g, :, h, :])
+            if a.max() == 0:
+                continue
+            i = np.unravel_index(np.argmax(a), a.shape)
+            assert codes[g, i[0], h, i[1]] & 0x7F == 0x7E          # the amax element lands on +-448
+            # round trip: within half an e4m3 step (2^-4 relative for normals, 2^-10 absolute below)
+            y = np.abs(x[g, :, h, :]) / scale[g, h]
+            step = np.where(y >= 2.0 ** -6, 2.0 ** (np.floor(np.log2(np.maximum(y, 2.0 ** -6))) - 3), 2.0 ** -9)
+            assert np.all(np.abs(deq[g, :, h, :] - x[g, :, h, :]) <= 0.5 * step * scale[g, h] * (1 + 1e-6))
