@@ -365,6 +365,42 @@ hsap_status hsap_attn_fwd_fused(const hsap_attn_desc* desc, const void* q, const
                                 int64_t num_runs, void* o_out, float* lse_out, void* hip_stream);
 
 /*
+ * hsap_quantize_fp8 -- e4m3 codes of bf16 Q or K for the fp8 score variant
+ * (an extension beyond the paper's bf16 attention).  For every group g and
+ * head h of x [G, rows, H, d]: amax = max |x| over rows and d; scale[g, h] =
+ * amax / 448 and inv = 448 / amax (fp32 divisions; both 0 when amax = 0);
+ * code = e4m3(clamp(x * inv, -448, 448)), the fp32 product rounded to nearest
+ * even into the OCP e4m3 format (bias 7, largest finite value 448).  A
+ * shard's Q is G = 1; the chunks' K is G = P (one scale per chunk and head).
+ *   x       device bf16 [G, rows, H, d], 16-byte aligned; d a multiple of 8.
+ *   codes   device uint8 [G, rows, H, d], 8-byte aligned.
+ *   scale   device fp32 [G, H].
+ * NaN or infinite inputs are not handled.
+ */
+hsap_status hsap_quantize_fp8(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
+                              uint8_t* codes, float* scale, void* hip_stream);
+
+/*
+ * hsap_partial_attn_fwd_fp8 -- hsap_partial_attn_fwd with the scores taken
+ * from e4m3 operands: S = (Q8 K8^T) * q_scale[h] * k_scale[c, g] /
+ * sqrt-scale as in desc, i.e. the attention of the dequantised Q and K
+ * (codes times scales); softmax, P V (bf16 V) and the outputs as in the bf16
+ * partial forward.  Uses the 32x32x64 fp8 MFMA (twice the bf16 rate).
+ *   q8        device uint8 [n, Hq, d], q_scale device fp32 [Hq]
+ *             (hsap_quantize_fp8 with G = 1), 16-byte aligned.
+ *   k8        device uint8 [P, n, Hkv, d], k_scale device fp32 [P, Hkv]
+ *             (G = P), 16-byte aligned.
+ *   v, doc_start, tiles, runs, o_part, lse_part, num_slots  as for
+ *             hsap_partial_attn_fwd.
+ * Supported: head_dim 128; BM 64, 128 or 256; BN 64 or 128.
+ */
+hsap_status hsap_partial_attn_fwd_fp8(const hsap_attn_desc* desc, const uint8_t* q8, const uint8_t* k8,
+                                      const void* v, const float* q_scale, const float* k_scale,
+                                      const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
+                                      int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots,
+                                      void* hip_stream);
+
+/*
  * hsap_lse_merge -- online-softmax combination of partial results (the ring's
  * online accumulation, after Milakov & Gimelshein, inter-group SP section):
  *   L = m + ln sum_p exp(LSE_p - m),  m = max_p LSE_p;

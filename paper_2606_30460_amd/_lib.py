@@ -36,7 +36,8 @@ MAX_MERGE_PARTS = 64
 EXPORTED = (
     "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_load_matrix",
     "hsap_balance", "hsap_emit_forward", "hsap_doc_start",
-    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
+    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_quantize_fp8",
+    "hsap_partial_attn_fwd_fp8", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
     "hsap_partial_attn_bwd", "hsap_attn_bwd_bf16", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
     "hsap_executor_plan", "hsap_executor_info", "hsap_executor_forward", "hsap_executor_partial_forward",
     "hsap_executor_merge", "hsap_executor_backward",
@@ -102,6 +103,8 @@ _SIG = {
     "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
     "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_attn_fwd_fused": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
+    "hsap_quantize_fp8": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _P, _P, _P]),
+    "hsap_partial_attn_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_lse_merge": (ctypes.c_int, [_I32, _P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P,
@@ -356,6 +359,44 @@ def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev
     _check(lib().hsap_partial_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(doc_start_dev),
                                        _ptr(tiles_dev), _ptr(runs_dev), runs_dev.numel() // 4, _ptr(o_part),
                                        _ptr(lse_part), int(slots), _stream(stream)))
+
+
+def quantize_fp8(x, codes, scale, stream=None) -> None:
+    """hsap_quantize_fp8: x bf16 [G, rows, H, d] -> codes uint8 (same shape), scale fp32 [G, H]."""
+    if x.dim() != 4:
+        raise ValueError("x must be [groups, rows, heads, head_dim]")
+    G, rows, H, d = x.shape
+    _dev(x, "bfloat16", "x")
+    _dev(codes, "uint8", "codes", x.numel())
+    _dev(scale, "float32", "scale", G * H)
+    _check(lib().hsap_quantize_fp8(_ptr(x), int(G), int(rows), int(H), int(d), _ptr(codes), _ptr(scale),
+                                   _stream(stream)))
+
+
+def partial_attn_fwd_fp8(desc: AttnDesc, q8, k8, v, q_scale, k_scale, doc_start_dev, tiles_dev, runs_dev, o_part,
+                         lse_part, stream=None) -> None:
+    """hsap_partial_attn_fwd_fp8: the partial forward with e4m3 Q [n, Hq, d] and K [P, n, Hkv, d] and their
+    scales [Hq] and [P, Hkv] (hsap_quantize_fp8); V, outputs and lists as for partial_attn_fwd."""
+    s = desc.shard
+    n = s.rows
+    hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
+    _dev(q8, "uint8", "q8", n * hq * d)
+    _dev(k8, "uint8", "k8", P * n * hkv * d)
+    _dev(v, "bfloat16", "v", P * n * hkv * d)
+    _dev(q_scale, "float32", "q_scale", hq)
+    _dev(k_scale, "float32", "k_scale", P * hkv)
+    _dev(doc_start_dev, "int32", "doc_start", s.positions)
+    _dev(tiles_dev, "int32", "tiles")
+    _dev(runs_dev, "int32", "runs")
+    _dev(o_part, "float32", "o_part")
+    _dev(lse_part, "float32", "lse_part")
+    slots = o_part.numel() // (n * hq * d)
+    if o_part.numel() != slots * n * hq * d or lse_part.numel() != slots * hq * n or slots < 1:
+        raise ValueError("o_part / lse_part must hold a whole number of [n, Hq, d] / [Hq, n] slots")
+    _check(lib().hsap_partial_attn_fwd_fp8(ctypes.byref(desc), _ptr(q8), _ptr(k8), _ptr(v), _ptr(q_scale),
+                                           _ptr(k_scale), _ptr(doc_start_dev), _ptr(tiles_dev), _ptr(runs_dev),
+                                           runs_dev.numel() // 4, _ptr(o_part), _ptr(lse_part), int(slots),
+                                           _stream(stream)))
 
 
 def attn_fwd_fused(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev, o_out, lse_out, stream=None) -> None:

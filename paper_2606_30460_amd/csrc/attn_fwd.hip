@@ -26,6 +26,8 @@
 // FULL tiles skip all mask arithmetic; MASKED tiles compare each key position
 // with the query's document start and position.  O is rescaled only when
 // some row of the wave raised its running max by more than a fixed slack.
+#include <type_traits>
+
 #include "hsap_internal.h"
 #include "mfma.h"
 
@@ -43,6 +45,8 @@ struct FwdArgs {
   int32_t num_slots;
   __bf16* o_out;    // fused forward: final output [n, Hq, d]
   float* lse_out;   // fused forward: final LSE [Hq, n]
+  const float* q_scale;  // fp8 scores: dequantisation scale per query head [Hq]
+  const float* k_scale;  // fp8 scores: dequantisation scale per (chunk, K/V head) [P, Hkv]
   Geom geom;
   int32_t shard;
   int32_t hq;
@@ -51,19 +55,28 @@ struct FwdArgs {
   float scale_log2;
 };
 
-template <int D, int BN, int WAVES, bool FUSED>
+// FP8: Q and K are e4m3 codes (scores S = (Q8 K8^T) * q_scale[h] * k_scale[chunk, g]
+// from the 32x32x64 fp8 MFMA, a K row held as 128 bytes), V and the rest as in bf16.
+template <int D, int BN, int WAVES, bool FUSED, bool FP8 = false>
 __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
+  static_assert(!FP8 || D == 128, "fp8 scores need head_dim 128");
+  using KT = std::conditional_t<FP8, uint8_t, __bf16>;    // K element
+  using K16 = std::conditional_t<FP8, uint4, bf16x8>;     // 16 bytes of K
   constexpr int KB = 64;                     // keys per step
   constexpr int SUBS = BN / KB;              // steps per listed k-tile
   constexpr int NT = 64 * WAVES;
-  constexpr int KS = D + 8;                  // K row stride (bf16): 68 dwords, rows of a 16-lane b128 read hit distinct banks
+  // K row stride in elements: bf16 D + 8 (68 dwords), fp8 D + 16 (36 dwords); either way the
+  // rows of a 16-lane b128 read hit distinct banks
+  constexpr int KS = FP8 ? D + 16 : D + 8;
   constexpr int VS = D + 32;                 // V row stride (bf16): 16 (mod 64) dwords, 32 lanes of a transpose read hit distinct banks
-  constexpr int CHUNKS = KB * D / 8;         // 16-byte chunks per K (or V) step
+  constexpr int CHUNKS = KB * D / 8;         // 16-byte chunks per V (and bf16 K) step
   constexpr int PER_T = CHUNKS / NT;         // chunks per thread
-  static_assert(CHUNKS % NT == 0, "step must split evenly over the threads");
+  constexpr int KCPR = D * (int)sizeof(KT) / 16;   // 16-byte chunks per K row
+  constexpr int PER_TK = KB * KCPR / NT;     // K chunks per thread
+  static_assert(CHUNKS % NT == 0 && (KB * KCPR) % NT == 0, "step must split evenly over the threads");
   constexpr float NEG_INF = -__builtin_inff();
   constexpr float RESCALE_SLACK = 8.f;       // log2 units a row max may rise before O is rescaled
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[2][KB * KS];
+  __shared__ __attribute__((aligned(16))) KT Ks[2][KB * KS];
   __shared__ __attribute__((aligned(16))) __bf16 Vs[2][KB * VS];
 
   const int tid = threadIdx.x;
@@ -93,11 +106,21 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   const int32_t qstart = a.doc_start[gq];
   const uint32_t span = (uint32_t)(gq - qstart);  // key j is allowed iff 0 <= j - start <= span
   bf16x8 qf[D / 16];
-  {
+  i32x8 qf8[2];  // fp8: lane half hi holds bytes 64 kk + 32 hi .. +31 of its query's row
+  if constexpr (FP8) {
+    const uint8_t* qp = (const uint8_t*)a.q + (qrow * a.hq + h) * D + 32 * hi;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const uint4 lo = *(const uint4*)(qp + 64 * kk), hi4 = *(const uint4*)(qp + 64 * kk + 16);
+      qf8[kk] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi4.x, (int)hi4.y, (int)hi4.z, (int)hi4.w};
+    }
+  } else {
     const __bf16* qp = a.q + (qrow * a.hq + h) * D + 8 * hi;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
   }
+  // exp2 argument scale of this head (fp8: times the per-chunk K scale each step)
+  const float head_scale = FP8 ? a.scale_log2 * a.q_scale[h] : a.scale_log2;
   const int64_t rstride = (int64_t)a.hkv * D;
   const int total = run.count * SUBS;
   auto tile_at = [&](int s) { return a.tiles[run.first + s / SUBS]; };
@@ -111,19 +134,26 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   };
 
   // staging: thread t moves chunks t, t + NT, ... of a step's [KB][D] tile
-  int32_t goff[PER_T], koff[PER_T], voff[PER_T];
+  int32_t goff[PER_T], voff[PER_T], kgoff[PER_TK], koff[PER_TK];
 #pragma unroll
   for (int i = 0; i < PER_T; ++i) {
     const int idx = tid + i * NT, row = idx / (D / 8), cc = idx % (D / 8);
     goff[i] = (int32_t)(row * rstride + cc * 8);
-    koff[i] = row * KS + cc * 8;
     voff[i] = row * VS + cc * 8;
   }
-  bf16x8 kreg[PER_T], vreg[PER_T];
-  auto load_k = [&](int64_t off) {
-    const __bf16* src = a.k + off;
 #pragma unroll
-    for (int i = 0; i < PER_T; ++i) kreg[i] = *(const bf16x8*)(src + goff[i]);
+  for (int i = 0; i < PER_TK; ++i) {
+    const int idx = tid + i * NT, row = idx / KCPR, cc = idx % KCPR;
+    constexpr int EPC = 16 / (int)sizeof(KT);  // K elements per 16-byte chunk
+    kgoff[i] = (int32_t)(row * rstride + cc * EPC);
+    koff[i] = row * KS + cc * EPC;
+  }
+  K16 kreg[PER_TK];
+  bf16x8 vreg[PER_T];
+  auto load_k = [&](int64_t off) {
+    const KT* src = (const KT*)a.k + off;
+#pragma unroll
+    for (int i = 0; i < PER_TK; ++i) kreg[i] = *(const K16*)(src + kgoff[i]);
   };
   auto load_v = [&](int64_t off) {
     const __bf16* src = a.v + off;
@@ -132,7 +162,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   };
   auto store_k = [&](int slot) {
 #pragma unroll
-    for (int i = 0; i < PER_T; ++i) *(bf16x8*)(&Ks[slot][koff[i]]) = kreg[i];
+    for (int i = 0; i < PER_TK; ++i) *(K16*)(&Ks[slot][koff[i]]) = kreg[i];
   };
   auto store_v = [&](int slot) {
 #pragma unroll
@@ -140,15 +170,26 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   };
   // S^T = K Q^T for the two 32-key blocks of a step held in K slot `slot`
   auto scores = [&](int slot, f32x16 (&sc)[KB / 32]) {
-    const __bf16* K = Ks[slot];
+    const KT* K = Ks[slot];
 #pragma unroll
     for (int nb = 0; nb < KB / 32; ++nb) {
-      bf16x8 kf[D / 16];
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(K + (32 * nb + l32) * KS + 16 * kk + 8 * hi);
       sc[nb] = f32x16{};
+      if constexpr (FP8) {
+        // the K row's bytes 64 kk + 32 hi .. +31 pair with the same bytes of the query's row
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) sc[nb] = mfma32(kf[kk], qf[kk], sc[nb]);
+        for (int kk = 0; kk < 2; ++kk) {
+          const uint8_t* kp = K + (32 * nb + l32) * KS + 64 * kk + 32 * hi;
+          const uint4 lo = *(const uint4*)kp, hi4 = *(const uint4*)(kp + 16);
+          const i32x8 kf{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi4.x, (int)hi4.y, (int)hi4.z, (int)hi4.w};
+          sc[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf, qf8[kk], sc[nb], 0, 0, 0, 127, 0, 127);
+        }
+      } else {
+        bf16x8 kf[D / 16];
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(K + (32 * nb + l32) * KS + 16 * kk + 8 * hi);
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) sc[nb] = mfma32(kf[kk], qf[kk], sc[nb]);
+      }
     }
   };
 
@@ -186,6 +227,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 
   for (int s = 0; s < total; ++s) {
     const hsap_tile tile = tile_at(s);
+    const float sl = FP8 ? head_scale * a.k_scale[tile.chunk * a.hkv + g] : head_scale;
     if (s + 2 < total) load_k(step_off(tile_at(s + 2), s + 2));
     if (s + 1 < total) load_v(step_off(tile_at(s + 1), s + 1));
     // scores of the next step: independent of this step's softmax
@@ -206,7 +248,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
-    const float m_new = fmaxf(m_run, pair_max(mx) * a.scale_log2);
+    const float m_new = fmaxf(m_run, pair_max(mx) * sl);
     // The reference max only has to bound the scores loosely: O / l and
     // m + log2(l) do not depend on it.  Rescale only when some row's max rose
     // by more than RESCALE_SLACK (p then stays below 2^RESCALE_SLACK).
@@ -224,7 +266,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const float p = fast_exp2(__builtin_fmaf(sc[nb][j], a.scale_log2, -m_use));
+        const float p = fast_exp2(__builtin_fmaf(sc[nb][j], sl, -m_use));
         rs += p;
         pb[nb][j >> 3][j & 7] = (__bf16)p;
       }
@@ -538,18 +580,19 @@ static hsap_status launch_dl(const FwdArgs& a, int64_t num_runs, hipStream_t str
   return HSAP_OK;
 }
 
-template <int D, int BN, int WAVES, bool FUSED>
+template <int D, int BN, int WAVES, bool FUSED, bool FP8 = false>
 static hsap_status launch(const FwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_fwd_kernel<D, BN, WAVES, FUSED>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, BN, WAVES, FUSED, FP8>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream,
+                     a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
   return HSAP_OK;
 }
 
-// shared argument checks and dispatch of the partial and fused forwards
-template <bool FUSED>
+// shared argument checks and dispatch of the partial and fused forwards (FP8: e4m3 Q and K)
+template <bool FUSED, bool FP8 = false>
 static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
                            const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs, int64_t num_runs,
                            FwdArgs& a, hipStream_t s) {
@@ -560,7 +603,10 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
   if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
   const bool shape_ok = (d == 128 || d == 64) && (bn == 128 || bn == 64) &&
-                        (bm == 128 || bm == 64 || (bm == 256 && d == 128));
+                        (bm == 128 || bm == 64 || (bm == 256 && d == 128)) && (!FP8 || d == 128);
+  if (FP8 && !shape_ok)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no fp8 forward kernel for head_dim=%d BM=%d BN=%d (head_dim 128; BM 64, 128 or 256; "
+              "BN 64 or 128)", d, bm, bn);
   if (!shape_ok)
     HSAP_FAIL(HSAP_ERR_UNSUPPORTED,
               "no forward kernel for head_dim=%d BM=%d BN=%d (BM in {64, 128}, or 256 with d = 128; BN in {64, 128})",
@@ -581,6 +627,16 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   a.hkv = desc->heads_kv;
   a.group = desc->heads_q / desc->heads_kv;
   a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
+  if constexpr (FP8) {
+    if ((uintptr_t)q & 15 || (uintptr_t)k & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "fp8 q and k must be 16-byte aligned");
+    const int w = bm / 32;
+    if (bn == 128) return w == 2 ? launch<128, 128, 2, FUSED, true>(a, num_runs, s)
+                        : w == 4 ? launch<128, 128, 4, FUSED, true>(a, num_runs, s)
+                                 : launch<128, 128, 8, FUSED, true>(a, num_runs, s);
+    return w == 2 ? launch<128, 64, 2, FUSED, true>(a, num_runs, s)
+         : w == 4 ? launch<128, 64, 4, FUSED, true>(a, num_runs, s)
+                  : launch<128, 64, 8, FUSED, true>(a, num_runs, s);
+  } else {
 #define HSAP_FWD_CASE(D_, BN_, W_) \
   if (d == D_ && bn == BN_ && bm == 32 * W_) return launch<D_, BN_, W_, FUSED>(a, num_runs, s);
   if (d == 128 && bm == 256) return bn == 128 ? launch_dl<128, FUSED>(a, num_runs, s) : launch_dl<64, FUSED>(a, num_runs, s);
@@ -593,6 +649,7 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   HSAP_FWD_CASE(64, 128, 2)
   HSAP_FWD_CASE(64, 64, 2)
 #undef HSAP_FWD_CASE
+  }
   HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no forward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
 }
 
@@ -626,4 +683,23 @@ extern "C" hsap_status hsap_attn_fwd_fused(const hsap_attn_desc* desc, const voi
   a.lse_out = lse_out;
   a.num_slots = 1;
   return forward<true>(desc, q, k, v, doc_start, tiles, runs, num_runs, a, (hipStream_t)hip_stream);
+}
+
+extern "C" hsap_status hsap_partial_attn_fwd_fp8(const hsap_attn_desc* desc, const uint8_t* q8, const uint8_t* k8,
+                                                 const void* v, const float* q_scale, const float* k_scale,
+                                                 const int32_t* doc_start, const hsap_tile* tiles,
+                                                 const hsap_run* runs, int64_t num_runs, float* o_part,
+                                                 float* lse_part, int32_t num_slots, void* hip_stream) {
+  clear_error();
+  if (num_slots < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_slots < 1");
+  if (num_runs > 0 && (!o_part || !lse_part || !q_scale || !k_scale))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if ((uintptr_t)o_part & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_part must be 16-byte aligned");
+  FwdArgs a{};
+  a.o_part = o_part;
+  a.lse_part = lse_part;
+  a.num_slots = num_slots;
+  a.q_scale = q_scale;
+  a.k_scale = k_scale;
+  return forward<false, true>(desc, q8, k8, v, doc_start, tiles, runs, num_runs, a, (hipStream_t)hip_stream);
 }

@@ -1,6 +1,7 @@
 // Memory-bound kernels of libhsap: the LSE merge of partial results, the
 // backward's row term delta = rowsum(dO * O), fp32 -> bf16 conversion, the
-// per-position document start, and the gather into sharded order.
+// per-position document start, the gather into sharded order, and the e4m3
+// quantisation of Q and K for the fp8 score variant.
 #include <algorithm>
 
 #include "hsap_internal.h"
@@ -247,6 +248,51 @@ __global__ __launch_bounds__(256) void zero_kernel(uint4* dst, int64_t words16, 
   if (blockIdx.x == 0 && (int)threadIdx.x < tail_words) tail[threadIdx.x] = 0;
 }
 
+// ---------------------------------------------------------------------------
+// e4m3 quantisation: one workgroup per (group g, head h) of x [G, rows, H, d]:
+// amax over the slice, scale = amax / 448, then code = e4m3(clamp(x * 448 /
+// amax, +-448)) with the hardware's round-to-nearest-even conversion (which
+// without the clamp would turn values beyond 448 into NaN codes).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void quantize_fp8_kernel(const __bf16* x, int64_t rows, int32_t heads, int32_t d,
+                                                           uint8_t* out, float* scale) {
+  __shared__ float part[4];
+  const int gh = blockIdx.x, h = gh % heads;
+  const int64_t g = gh / heads;
+  const int per_row = d / 8;  // 16-byte chunks of a row
+  const int64_t chunks = rows * per_row;
+  auto offset = [&](int64_t i) {
+    const int64_t r = i / per_row;
+    return ((g * rows + r) * heads + h) * d + (i - r * per_row) * 8;
+  };
+  float amax = 0.f;
+  for (int64_t i = threadIdx.x; i < chunks; i += 256) {
+    const bf16x8 v = *(const bf16x8*)(x + offset(i));
+#pragma unroll
+    for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)v[e]));
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 64));
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3]));
+  const float inv = amax > 0.f ? 448.f / amax : 0.f;
+  if (threadIdx.x == 0) scale[gh] = amax > 0.f ? amax / 448.f : 0.f;
+  for (int64_t i = threadIdx.x; i < chunks; i += 256) {
+    const int64_t o = offset(i);
+    const bf16x8 v = *(const bf16x8*)(x + o);
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = fminf(fmaxf((float)v[e] * inv, -448.f), 448.f);
+    int lo = 0, hi = 0;
+    lo = __builtin_amdgcn_cvt_pk_fp8_f32(y[0], y[1], lo, false);
+    lo = __builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], lo, true);
+    hi = __builtin_amdgcn_cvt_pk_fp8_f32(y[4], y[5], hi, false);
+    hi = __builtin_amdgcn_cvt_pk_fp8_f32(y[6], y[7], hi, true);
+    *(uint2*)(out + o) = make_uint2((uint32_t)lo, (uint32_t)hi);
+  }
+}
+
 static hsap_status check_launch(const char* what) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
@@ -351,6 +397,21 @@ hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, vo
   hipLaunchKernelGGL(convert_kernel, dim3(grid_for((count + 7) / 8)), dim3(256), 0, (hipStream_t)hip_stream, src,
                      (__bf16*)dst, count, vec);
   return check_launch("convert");
+}
+
+hsap_status hsap_quantize_fp8(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
+                              uint8_t* codes, float* scale, void* hip_stream) {
+  clear_error();
+  if (groups < 1 || rows < 1 || heads < 1 || head_dim < 8 || head_dim % 8)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "bad shape: groups %d, rows %lld, heads %d, head_dim %d (a multiple of 8)", groups,
+              (long long)rows, heads, head_dim);
+  if ((int64_t)groups * heads > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many groups x heads");
+  if (!x || !codes || !scale) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (((uintptr_t)x & 15) || ((uintptr_t)codes & 7))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "x must be 16-byte and codes 8-byte aligned");
+  hipLaunchKernelGGL(quantize_fp8_kernel, dim3((unsigned)(groups * heads)), dim3(256), 0, (hipStream_t)hip_stream,
+                     (const __bf16*)x, rows, heads, head_dim, codes, scale);
+  return check_launch("quantize_fp8");
 }
 
 hsap_status hsap_doc_start(const int32_t* cu_seqlens, int32_t num_docs, int64_t total_tokens, int32_t* doc_start,
