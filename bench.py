@@ -327,6 +327,64 @@ def all_shards_analysis(name: str, layouts=None, reps: int = 5) -> dict:
     return out
 
 
+def fp8_analysis(name: str, reps: int = 20) -> dict:
+    """The fp8 score variant on the workload's shard: e4m3 quantisation of Q and of every chunk's K
+    (hsap_quantize_fp8), then the partial forward with fp8 scores (hsap_partial_attn_fwd_fp8) over
+    the same plan as the bf16 partial forward, which is timed beside it; back-to-back launches
+    between two events, mean per launch."""
+    import torch
+    from paper_2606_30460_amd import _lib as L
+    from paper_2606_30460_amd.shard_attention import ShardAttention, to_sharded
+    from workloads import make_workload
+
+    w = make_workload(name)
+    if w.head_dim != 128 or w.batch != 1:
+        return {}
+    shard = w.shard if w.shard is not None else _critical_shard(L, w)
+    sa = ShardAttention(w.cu_seqlens, w.total_tokens, w.sp_degree, w.layout, shard, w.heads_q, w.heads_kv,
+                        w.head_dim, w.block_m, w.block_n)
+    sa.plan()
+    dev = torch.device("cuda")
+    t = w.tensors(backward=False)
+    q = to_sharded(sa.shard, t["q"].to(dev))[shard].contiguous()
+    k, v = to_sharded(sa.shard, t["k"].to(dev)), to_sharded(sa.shard, t["v"].to(dev))
+    del t
+    q8 = torch.empty(q.shape, dtype=torch.uint8, device=dev)
+    k8 = torch.empty(k.shape, dtype=torch.uint8, device=dev)
+    qs = torch.empty(1, w.heads_q, dtype=torch.float32, device=dev)
+    ks = torch.empty(w.sp_degree, w.heads_kv, dtype=torch.float32, device=dev)
+    work = torch.empty(w.sp_degree * max(w.heads_q, w.heads_kv) * L.QUANT_SPLIT, dtype=torch.float32, device=dev)
+    bufs = sa.alloc_forward()
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        for _ in range(reps):
+            fn()
+        e[1].record()
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / reps
+
+    wq, wk = work[:w.heads_q * L.QUANT_SPLIT], work[:w.sp_degree * w.heads_kv * L.QUANT_SPLIT]
+    quant_ms = timed(lambda: (L.quantize_fp8(q.unsqueeze(0), q8.unsqueeze(0), qs, wq), L.quantize_fp8(k, k8, ks, wk)))
+    fp8_ms = timed(lambda: L.partial_attn_fwd_fp8(sa.desc, q8, k8, v, qs, ks, sa.doc_start, sa.tiles_q, sa.runs_q,
+                                                  bufs["o_part"], bufs["lse_part"]))
+    bf16_ms = timed(lambda: L.partial_attn_fwd(sa.desc, q, k, v, sa.doc_start, sa.tiles_q, sa.runs_q, bufs["o_part"],
+                                               bufs["lse_part"]))
+    flops = 4.0 * w.head_dim * w.heads_q * sa.total_useful_pairs
+    log("[bench] fp8 scores %s: partial forward %.3f ms (%.1f TFLOP/s) vs bf16 %.3f ms; quantisation %.3f ms" % (
+        name, fp8_ms, flops / (fp8_ms * 1e-3) / 1e12, bf16_ms, quant_ms))
+    out = {"fp8_partial_fwd_ms": round(fp8_ms, 5), "fp8_partial_fwd_tflops": round(flops / (fp8_ms * 1e-3) / 1e12, 1),
+           "bf16_partial_fwd_ms_same_loop": round(bf16_ms, 5),
+           "bf16_partial_fwd_tflops_same_loop": round(flops / (bf16_ms * 1e-3) / 1e12, 1),
+           "quantize_q_and_k_ms": round(quant_ms, 5)}
+    del q, k, v, q8, k8, bufs, sa
+    torch.cuda.empty_cache()
+    return out
+
+
 FWD_SOURCES = ("paper_2606_30460_amd/csrc/attn_fwd.hip", "paper_2606_30460_amd/csrc/mfma.h",
                "paper_2606_30460_amd/csrc/hsap_internal.h")
 TRAFFIC_SUMMARY = "profiles/attn_fwd_hbm_traffic.md"
@@ -416,6 +474,10 @@ def main():
         r = measure(name, min(args.steps, 20), min(args.warmup, 3))
         r.pop("_fwd_flops", None)
         extra[name] = r
+    if not args.no_all_shards:       # analyses beside the timed step, skipped under kernel traces
+        for name, res in [(args.workload, main_res)] + list(extra.items()):
+            if not res["backward"]:
+                res["fp8_scores"] = fp8_analysis(name)
     if not args.no_all_shards:
         main_res["all_shards"] = all_shards_analysis(args.workload)
     cpu = None

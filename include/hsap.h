@@ -372,13 +372,18 @@ hsap_status hsap_attn_fwd_fused(const hsap_attn_desc* desc, const void* q, const
  * code = e4m3(clamp(x * inv, -448, 448)), the fp32 product rounded to nearest
  * even into the OCP e4m3 format (bias 7, largest finite value 448).  A
  * shard's Q is G = 1; the chunks' K is G = P (one scale per chunk and head).
- *   x       device bf16 [G, rows, H, d], 16-byte aligned; d a multiple of 8.
- *   codes   device uint8 [G, rows, H, d], 8-byte aligned.
- *   scale   device fp32 [G, H].
- * NaN or infinite inputs are not handled.
+ *   x          device bf16 [G, rows, H, d], 16-byte aligned; d a multiple
+ *              of 8.
+ *   codes      device uint8 [G, rows, H, d], 8-byte aligned.
+ *   scale      device fp32 [G, H].
+ *   workspace  device fp32 [G * H * HSAP_QUANT_SPLIT]: per-range maxima (each
+ *              slice's rows are reduced in HSAP_QUANT_SPLIT ranges); caller
+ *              owned, contents on entry ignored.
+ * Two launches on `stream`.  NaN or infinite inputs are not handled.
  */
+#define HSAP_QUANT_SPLIT 32
 hsap_status hsap_quantize_fp8(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
-                              uint8_t* codes, float* scale, void* hip_stream);
+                              uint8_t* codes, float* scale, float* workspace, void* hip_stream);
 
 /*
  * hsap_partial_attn_fwd_fp8 -- hsap_partial_attn_fwd with the scores taken

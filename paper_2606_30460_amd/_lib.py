@@ -103,7 +103,7 @@ _SIG = {
     "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
     "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_attn_fwd_fused": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
-    "hsap_quantize_fp8": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _P, _P, _P]),
+    "hsap_quantize_fp8": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _P, _P, _P, _P]),
     "hsap_partial_attn_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_lse_merge": (ctypes.c_int, [_I32, _P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
@@ -361,16 +361,21 @@ def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev
                                        _ptr(lse_part), int(slots), _stream(stream)))
 
 
-def quantize_fp8(x, codes, scale, stream=None) -> None:
-    """hsap_quantize_fp8: x bf16 [G, rows, H, d] -> codes uint8 (same shape), scale fp32 [G, H]."""
+QUANT_SPLIT = 32
+
+
+def quantize_fp8(x, codes, scale, workspace, stream=None) -> None:
+    """hsap_quantize_fp8: x bf16 [G, rows, H, d] -> codes uint8 (same shape), scale fp32 [G, H];
+    workspace fp32 [G * H * QUANT_SPLIT]."""
     if x.dim() != 4:
         raise ValueError("x must be [groups, rows, heads, head_dim]")
     G, rows, H, d = x.shape
     _dev(x, "bfloat16", "x")
     _dev(codes, "uint8", "codes", x.numel())
     _dev(scale, "float32", "scale", G * H)
+    _dev(workspace, "float32", "workspace", G * H * QUANT_SPLIT)
     _check(lib().hsap_quantize_fp8(_ptr(x), int(G), int(rows), int(H), int(d), _ptr(codes), _ptr(scale),
-                                   _stream(stream)))
+                                   _ptr(workspace), _stream(stream)))
 
 
 def partial_attn_fwd_fp8(desc: AttnDesc, q8, k8, v, q_scale, k_scale, doc_start_dev, tiles_dev, runs_dev, o_part,

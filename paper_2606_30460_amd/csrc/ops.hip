@@ -249,38 +249,76 @@ __global__ __launch_bounds__(256) void zero_kernel(uint4* dst, int64_t words16, 
 }
 
 // ---------------------------------------------------------------------------
-// e4m3 quantisation: one workgroup per (group g, head h) of x [G, rows, H, d]:
-// amax over the slice, scale = amax / 448, then code = e4m3(clamp(x * 448 /
-// amax, +-448)) with the hardware's round-to-nearest-even conversion (which
-// without the clamp would turn values beyond 448 into NaN codes).
+// e4m3 quantisation of x [G, rows, H, d]: each (group g, head h) slice is cut
+// into QSPLIT row ranges.  Pass 1: one workgroup per range writes the range's
+// amax to the workspace.  Pass 2: one workgroup per range takes the slice's
+// amax from its QSPLIT partial maxima, writes scale = amax / 448 (range 0),
+// and converts its rows: code = e4m3(clamp(x * 448 / amax, +-448)) with the
+// hardware's round-to-nearest-even conversion (which without the clamp would
+// turn values beyond 448 into NaN codes).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void quantize_fp8_kernel(const __bf16* x, int64_t rows, int32_t heads, int32_t d,
-                                                           uint8_t* out, float* scale) {
-  __shared__ float part[4];
-  const int gh = blockIdx.x, h = gh % heads;
-  const int64_t g = gh / heads;
-  const int per_row = d / 8;  // 16-byte chunks of a row
-  const int64_t chunks = rows * per_row;
-  auto offset = [&](int64_t i) {
+constexpr int QSPLIT = HSAP_QUANT_SPLIT;
+
+struct QuantArgs {
+  const __bf16* x;
+  int64_t rows;
+  int32_t heads, d;
+  uint8_t* out;
+  float* scale;
+  float* partial;  // [G * H * QSPLIT]
+};
+
+// the 16-byte chunks [c0, c1) of slice gh's row range s, and the element offset of chunk i
+struct QuantRange {
+  int64_t c0, c1, g;
+  int32_t h, per_row;
+  __device__ QuantRange(const QuantArgs& a, int gh, int s) {
+    g = gh / a.heads;
+    h = gh - (int32_t)g * a.heads;
+    per_row = a.d / 8;
+    const int64_t r0 = a.rows * s / QSPLIT, r1 = a.rows * (s + 1) / QSPLIT;
+    c0 = r0 * per_row;
+    c1 = r1 * per_row;
+  }
+  __device__ int64_t offset(const QuantArgs& a, int64_t i) const {
     const int64_t r = i / per_row;
-    return ((g * rows + r) * heads + h) * d + (i - r * per_row) * 8;
-  };
+    return ((g * a.rows + r) * a.heads + h) * a.d + (i - r * per_row) * 8;
+  }
+};
+
+__device__ inline float block_max_256(float v, float* part) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3]));
+}
+
+__global__ __launch_bounds__(256) void quantize_amax_kernel(QuantArgs a) {
+  __shared__ float part[4];
+  const int gh = blockIdx.x / QSPLIT, sp = blockIdx.x - gh * QSPLIT;
+  const QuantRange q(a, gh, sp);
   float amax = 0.f;
-  for (int64_t i = threadIdx.x; i < chunks; i += 256) {
-    const bf16x8 v = *(const bf16x8*)(x + offset(i));
+  for (int64_t i = q.c0 + threadIdx.x; i < q.c1; i += 256) {
+    const bf16x8 v = *(const bf16x8*)(a.x + q.offset(a, i));
 #pragma unroll
     for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)v[e]));
   }
+  amax = block_max_256(amax, part);
+  if (threadIdx.x == 0) a.partial[blockIdx.x] = amax;
+}
+
+__global__ __launch_bounds__(256) void quantize_convert_kernel(QuantArgs a) {
+  const int gh = blockIdx.x / QSPLIT, sp = blockIdx.x - gh * QSPLIT;
+  float amax = 0.f;
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 64));
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = amax;
-  __syncthreads();
-  amax = fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3]));
+  for (int i = 0; i < QSPLIT; ++i) amax = fmaxf(amax, a.partial[gh * QSPLIT + i]);
   const float inv = amax > 0.f ? 448.f / amax : 0.f;
-  if (threadIdx.x == 0) scale[gh] = amax > 0.f ? amax / 448.f : 0.f;
-  for (int64_t i = threadIdx.x; i < chunks; i += 256) {
-    const int64_t o = offset(i);
-    const bf16x8 v = *(const bf16x8*)(x + o);
+  if (sp == 0 && threadIdx.x == 0) a.scale[gh] = amax > 0.f ? amax / 448.f : 0.f;
+  const QuantRange q(a, gh, sp);
+  for (int64_t i = q.c0 + threadIdx.x; i < q.c1; i += 256) {
+    const int64_t o = q.offset(a, i);
+    const bf16x8 v = *(const bf16x8*)(a.x + o);
     float y[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) y[e] = fminf(fmaxf((float)v[e] * inv, -448.f), 448.f);
@@ -289,7 +327,7 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(const __bf16* x, int6
     lo = __builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], lo, true);
     hi = __builtin_amdgcn_cvt_pk_fp8_f32(y[4], y[5], hi, false);
     hi = __builtin_amdgcn_cvt_pk_fp8_f32(y[6], y[7], hi, true);
-    *(uint2*)(out + o) = make_uint2((uint32_t)lo, (uint32_t)hi);
+    *(uint2*)(a.out + o) = make_uint2((uint32_t)lo, (uint32_t)hi);
   }
 }
 
@@ -400,18 +438,22 @@ hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, vo
 }
 
 hsap_status hsap_quantize_fp8(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
-                              uint8_t* codes, float* scale, void* hip_stream) {
+                              uint8_t* codes, float* scale, float* workspace, void* hip_stream) {
   clear_error();
   if (groups < 1 || rows < 1 || heads < 1 || head_dim < 8 || head_dim % 8)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "bad shape: groups %d, rows %lld, heads %d, head_dim %d (a multiple of 8)", groups,
               (long long)rows, heads, head_dim);
-  if ((int64_t)groups * heads > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many groups x heads");
-  if (!x || !codes || !scale) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if ((int64_t)groups * heads * QSPLIT > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many groups x heads");
+  if (!x || !codes || !scale || !workspace) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if (((uintptr_t)x & 15) || ((uintptr_t)codes & 7))
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "x must be 16-byte and codes 8-byte aligned");
-  hipLaunchKernelGGL(quantize_fp8_kernel, dim3((unsigned)(groups * heads)), dim3(256), 0, (hipStream_t)hip_stream,
-                     (const __bf16*)x, rows, heads, head_dim, codes, scale);
-  return check_launch("quantize_fp8");
+  const QuantArgs a{(const __bf16*)x, rows, heads, head_dim, codes, scale, workspace};
+  const dim3 grid((unsigned)(groups * heads * QSPLIT));
+  hipLaunchKernelGGL(quantize_amax_kernel, grid, dim3(256), 0, (hipStream_t)hip_stream, a);
+  hsap_status st = check_launch("quantize_fp8 amax");
+  if (st != HSAP_OK) return st;
+  hipLaunchKernelGGL(quantize_convert_kernel, grid, dim3(256), 0, (hipStream_t)hip_stream, a);
+  return check_launch("quantize_fp8 convert");
 }
 
 hsap_status hsap_doc_start(const int32_t* cu_seqlens, int32_t num_docs, int64_t total_tokens, int32_t* doc_start,

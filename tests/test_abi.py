@@ -164,10 +164,11 @@ def test_fp8_entry_points_validate_before_launch():
     st = lib.hsap_partial_attn_fwd_fp8(ctypes.byref(_attn_desc()), ctypes.c_void_p(4104), fake, fake, fake, fake,
                                        fake, fake, fake, 1, fake, fake, 1, None)
     assert st == L.HSAP_ERR_INVALID_ARG                      # q8 not 16-byte aligned
-    assert lib.hsap_quantize_fp8(fake, 1, 4, 2, 12, fake, fake, None) == L.HSAP_ERR_INVALID_ARG   # d % 8
-    assert lib.hsap_quantize_fp8(fake, 0, 4, 2, 16, fake, fake, None) == L.HSAP_ERR_INVALID_ARG
-    assert lib.hsap_quantize_fp8(ctypes.c_void_p(4100), 1, 4, 2, 16, fake, fake, None) == L.HSAP_ERR_INVALID_ARG
-    assert lib.hsap_quantize_fp8(fake, 1, 4, 2, 16, None, fake, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_quantize_fp8(fake, 1, 4, 2, 12, fake, fake, fake, None) == L.HSAP_ERR_INVALID_ARG   # d % 8
+    assert lib.hsap_quantize_fp8(fake, 0, 4, 2, 16, fake, fake, fake, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_quantize_fp8(ctypes.c_void_p(4100), 1, 4, 2, 16, fake, fake, fake, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_quantize_fp8(fake, 1, 4, 2, 16, None, fake, fake, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_quantize_fp8(fake, 1, 4, 2, 16, fake, fake, None, None) == L.HSAP_ERR_INVALID_ARG
 
 
 def test_backward_validates_before_launch():

@@ -28,7 +28,8 @@ def _say(*a):
 def _quantize(x):
     codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
     scale = torch.empty(x.shape[0], x.shape[2], dtype=torch.float32, device=x.device)
-    L.quantize_fp8(x, codes, scale)
+    work = torch.full((x.shape[0] * x.shape[2] * L.QUANT_SPLIT,), float("nan"), dtype=torch.float32, device=x.device)
+    L.quantize_fp8(x, codes, scale, work)
     return codes, scale
 
 
