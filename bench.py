@@ -61,16 +61,19 @@ def _positions(N: int, P: int, layout: int, x: int, local: np.ndarray) -> np.nda
     return b * N + np.where(local < m, x * m + local, (2 * P - 1 - x) * m + (local - m))
 
 
-def _finite_partial_rows(L, cu, sd, split: int) -> int:
-    """(part, query row) pairs whose partial LSE is finite, from the plan on the host: a row of a
+def _merged_rows(L, cu, sd, split: int):
+    """(finite, merged): the (part, query row) pairs whose partial LSE is finite among the rows the
+    merge handles, and the number of those rows, from the plan on the host.  A q-tile whose only
+    run holding tiles is unsplit is written final by the partial forward and not merged; a row of a
     q-major run has an allowed key iff some tile of the run holds a key j with start(i) <= j <= i."""
     tiles = L.plan(cu, sd)["tiles"]
     sorted_tiles, runs, _ = L.plan_runs(sd, tiles, L.MAJOR_Q, split)
     N, P, bm, bn = sd.total_tokens, sd.sp_degree, sd.block_m, sd.block_n
+    busy = np.bincount(runs[runs[:, 3] > 0][:, 1], minlength=sd.rows // bm)
     starts = np.repeat(cu[:-1].astype(np.int64), np.diff(cu))
     count = 0
     for _, t, first, cnt in runs:
-        if cnt == 0:
+        if cnt == 0 or busy[t] == 1:
             continue
         gi = _positions(N, P, sd.layout, sd.shard_id, np.arange(t * bm, (t + 1) * bm))
         si = starts[gi]
@@ -79,7 +82,7 @@ def _finite_partial_rows(L, cu, sd, split: int) -> int:
             k0 = int(_positions(N, P, sd.layout, int(c), np.array([kt * bn]))[0])  # a tile's keys are contiguous
             ok |= (k0 <= gi) & (k0 + bn - 1 >= si)
         count += int(ok.sum())
-    return count
+    return count, int(np.sum(busy != 1)) * bm
 
 
 def measure(name: str, steps: int, warmup: int, backward=None):
@@ -117,7 +120,7 @@ def measure(name: str, steps: int, warmup: int, backward=None):
         ex.plan(cu)
         if e:
             e[0].record()
-        ex.partial_forward(q, k, v)
+        ex.partial_forward(q, k, v, o, lse)
         if e:
             e[1].record()
         ex.merge(o, lse)
@@ -168,10 +171,11 @@ def measure(name: str, steps: int, warmup: int, backward=None):
         L.plan(cu, sd)
     plan_ms = (time.perf_counter() - t1) / reps * 1e3
 
-    # algorithmic merge bytes: every part's LSE row, the O row of parts whose LSE is finite, the outputs
-    finite_rows = _finite_partial_rows(L, cu, sd, info["split_length"]) * w.heads_q
-    merge_bytes = (info["num_parts"] * w.heads_q * n * 4 + finite_rows * w.head_dim * 4
-                   + n * w.heads_q * (2 * w.head_dim + 4))
+    # algorithmic merge bytes over the rows it merges: every part's LSE, the O rows of parts whose
+    # LSE is finite, the outputs (rows of single-part q-tiles are written final by the forward)
+    finite, merged = _merged_rows(L, cu, sd, info["split_length"])
+    merge_bytes = (info["num_parts"] * w.heads_q * merged * 4 + finite * w.heads_q * w.head_dim * 4
+                   + merged * w.heads_q * (2 * w.head_dim + 4))
 
     pairs = info["useful_pairs"]
     tiles = info["num_tiles"]

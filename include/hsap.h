@@ -537,7 +537,8 @@ typedef struct {
   int32_t num_parts;        /* partial outputs the forward writes and merges */
   int32_t split_length;     /* max_run_tiles used for the q-major runs (0: none) */
   int32_t chunks_with_tiles;
-  int32_t reserved;
+  int32_t final_q_tiles;    /* q-tiles whose only part the partial forward
+                               writes as final output (the merge skips them) */
   uint64_t chunk_mask;      /* bit c set: chunk c has tiles (P <= 64)        */
 } hsap_exec_info;
 
@@ -579,7 +580,11 @@ hsap_status hsap_executor_info(const hsap_executor* ex, hsap_exec_info* info);
 /*
  * hsap_executor_forward -- the shard's attention against every chunk for the
  * current plan.  fused = 0: hsap_partial_attn_fwd over all q-major runs into
- * the executor's partials, then hsap_lse_merge of the num_parts partials.
+ * the executor's partials, then hsap_lse_merge of the num_parts partials --
+ * except that a q-tile whose tiles all lie in one chunk, in one unsplit run,
+ * has a single part: that run writes its final O (bf16) and LSE to o_out /
+ * lse_out directly and the merge leaves those rows alone (the merge of one
+ * part returns it unchanged, so the result is the same bit for bit).
  * fused = 1 (needs HSAP_EXEC_FUSED): hsap_attn_fwd_fused.
  *   q        device bf16 [n, Hq, d];  k, v  device bf16 [P, n, Hkv, d].
  *   o_out    device bf16 [n, Hq, d];  lse_out  device fp32 [Hq, n].
@@ -590,12 +595,14 @@ hsap_status hsap_executor_forward(hsap_executor* ex, const void* q, const void* 
 /*
  * hsap_executor_partial_forward, hsap_executor_merge -- the two stages of
  * hsap_executor_forward(fused = 0), callable one by one (e.g. to time them):
- * the partial attention of every q-major run into the executor's partials,
- * then their merge into o_out / lse_out.  The merge reads the partials of
- * the last partial forward; call them in this order, after the same plan.
+ * the partial attention of every q-major run into the executor's partials
+ * (single-part q-tiles straight into o_out / lse_out), then the merge of the
+ * other rows into o_out / lse_out.  The merge reads the partials of the last
+ * partial forward; call them in this order, after the same plan, with the
+ * same outputs.
  */
 hsap_status hsap_executor_partial_forward(hsap_executor* ex, const void* q, const void* k, const void* v,
-                                          void* hip_stream);
+                                          void* o_out, float* lse_out, void* hip_stream);
 hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, void* hip_stream);
 
 /*

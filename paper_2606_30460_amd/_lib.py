@@ -82,7 +82,7 @@ class ExecInfo(ctypes.Structure):
     _fields_ = [("num_tiles", ctypes.c_int64), ("num_full_tiles", ctypes.c_int64), ("useful_pairs", ctypes.c_int64),
                 ("num_runs_q", ctypes.c_int64), ("num_runs_k", ctypes.c_int64), ("num_runs_all", ctypes.c_int64),
                 ("num_parts", ctypes.c_int32), ("split_length", ctypes.c_int32),
-                ("chunks_with_tiles", ctypes.c_int32), ("reserved", ctypes.c_int32), ("chunk_mask", ctypes.c_uint64)]
+                ("chunks_with_tiles", ctypes.c_int32), ("final_q_tiles", ctypes.c_int32), ("chunk_mask", ctypes.c_uint64)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -116,7 +116,7 @@ _SIG = {
     "hsap_executor_plan": (ctypes.c_int, [_P, _P, _I32, _P]),
     "hsap_executor_info": (ctypes.c_int, [_P, _P]),
     "hsap_executor_forward": (ctypes.c_int, [_P, _P, _P, _P, _I32, _P, _P, _P]),
-    "hsap_executor_partial_forward": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+    "hsap_executor_partial_forward": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "hsap_executor_merge": (ctypes.c_int, [_P, _P, _P, _P]),
     "hsap_executor_backward": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
 }
@@ -556,7 +556,7 @@ class Executor:
     def info(self) -> Dict[str, int]:
         out = ExecInfo()
         _check(lib().hsap_executor_info(self._handle(), ctypes.byref(out)))
-        return {name: int(getattr(out, name)) for name, _ in ExecInfo._fields_ if name != "reserved"}
+        return {name: int(getattr(out, name)) for name, _ in ExecInfo._fields_}
 
     def forward(self, q, k, v, o_out, lse_out, fused: bool = False, stream=None) -> None:
         _dev(q, "bfloat16", "q", self._q_numel)
@@ -567,15 +567,19 @@ class Executor:
         _check(lib().hsap_executor_forward(self._handle(), _ptr(q), _ptr(k), _ptr(v), int(bool(fused)), _ptr(o_out),
                                            _ptr(lse_out), _stream(stream)))
 
-    def partial_forward(self, q, k, v, stream=None) -> None:
-        """First stage of forward(fused=False): partial attention into the executor's partials."""
+    def partial_forward(self, q, k, v, o_out, lse_out, stream=None) -> None:
+        """First stage of forward(fused=False): partial attention into the executor's partials (q-tiles
+        with a single part straight into o_out / lse_out)."""
         _dev(q, "bfloat16", "q", self._q_numel)
         _dev(k, "bfloat16", "k", self._kv_numel)
         _dev(v, "bfloat16", "v", self._kv_numel)
-        _check(lib().hsap_executor_partial_forward(self._handle(), _ptr(q), _ptr(k), _ptr(v), _stream(stream)))
+        _dev(o_out, "bfloat16", "o_out", self._q_numel)
+        _dev(lse_out, "float32", "lse_out", self._lse_numel)
+        _check(lib().hsap_executor_partial_forward(self._handle(), _ptr(q), _ptr(k), _ptr(v), _ptr(o_out),
+                                                   _ptr(lse_out), _stream(stream)))
 
     def merge(self, o_out, lse_out, stream=None) -> None:
-        """Second stage: LSE merge of the partials into o_out / lse_out."""
+        """Second stage: LSE merge of the partials into o_out / lse_out (the rows the first stage left)."""
         _dev(o_out, "bfloat16", "o_out", self._q_numel)
         _dev(lse_out, "float32", "lse_out", self._lse_numel)
         _check(lib().hsap_executor_merge(self._handle(), _ptr(o_out), _ptr(lse_out), _stream(stream)))

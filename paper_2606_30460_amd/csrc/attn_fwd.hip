@@ -85,13 +85,15 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   const int h = blockIdx.x - run_idx * a.hq;
   const hsap_run run = a.runs[run_idx];
   const int slot = run.slot;  // partial-output slot of this run (partial forward)
-  if (!FUSED && (slot < 0 || slot >= a.num_slots)) return;
+  // FUSED, or a partial run marked final (its q-tile's only part): write the final output
+  const bool final_out = FUSED || (slot == kFinalSlot && a.o_out != nullptr);
+  if (!final_out && (slot < 0 || slot >= a.num_slots)) return;
   const int g = h / a.group;
   const int64_t n = a.geom.n;
   const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;  // this lane's query row (shard-local)
 
   if (run.count == 0) {  // no key for this q-tile in this run
-    if (FUSED) {
+    if (final_out) {
       bf16x4* op = (bf16x4*)(a.o_out + (qrow * a.hq + h) * D + 4 * hi);
 #pragma unroll
       for (int e = 0; e < D / 8; ++e) op[2 * e] = bf16x4{};
@@ -297,7 +299,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   l_run = pair_sum(l_run);
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
   const float lse = l_run > 0.f ? (m_run + __log2f(l_run)) * 0.69314718055994530942f : NEG_INF;
-  if (FUSED) {
+  if (final_out) {
     // final output: this lane's query, d = 32 mb + 8 grp + 4 hi + 0..3
     __bf16* op = a.o_out + (qrow * a.hq + h) * D + 4 * hi;
 #pragma unroll
@@ -349,13 +351,14 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   const int h = blockIdx.x - run_idx * a.hq;
   const hsap_run run = a.runs[run_idx];
   const int slot = run.slot;
-  if (!FUSED && (slot < 0 || slot >= a.num_slots)) return;
+  const bool final_out = FUSED || (slot == kFinalSlot && a.o_out != nullptr);
+  if (!final_out && (slot < 0 || slot >= a.num_slots)) return;
   const int g = h / a.group;
   const int64_t n = a.geom.n;
   const int64_t qrow = (int64_t)run.tile * 256 + 32 * w + l32;
 
   if (run.count == 0) {
-    if (FUSED) {
+    if (final_out) {
       bf16x4* op = (bf16x4*)(a.o_out + (qrow * a.hq + h) * D + 4 * hi);
 #pragma unroll
       for (int e = 0; e < D / 8; ++e) op[2 * e] = bf16x4{};
@@ -545,7 +548,7 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   l_run = pair_sum(l_run);
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
   const float lse = l_run > 0.f ? (m_run + __log2f(l_run)) * 0.69314718055994530942f : NEG_INF;
-  if (FUSED) {
+  if (final_out) {
     __bf16* op = a.o_out + (qrow * a.hq + h) * D + 4 * hi;
 #pragma unroll
     for (int mb = 0; mb < D / 32; ++mb)
@@ -703,3 +706,24 @@ extern "C" hsap_status hsap_partial_attn_fwd_fp8(const hsap_attn_desc* desc, con
   a.k_scale = k_scale;
   return forward<false, true>(desc, q8, k8, v, doc_start, tiles, runs, num_runs, a, (hipStream_t)hip_stream);
 }
+
+namespace hsap {
+
+hsap_status partial_attn_fwd_final(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                   const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
+                                   int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots, void* o_out,
+                                   float* lse_out, hipStream_t stream) {
+  if (num_slots < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_slots < 1");
+  if (num_runs > 0 && (!o_part || !lse_part || !o_out || !lse_out)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if ((uintptr_t)o_part & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_part must be 16-byte aligned");
+  if ((uintptr_t)o_out & 7) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_out must be 8-byte aligned");
+  FwdArgs a{};
+  a.o_part = o_part;
+  a.lse_part = lse_part;
+  a.num_slots = num_slots;
+  a.o_out = (__bf16*)o_out;
+  a.lse_out = lse_out;
+  return forward<false>(desc, q, k, v, doc_start, tiles, runs, num_runs, a, stream);
+}
+
+}  // namespace hsap

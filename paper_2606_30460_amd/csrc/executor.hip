@@ -46,6 +46,7 @@ struct hsap_executor {
   std::vector<hsap_run> runs_q, runs_k, runs_all;
   std::vector<int64_t> step_offsets, pairs;
   std::vector<int32_t> slot_map;
+  std::vector<uint8_t> final_tile;  // per q-tile: 1 when its only part is written final by the partial forward
 
   // pinned staging, double-buffered; `uploaded[i]` follows the copy out of pinned[i]
   DevBuf pinned[2];
@@ -54,7 +55,7 @@ struct hsap_executor {
   int next_slot = 0;
 
   // device side
-  DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu]
+  DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu | final_tile]
   int32_t* doc_start = nullptr;
   DevBuf o_part, lse_part;
   float* delta = nullptr;
@@ -68,6 +69,7 @@ struct hsap_executor {
   const hsap_run* d_runs_k = nullptr;
   const hsap_tile* d_tiles_all = nullptr;
   const hsap_run* d_runs_all = nullptr;
+  const uint8_t* d_final_tile = nullptr;
   std::vector<uint8_t> chunk_has_tiles;
 };
 
@@ -242,8 +244,30 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   for (int32_t s = 0; s < slots; ++s)
     if (ex->slot_map[(size_t)s] >= 0) ex->chunk_has_tiles[(size_t)(s % P)] = 1;
   for (int64_t i = 0; i < RQ; ++i) ex->runs_q[(size_t)i].slot = ex->slot_map[(size_t)ex->runs_q[(size_t)i].slot];
+  // A q-tile with exactly one run holding tiles (one chunk, unsplit) has a single part: the merge
+  // would return it unchanged, so that run writes the final output and the merge skips the
+  // q-tile; the q-tile's empty runs (LSE = -inf parts nobody reads) are dropped.
+  {
+    std::vector<int32_t> busy((size_t)ex->nq, 0);
+    for (int64_t i = 0; i < RQ; ++i)
+      if (ex->runs_q[(size_t)i].count > 0) ++busy[(size_t)ex->runs_q[(size_t)i].tile];
+    ex->final_tile.assign((size_t)ex->nq, 0);
+    int64_t kept = 0;
+    for (int64_t i = 0; i < RQ; ++i) {
+      hsap_run r = ex->runs_q[(size_t)i];
+      if (busy[(size_t)r.tile] == 1) {
+        if (r.count == 0) continue;
+        r.slot = kFinalSlot;
+        ex->final_tile[(size_t)r.tile] = 1;
+      }
+      ex->runs_q[(size_t)kept++] = r;
+    }
+    RQ = kept;
+  }
   ex->info.num_runs_q = RQ;
   ex->info.num_parts = parts;
+  ex->info.final_q_tiles = 0;
+  for (uint8_t f : ex->final_tile) ex->info.final_q_tiles += f;
   ex->info.split_length = split;
   for (int32_t c = 0; c < P; ++c)
     if (ex->chunk_has_tiles[(size_t)c]) {
@@ -275,8 +299,9 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   const size_t w_tk = RK ? w_tq : 0, w_rk = words16((size_t)RK * 4);
   const size_t w_ta = RA ? w_tq : 0, w_ra = words16((size_t)RA * 4);
   const size_t w_cu = words16((size_t)num_docs + 1);
+  const size_t w_ft = words16(((size_t)ex->nq + 3) / 4);
   const size_t o_rq = w_tq, o_tk = o_rq + w_rq, o_rk = o_tk + w_tk, o_ta = o_rk + w_rk, o_ra = o_ta + w_ta,
-               o_cu = o_ra + w_ra, words = o_cu + w_cu;
+               o_cu = o_ra + w_ra, o_ft = o_cu + w_cu, words = o_ft + w_ft;
   const int slot = ex->next_slot;
   if (ex->recorded[slot]) {
     const hipError_t e = hipEventSynchronize(ex->uploaded[slot]);
@@ -297,6 +322,7 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
     std::memcpy(h + o_ra, ex->runs_all.data(), (size_t)RA * sizeof(hsap_run));
   }
   std::memcpy(h + o_cu, cu_seqlens, ((size_t)num_docs + 1) * sizeof(int32_t));
+  std::memcpy(h + o_ft, ex->final_tile.data(), (size_t)ex->nq);
   hipError_t e = hipMemcpyAsync(ex->lists.p, h, words * 4, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail("list upload", e);
   e = hipEventRecord(ex->uploaded[slot], stream);
@@ -311,6 +337,7 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   ex->d_runs_k = RK ? (const hsap_run*)(d + o_rk) : nullptr;
   ex->d_tiles_all = RA ? (const hsap_tile*)(d + o_ta) : nullptr;
   ex->d_runs_all = RA ? (const hsap_run*)(d + o_ra) : nullptr;
+  ex->d_final_tile = (const uint8_t*)(d + o_ft);
 
   // 6. start(t) for every position
   st = hsap_doc_start(d + o_cu, num_docs, ex->geom.N, ex->doc_start, hip_stream);
@@ -328,13 +355,14 @@ hsap_status hsap_executor_info(const hsap_executor* ex, hsap_exec_info* info) {
 }
 
 hsap_status hsap_executor_partial_forward(hsap_executor* ex, const void* q, const void* k, const void* v,
-                                          void* hip_stream) {
+                                          void* o_out, float* lse_out, void* hip_stream) {
   clear_error();
   if (!ex) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL executor");
   if (!ex->planned) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "executor has no plan");
-  if (!q || !k || !v) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
-  return hsap_partial_attn_fwd(&ex->desc, q, k, v, ex->doc_start, ex->d_tiles_q, ex->d_runs_q, ex->info.num_runs_q,
-                               (float*)ex->o_part.p, (float*)ex->lse_part.p, ex->info.num_parts, hip_stream);
+  if (!q || !k || !v || !o_out || !lse_out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  return partial_attn_fwd_final(&ex->desc, q, k, v, ex->doc_start, ex->d_tiles_q, ex->d_runs_q, ex->info.num_runs_q,
+                                (float*)ex->o_part.p, (float*)ex->lse_part.p, ex->info.num_parts, o_out, lse_out,
+                                (hipStream_t)hip_stream);
 }
 
 hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, void* hip_stream) {
@@ -350,8 +378,9 @@ hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, 
     o_ptrs[p] = (const float*)ex->o_part.p + (size_t)p * rows * ex->desc.head_dim;
     l_ptrs[p] = (const float*)ex->lse_part.p + (size_t)p * rows;
   }
-  return hsap_lse_merge(parts, o_ptrs, l_ptrs, ex->geom.n, ex->desc.heads_q, ex->desc.head_dim, o_out, lse_out,
-                        hip_stream);
+  if (ex->info.final_q_tiles == ex->nq) return HSAP_OK;  // every q-tile was written final
+  return lse_merge(parts, o_ptrs, l_ptrs, ex->geom.n, ex->desc.heads_q, ex->desc.head_dim, o_out, lse_out,
+                   ex->d_final_tile, ex->desc.shard.block_m, (hipStream_t)hip_stream);
 }
 
 hsap_status hsap_executor_forward(hsap_executor* ex, const void* q, const void* k, const void* v, int32_t fused,
@@ -365,7 +394,7 @@ hsap_status hsap_executor_forward(hsap_executor* ex, const void* q, const void* 
     return hsap_attn_fwd_fused(&ex->desc, q, k, v, ex->doc_start, ex->d_tiles_all, ex->d_runs_all,
                                ex->info.num_runs_all, o_out, lse_out, hip_stream);
   }
-  const hsap_status st = hsap_executor_partial_forward(ex, q, k, v, hip_stream);
+  const hsap_status st = hsap_executor_partial_forward(ex, q, k, v, o_out, lse_out, hip_stream);
   if (st != HSAP_OK) return st;
   return hsap_executor_merge(ex, o_out, lse_out, hip_stream);
 }

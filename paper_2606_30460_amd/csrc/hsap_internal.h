@@ -70,6 +70,20 @@ hsap_status check_attn(const hsap_attn_desc* d, Geom* g);
 // Writes `bytes` zero bytes at dst on `stream` with a kernel (bytes a multiple
 // of 4, dst 16-byte aligned).
 hsap_status zero_fill(void* dst, int64_t bytes, hipStream_t stream);
+
+// hsap_lse_merge with an optional per-q-tile skip flag (skip[row / block_m] != 0: the rows are
+// already final and are neither read nor written).
+hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const float* const* lse_parts, int64_t n,
+                      int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, const uint8_t* skip,
+                      int32_t block_m, hipStream_t stream);
+
+// hsap_partial_attn_fwd where runs whose slot is kFinalSlot write the final bf16 O and LSE of
+// their q-tile to o_out / lse_out (the q-tile's only part: nothing to merge).
+constexpr int32_t kFinalSlot = -2;
+hsap_status partial_attn_fwd_final(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                   const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
+                                   int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots, void* o_out,
+                                   float* lse_out, hipStream_t stream);
 #endif
 
 }  // namespace hsap

@@ -25,6 +25,8 @@ struct MergeArgs {
   int64_t n;
   __bf16* o_out;
   float* lse_out;
+  const uint8_t* skip;  // per BM-row q-tile: 1 = rows already final, not merged (NULL: merge every row)
+  int32_t bm;
 };
 
 // Few parts (num_parts <= PR): one wave merges one head's 16 consecutive rows.
@@ -52,22 +54,24 @@ __global__ __launch_bounds__(256) void lse_merge_few_kernel(MergeArgs a) {
   for (int64_t grp = wave0; grp < groups; grp += waves) {
     const int64_t h = grp / groups_per_head;
     const int64_t r0 = (grp - h * groups_per_head) * 16;
-    // LSE of row r0 + (lane & 15) for every part
+    if (a.skip && a.skip[r0 / a.bm]) continue;  // a 16-row group never straddles q-tiles (BM % 16 == 0)
+    // LSE of row r0 + (lane & 15) for every part; max and result in natural-log units, only
+    // differences scaled to log2 units, so a row with one finite part keeps its LSE exactly
     const int64_t my_row = r0 + (lane & 15);
     const bool row_ok = my_row < a.n;
     float l[PR];
 #pragma unroll
-    for (int p = 0; p < PR; ++p) l[p] = (p < a.num_parts && row_ok) ? a.lse[p][h * a.n + my_row] * LOG2E : NEG_INF;
+    for (int p = 0; p < PR; ++p) l[p] = (p < a.num_parts && row_ok) ? a.lse[p][h * a.n + my_row] : NEG_INF;
     float mx = l[0];
 #pragma unroll
     for (int p = 1; p < PR; ++p) mx = fmaxf(mx, l[p]);
     float sum = 0.f;
 #pragma unroll
-    for (int p = 0; p < PR; ++p) sum += l[p] == NEG_INF ? 0.f : fast_exp2(l[p] - mx);
-    const float L2 = mx == NEG_INF ? NEG_INF : mx + __log2f(sum);
+    for (int p = 0; p < PR; ++p) sum += l[p] == NEG_INF ? 0.f : fast_exp2((l[p] - mx) * LOG2E);
+    const float Lm = mx == NEG_INF ? NEG_INF : mx + __log2f(sum) * LN2;
     float wl[PR];
 #pragma unroll
-    for (int p = 0; p < PR; ++p) wl[p] = l[p] == NEG_INF ? 0.f : fast_exp2(l[p] - L2);
+    for (int p = 0; p < PR; ++p) wl[p] = l[p] == NEG_INF ? 0.f : fast_exp2((l[p] - Lm) * LOG2E);
     // O rows: instruction k covers rows r0 + RPI * k + sub
 #pragma unroll
     for (int k = 0; k < STEPS; ++k) {
@@ -88,7 +92,7 @@ __global__ __launch_bounds__(256) void lse_merge_few_kernel(MergeArgs a) {
       const bf16x4 out{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
       *(bf16x4*)(a.o_out + (row * a.hq + h) * D + d0) = out;
     }
-    if (lane < 16 && row_ok) a.lse_out[h * a.n + my_row] = L2 == NEG_INF ? NEG_INF : L2 * LN2;
+    if (lane < 16 && row_ok) a.lse_out[h * a.n + my_row] = Lm;
   }
 }
 
@@ -111,11 +115,11 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
 #pragma unroll
   for (int it = 0; it < ITEMS; ++it) {
     rh[it] = base + it * stride;  // rh = row * hq + head
-    live[it] = rh[it] < items;
     const int64_t row = rh[it] / a.hq;
+    live[it] = rh[it] < items && !(a.skip && a.skip[row / a.bm]);
     li[it] = (int64_t)(rh[it] - row * a.hq) * a.n + row;  // index into [Hq, n]
   }
-  // pass 1: running max and sum of 2^(LSE*log2e) over the parts (log2 domain)
+  // pass 1: running max (natural-log units) and sum of exp(LSE - max) over the parts
   float mx[ITEMS], sum[ITEMS];
 #pragma unroll
   for (int it = 0; it < ITEMS; ++it) {
@@ -125,17 +129,18 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
   for (int p = 0; p < a.num_parts; ++p) {
     float l[ITEMS];
 #pragma unroll
-    for (int it = 0; it < ITEMS; ++it) l[it] = live[it] ? a.lse[p][li[it]] * LOG2E : NEG_INF;
+    for (int it = 0; it < ITEMS; ++it) l[it] = live[it] ? a.lse[p][li[it]] : NEG_INF;
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const float m_new = fmaxf(mx[it], l[it]);
-      if (m_new != NEG_INF) sum[it] = sum[it] * fast_exp2(mx[it] - m_new) + fast_exp2(l[it] - m_new);
+      if (m_new != NEG_INF)
+        sum[it] = sum[it] * fast_exp2((mx[it] - m_new) * LOG2E) + fast_exp2((l[it] - m_new) * LOG2E);
       mx[it] = m_new;
     }
   }
-  float L2[ITEMS];  // merged LSE in log2 units
+  float Lm[ITEMS];  // merged LSE
 #pragma unroll
-  for (int it = 0; it < ITEMS; ++it) L2[it] = mx[it] == NEG_INF ? NEG_INF : mx[it] + __log2f(sum[it]);
+  for (int it = 0; it < ITEMS; ++it) Lm[it] = mx[it] == NEG_INF ? NEG_INF : mx[it] + __log2f(sum[it]) * LN2;
   // pass 2: weighted sum of the finite parts
   f32x4 acc[ITEMS];
 #pragma unroll
@@ -145,8 +150,8 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
     f32x4 x[ITEMS];
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
-      const float l = live[it] ? a.lse[p][li[it]] * LOG2E : NEG_INF;
-      wgt[it] = l == NEG_INF ? 0.f : fast_exp2(l - L2[it]);
+      const float l = live[it] ? a.lse[p][li[it]] : NEG_INF;
+      wgt[it] = l == NEG_INF ? 0.f : fast_exp2((l - Lm[it]) * LOG2E);
       x[it] = wgt[it] > 0.f ? *(const f32x4*)(a.o[p] + rh[it] * D + 4 * part) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
@@ -157,7 +162,7 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
     if (!live[it]) continue;
     const bf16x4 out{(__bf16)acc[it][0], (__bf16)acc[it][1], (__bf16)acc[it][2], (__bf16)acc[it][3]};
     *(bf16x4*)(a.o_out + rh[it] * D + 4 * part) = out;
-    if (part == 0) a.lse_out[li[it]] = L2[it] == NEG_INF ? NEG_INF : L2[it] * LN2;
+    if (part == 0) a.lse_out[li[it]] = Lm[it];
   }
 }
 
@@ -361,6 +366,17 @@ extern "C" {
 hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const float* const* lse_parts, int64_t n,
                            int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, void* hip_stream) {
   clear_error();
+  return lse_merge(num_parts, o_parts, lse_parts, n, heads_q, head_dim, o_out, lse_out, nullptr, 1,
+                   (hipStream_t)hip_stream);
+}
+
+}  // extern "C"
+
+namespace hsap {
+
+hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const float* const* lse_parts, int64_t n,
+                      int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, const uint8_t* skip,
+                      int32_t block_m, hipStream_t s) {
   if (num_parts < 1 || num_parts > HSAP_MAX_MERGE_PARTS)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_parts %d outside 1..%d", num_parts, HSAP_MAX_MERGE_PARTS);
   if (!o_parts || !lse_parts || !o_out || !lse_out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
@@ -380,7 +396,9 @@ hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const
   a.n = n;
   a.o_out = (__bf16*)o_out;
   a.lse_out = lse_out;
-  hipStream_t s = (hipStream_t)hip_stream;
+  if (skip && (block_m < 16 || block_m % 16)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "skip flags need BM a multiple of 16");
+  a.skip = skip;
+  a.bm = skip ? block_m : 1;
   const dim3 block(256);
   if (num_parts <= 4) {
     // one wave per (head, 16 rows) group, four waves per block, grid-stride beyond 65536 blocks
@@ -404,6 +422,10 @@ hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const
   }
   return check_launch("lse_merge");
 }
+
+}  // namespace hsap
+
+extern "C" {
 
 hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, int32_t heads_q, int32_t head_dim,
                                      float* delta, void* hip_stream) {

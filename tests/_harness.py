@@ -99,7 +99,7 @@ class Case:
             of, lsef = torch.full_like(o, float("nan")), torch.full_like(lse, float("nan"))
             ex.forward(q_sh, k_sh, v_sh, of, lsef, fused=True)
             os_, lses = torch.full_like(o, float("nan")), torch.full_like(lse, float("nan"))
-            ex.partial_forward(q_sh, k_sh, v_sh)     # the same forward as two stage calls
+            ex.partial_forward(q_sh, k_sh, v_sh, os_, lses)     # the same forward as two stage calls
             ex.merge(os_, lses)
             out = {"info": ex.info(), "o": o.float().cpu().numpy(), "lse": lse.cpu().numpy(),
                    "o_fused": of.float().cpu().numpy(), "lse_fused": lsef.cpu().numpy(),

@@ -267,5 +267,5 @@ def test_executor_validates_before_touching_the_device():
     assert lib.hsap_executor_forward(None, 1, 1, 1, 0, 1, 1, None) == L.HSAP_ERR_INVALID_ARG
     assert lib.hsap_executor_backward(None, 1, 1, 1, 1, 1, 1, 1, 1, 1, None) == L.HSAP_ERR_INVALID_ARG
     lib.hsap_executor_destroy(None)                          # no-op
-    assert lib.hsap_executor_partial_forward(None, 1, 1, 1, None) == L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_executor_partial_forward(None, 1, 1, 1, 1, 1, None) == L.HSAP_ERR_INVALID_ARG
     assert lib.hsap_executor_merge(None, 1, 1, None) == L.HSAP_ERR_INVALID_ARG
