@@ -565,9 +565,8 @@ void hsap_executor_destroy(hsap_executor* ex);
  * hsap_executor_plan -- plan one packed batch: hsap_plan, hsap_plan_runs for
  * the q-major runs (partial slots renumbered densely 0..num_parts-1 in
  * increasing original slot order) and, per the options, the k-major and
- * MAJOR_Q_ALL runs, and the document start of each of the shard's rows (the
- * only starts the kernels read); then one asynchronous upload of all of it
- * from a pinned staging buffer on `stream` (no per-step start kernel).
+ * MAJOR_Q_ALL runs; then one asynchronous upload of every list and
+ * cu_seqlens from a pinned staging buffer, and hsap_doc_start, on `stream`.
  * The host blocks only while the staging buffer it is about to reuse is
  * still being uploaded (two plans in flight).
  *   cu_seqlens  host int32 [num_docs + 1] for the executor's N (rules of

@@ -34,8 +34,7 @@ struct BwdArgs {
   const __bf16* d_o;
   const float* lse;
   const float* delta;
-  const int32_t* doc_start;  // document starts by global position, or by the shard's local row (start_by_row)
-  int32_t start_by_row;
+  const int32_t* doc_start;
   const hsap_tile* tiles;
   const hsap_run* runs;
   float* dq;       // fp32 accumulators (+=), or
@@ -177,7 +176,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
     if (tid < SUB) {
       lreg = a.lse[(int64_t)h * n + q0 + tid];
       dreg = a.delta[(int64_t)h * n + q0 + tid];
-      sreg = a.doc_start[(a.start_by_row ? q0 : global_pos(a.geom, a.shard, q0)) + tid];
+      sreg = a.doc_start[global_pos(a.geom, a.shard, q0) + tid];
     }
   };
   auto store_sub = [&](int buf) {
@@ -336,7 +335,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
     return;
   }
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
-  const int32_t qstart = a.doc_start[a.start_by_row ? qrow : (int64_t)gq];
+  const int32_t qstart = a.doc_start[gq];
   const uint32_t span = (uint32_t)(gq - qstart);
   const float lse_raw = a.lse[(int64_t)h * n + qrow];
   const float lse2 = lse_raw == NEG_INF ? __builtin_inff() : lse_raw * LOG2E;  // no key: P = 0
@@ -492,7 +491,7 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
                             const float* lse, const float* delta, const int32_t* doc_start, const hsap_tile* tiles_k,
                             const hsap_run* runs_k, int64_t num_runs_k, const hsap_tile* tiles_q,
                             const hsap_run* runs_q, int64_t num_runs_q, void* dq, void* dk, void* dv,
-                            hipStream_t s, bool start_by_row = false) {
+                            hipStream_t s) {
   Geom geom;
   hsap_status st = check_attn(desc, &geom);
   if (st != HSAP_OK) return st;
@@ -520,7 +519,6 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
   a.lse = lse;
   a.delta = delta;
   a.doc_start = doc_start;
-  a.start_by_row = start_by_row ? 1 : 0;
   if (BF16OUT) {
     a.dq16 = (__bf16*)dq;
     a.dk16 = (__bf16*)dk;
@@ -588,16 +586,3 @@ extern "C" hsap_status hsap_attn_bwd_bf16(const hsap_attn_desc* desc, const void
   return backward<true>(desc, q, k, v, d_o, lse, delta, doc_start, tiles_k, runs_k, num_runs_k, tiles_q, runs_q,
                         num_runs_q, dq, dk, dv, (hipStream_t)hip_stream);
 }
-
-namespace hsap {
-
-hsap_status attn_bwd_bf16_rows(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
-                               const void* d_o, const float* lse, const float* delta, const int32_t* row_start,
-                               const hsap_tile* tiles_k, const hsap_run* runs_k, int64_t num_runs_k,
-                               const hsap_tile* tiles_q, const hsap_run* runs_q, int64_t num_runs_q, void* dq,
-                               void* dk, void* dv, hipStream_t stream) {
-  return backward<true>(desc, q, k, v, d_o, lse, delta, row_start, tiles_k, runs_k, num_runs_k, tiles_q, runs_q,
-                        num_runs_q, dq, dk, dv, stream, true);
-}
-
-}  // namespace hsap

@@ -37,8 +37,7 @@ struct FwdArgs {
   const __bf16* q;
   const __bf16* k;
   const __bf16* v;
-  const int32_t* doc_start;  // document starts by global position, or by the shard's local row (start_by_row)
-  int32_t start_by_row;
+  const int32_t* doc_start;
   const hsap_tile* tiles;
   const hsap_run* runs;
   float* o_part;
@@ -106,7 +105,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   }
 
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
-  const int32_t qstart = a.doc_start[a.start_by_row ? qrow : (int64_t)gq];
+  const int32_t qstart = a.doc_start[gq];
   const uint32_t span = (uint32_t)(gq - qstart);  // key j is allowed iff 0 <= j - start <= span
   bf16x8 qf[D / 16];
   i32x8 qf8[2];  // fp8: lane half hi holds bytes 64 kk + 32 hi .. +31 of its query's row
@@ -371,7 +370,7 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   }
 
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
-  const int32_t qstart = a.doc_start[a.start_by_row ? qrow : (int64_t)gq];
+  const int32_t qstart = a.doc_start[gq];
   const uint32_t span = (uint32_t)(gq - qstart);
   bf16x8 qf[D / 16];
   {
@@ -711,7 +710,7 @@ extern "C" hsap_status hsap_partial_attn_fwd_fp8(const hsap_attn_desc* desc, con
 namespace hsap {
 
 hsap_status partial_attn_fwd_final(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
-                                   const int32_t* row_start, const hsap_tile* tiles, const hsap_run* runs,
+                                   const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
                                    int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots, void* o_out,
                                    float* lse_out, hipStream_t stream) {
   if (num_slots < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_slots < 1");
@@ -724,21 +723,7 @@ hsap_status partial_attn_fwd_final(const hsap_attn_desc* desc, const void* q, co
   a.num_slots = num_slots;
   a.o_out = (__bf16*)o_out;
   a.lse_out = lse_out;
-  a.start_by_row = 1;
-  return forward<false>(desc, q, k, v, row_start, tiles, runs, num_runs, a, stream);
-}
-
-hsap_status attn_fwd_fused_rows(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
-                                const int32_t* row_start, const hsap_tile* tiles, const hsap_run* runs,
-                                int64_t num_runs, void* o_out, float* lse_out, hipStream_t stream) {
-  if (num_runs > 0 && (!o_out || !lse_out)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
-  if ((uintptr_t)o_out & 7) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_out must be 8-byte aligned");
-  FwdArgs a{};
-  a.o_out = (__bf16*)o_out;
-  a.lse_out = lse_out;
-  a.num_slots = 1;
-  a.start_by_row = 1;
-  return forward<true>(desc, q, k, v, row_start, tiles, runs, num_runs, a, stream);
+  return forward<false>(desc, q, k, v, doc_start, tiles, runs, num_runs, a, stream);
 }
 
 }  // namespace hsap

@@ -47,7 +47,6 @@ struct hsap_executor {
   std::vector<int64_t> step_offsets, pairs;
   std::vector<int32_t> slot_map;
   std::vector<uint8_t> final_tile;  // per q-tile: 1 when its only part is written final by the partial forward
-  std::vector<int32_t> row_start;   // document start of each of the shard's local rows
 
   // pinned staging, double-buffered; `uploaded[i]` follows the copy out of pinned[i]
   DevBuf pinned[2];
@@ -56,7 +55,8 @@ struct hsap_executor {
   int next_slot = 0;
 
   // device side
-  DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | row_start | final_tile]
+  DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu | final_tile]
+  int32_t* doc_start = nullptr;
   DevBuf o_part, lse_part;
   float* delta = nullptr;
 
@@ -70,7 +70,6 @@ struct hsap_executor {
   const hsap_tile* d_tiles_all = nullptr;
   const hsap_run* d_runs_all = nullptr;
   const uint8_t* d_final_tile = nullptr;
-  const int32_t* d_row_start = nullptr;
   std::vector<uint8_t> chunk_has_tiles;
 };
 
@@ -119,7 +118,7 @@ void release(hsap_executor* ex) {
     if (ex->pinned[i].p) hipHostFree(ex->pinned[i].p);
     if (ex->uploaded[i]) hipEventDestroy(ex->uploaded[i]);
   }
-  void* dev[] = {ex->lists.p, ex->o_part.p, ex->lse_part.p, ex->delta};
+  void* dev[] = {ex->lists.p, ex->doc_start, ex->o_part.p, ex->lse_part.p, ex->delta};
   for (void* p : dev)
     if (p) hipFree(p);
   delete ex;
@@ -173,6 +172,7 @@ hsap_status hsap_executor_create(const hsap_attn_desc* desc, int32_t options, in
   hipError_t e = hipGetDevice(&ex->device);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ex->device);
   for (int i = 0; e == hipSuccess && i < 2; ++i) e = hipEventCreateWithFlags(&ex->uploaded[i], hipEventDisableTiming);
+  if (e == hipSuccess) e = hipMalloc((void**)&ex->doc_start, (size_t)g.N * sizeof(int32_t));
   if (e == hipSuccess && (options & HSAP_EXEC_BACKWARD))
     e = hipMalloc((void**)&ex->delta, (size_t)g.n * desc->heads_q * sizeof(float));
   if (e != hipSuccess) {
@@ -294,28 +294,14 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   if (st == HSAP_OK) st = grow_device(ex->lse_part, (size_t)parts * part_rows * sizeof(float), stream);
   if (st != HSAP_OK) return st;
 
-  // 5. the document start of each local row (the kernels read starts only of the shard's own queries)
-  {
-    const int64_t n = ex->geom.n;
-    ex->row_start.resize((size_t)n);
-    int64_t doc = 0;
-    for (int64_t l = 0; l < n; ++l) {
-      const int64_t p = global_pos(ex->geom, sd.shard_id, l);
-      if (l == 0 || p < cu_seqlens[doc])  // positions rise within a piece; re-search at piece starts
-        doc = (int64_t)(std::upper_bound(cu_seqlens, cu_seqlens + num_docs + 1, (int32_t)p) - cu_seqlens) - 1;
-      while (cu_seqlens[doc + 1] <= p) ++doc;
-      ex->row_start[(size_t)l] = cu_seqlens[doc];
-    }
-  }
-
-  // 6. one staging buffer, one upload
+  // 5. one staging buffer, one upload
   const size_t w_tq = words16((size_t)T * 4), w_rq = words16((size_t)RQ * 4);
   const size_t w_tk = RK ? w_tq : 0, w_rk = words16((size_t)RK * 4);
   const size_t w_ta = RA ? w_tq : 0, w_ra = words16((size_t)RA * 4);
-  const size_t w_rs = words16((size_t)ex->geom.n);
+  const size_t w_cu = words16((size_t)num_docs + 1);
   const size_t w_ft = words16(((size_t)ex->nq + 3) / 4);
   const size_t o_rq = w_tq, o_tk = o_rq + w_rq, o_rk = o_tk + w_tk, o_ta = o_rk + w_rk, o_ra = o_ta + w_ta,
-               o_rs = o_ra + w_ra, o_ft = o_rs + w_rs, words = o_ft + w_ft;
+               o_cu = o_ra + w_ra, o_ft = o_cu + w_cu, words = o_ft + w_ft;
   const int slot = ex->next_slot;
   if (ex->recorded[slot]) {
     const hipError_t e = hipEventSynchronize(ex->uploaded[slot]);
@@ -335,7 +321,7 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
     std::memcpy(h + o_ta, ex->sorted_all.data(), (size_t)T * sizeof(hsap_tile));
     std::memcpy(h + o_ra, ex->runs_all.data(), (size_t)RA * sizeof(hsap_run));
   }
-  std::memcpy(h + o_rs, ex->row_start.data(), (size_t)ex->geom.n * sizeof(int32_t));
+  std::memcpy(h + o_cu, cu_seqlens, ((size_t)num_docs + 1) * sizeof(int32_t));
   std::memcpy(h + o_ft, ex->final_tile.data(), (size_t)ex->nq);
   hipError_t e = hipMemcpyAsync(ex->lists.p, h, words * 4, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail("list upload", e);
@@ -352,7 +338,10 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   ex->d_tiles_all = RA ? (const hsap_tile*)(d + o_ta) : nullptr;
   ex->d_runs_all = RA ? (const hsap_run*)(d + o_ra) : nullptr;
   ex->d_final_tile = (const uint8_t*)(d + o_ft);
-  ex->d_row_start = d + o_rs;
+
+  // 6. start(t) for every position
+  st = hsap_doc_start(d + o_cu, num_docs, ex->geom.N, ex->doc_start, hip_stream);
+  if (st != HSAP_OK) return st;
   ex->planned = true;
   return HSAP_OK;
 }
@@ -371,7 +360,7 @@ hsap_status hsap_executor_partial_forward(hsap_executor* ex, const void* q, cons
   if (!ex) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL executor");
   if (!ex->planned) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "executor has no plan");
   if (!q || !k || !v || !o_out || !lse_out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
-  return partial_attn_fwd_final(&ex->desc, q, k, v, ex->d_row_start, ex->d_tiles_q, ex->d_runs_q, ex->info.num_runs_q,
+  return partial_attn_fwd_final(&ex->desc, q, k, v, ex->doc_start, ex->d_tiles_q, ex->d_runs_q, ex->info.num_runs_q,
                                 (float*)ex->o_part.p, (float*)ex->lse_part.p, ex->info.num_parts, o_out, lse_out,
                                 (hipStream_t)hip_stream);
 }
@@ -402,8 +391,8 @@ hsap_status hsap_executor_forward(hsap_executor* ex, const void* q, const void* 
   if (!q || !k || !v || !o_out || !lse_out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if (fused) {
     if (!(ex->options & HSAP_EXEC_FUSED)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "fused forward needs HSAP_EXEC_FUSED");
-    return attn_fwd_fused_rows(&ex->desc, q, k, v, ex->d_row_start, ex->d_tiles_all, ex->d_runs_all,
-                               ex->info.num_runs_all, o_out, lse_out, (hipStream_t)hip_stream);
+    return hsap_attn_fwd_fused(&ex->desc, q, k, v, ex->doc_start, ex->d_tiles_all, ex->d_runs_all,
+                               ex->info.num_runs_all, o_out, lse_out, hip_stream);
   }
   const hsap_status st = hsap_executor_partial_forward(ex, q, k, v, o_out, lse_out, hip_stream);
   if (st != HSAP_OK) return st;
@@ -430,9 +419,9 @@ hsap_status hsap_executor_backward(hsap_executor* ex, const void* q, const void*
     }
   if (st == HSAP_OK) st = hsap_attn_bwd_preprocess(o, d_o, n, (int32_t)hq, (int32_t)d, ex->delta, hip_stream);
   if (st == HSAP_OK)
-    st = attn_bwd_bf16_rows(&ex->desc, q, k, v, d_o, lse, ex->delta, ex->d_row_start, ex->d_tiles_k, ex->d_runs_k,
+    st = hsap_attn_bwd_bf16(&ex->desc, q, k, v, d_o, lse, ex->delta, ex->doc_start, ex->d_tiles_k, ex->d_runs_k,
                             ex->info.num_runs_k, ex->d_tiles_all, ex->d_runs_all, ex->info.num_runs_all, dq, dk, dv,
-                            (hipStream_t)hip_stream);
+                            hip_stream);
   return st;
 }
 

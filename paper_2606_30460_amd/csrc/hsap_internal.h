@@ -77,27 +77,13 @@ hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const floa
                       int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, const uint8_t* skip,
                       int32_t block_m, hipStream_t stream);
 
-// The executor's variants of the entry points.  `row_start` holds the document start of each
-// of the shard's local rows (instead of hsap_doc_start's array over every position), so no
-// per-step kernel has to build it.
-//
 // hsap_partial_attn_fwd where runs whose slot is kFinalSlot write the final bf16 O and LSE of
 // their q-tile to o_out / lse_out (the q-tile's only part: nothing to merge).
 constexpr int32_t kFinalSlot = -2;
 hsap_status partial_attn_fwd_final(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
-                                   const int32_t* row_start, const hsap_tile* tiles, const hsap_run* runs,
+                                   const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
                                    int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots, void* o_out,
                                    float* lse_out, hipStream_t stream);
-// hsap_attn_fwd_fused with starts by local row.
-hsap_status attn_fwd_fused_rows(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
-                                const int32_t* row_start, const hsap_tile* tiles, const hsap_run* runs,
-                                int64_t num_runs, void* o_out, float* lse_out, hipStream_t stream);
-// hsap_attn_bwd_bf16 with starts by local row.
-hsap_status attn_bwd_bf16_rows(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
-                               const void* d_o, const float* lse, const float* delta, const int32_t* row_start,
-                               const hsap_tile* tiles_k, const hsap_run* runs_k, int64_t num_runs_k,
-                               const hsap_tile* tiles_q, const hsap_run* runs_q, int64_t num_runs_q, void* dq,
-                               void* dk, void* dv, hipStream_t stream);
 #endif
 
 }  // namespace hsap
