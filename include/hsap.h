@@ -507,9 +507,12 @@ hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, vo
  * its kernels.
  *
  * An executor owns: two pinned staging buffers for the planner's lists, one
- * device list buffer, the device doc_start array, the fp32 partial outputs
- * of the forward (grown to the largest plan seen) and, with
- * HSAP_EXEC_BACKWARD, the backward's delta.  Buffers grow on demand; a
+ * device list buffer, the fp32 partial outputs of the forward (grown to the
+ * largest plan seen) and, with HSAP_EXEC_BACKWARD, the device doc_start
+ * array and the backward's delta.  The forwards take document starts from
+ * the uploaded cu_seqlens: each wave finds the document of its first query
+ * by binary search and scans the boundaries among its 32 queries, so a
+ * forward-only step runs no hsap_doc_start.  Buffers grow on demand; a
  * growth synchronises the stream first.
  *
  * Threading and streams: one executor is used by one host thread at a time,
@@ -566,7 +569,8 @@ void hsap_executor_destroy(hsap_executor* ex);
  * the q-major runs (partial slots renumbered densely 0..num_parts-1 in
  * increasing original slot order) and, per the options, the k-major and
  * MAJOR_Q_ALL runs; then one asynchronous upload of every list and
- * cu_seqlens from a pinned staging buffer, and hsap_doc_start, on `stream`.
+ * cu_seqlens from a pinned staging buffer, and (HSAP_EXEC_BACKWARD only)
+ * hsap_doc_start, on `stream`.
  * The host blocks only while the staging buffer it is about to reuse is
  * still being uploaded (two plans in flight).
  *   cu_seqlens  host int32 [num_docs + 1] for the executor's N (rules of

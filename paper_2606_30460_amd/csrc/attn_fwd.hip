@@ -47,6 +47,8 @@ struct FwdArgs {
   float* lse_out;   // fused forward: final LSE [Hq, n]
   const float* q_scale;  // fp8 scores: dequantisation scale per query head [Hq]
   const float* k_scale;  // fp8 scores: dequantisation scale per (chunk, K/V head) [P, Hkv]
+  const int32_t* cu;     // when set: cumulative document lengths [num_docs + 1], used instead of doc_start
+  int32_t num_docs;
   Geom geom;
   int32_t shard;
   int32_t hq;
@@ -54,6 +56,61 @@ struct FwdArgs {
   int32_t group;
   float scale_log2;
 };
+
+// Document start of this lane's query (global position gq), in two parts so the memory access
+// is issued at kernel start and consumed after the prologue.  With per-position starts it is one
+// load.  From the cumulative lengths instead: a wave's 32 queries (lanes 0..31; lane l ^ 32 holds
+// the query of lane l) are 32 consecutive positions -- every piece of a shard is a multiple of
+// the 64-, 128- or 256-row q-tile -- so at most 31 document boundaries lie after the document of
+// lane 0's position g_lo, up to lane 31's position g_hi.  The wave loads 64 consecutive entries
+// of cu_seqlens, starting at most 31 entries before the document of g_lo (a 64-way search in
+// rounds narrows the start when there are more than 32 entries), and each lane takes the largest
+// entry not above its position with ballots and lane reads: no further memory access.
+struct DocWindow {
+  int32_t w;           // cu[base + lane], or this lane's start when per-position starts are given
+  int32_t g_lo, g_hi;  // positions of the wave's first and last query
+};
+
+__device__ __forceinline__ DocWindow doc_window(const FwdArgs& a, int32_t gq, int lane) {
+  DocWindow r{};
+  if (!a.cu) {
+    r.w = a.doc_start[gq];
+    return r;
+  }
+  r.g_lo = __builtin_amdgcn_readlane(gq, 0);
+  r.g_hi = __builtin_amdgcn_readlane(gq, 31);
+  const int32_t nd = a.num_docs;
+  int32_t base = 0, len = nd + 1;  // the document of g_lo is one of base .. base + len - 1
+  while (len > 32) {
+    const int32_t stride = (len + 63) >> 6;
+    const int32_t v = a.cu[min(base + lane * stride, nd)];
+    base += stride * (__popcll(__builtin_amdgcn_ballot_w64(v <= r.g_lo)) - 1);
+    len = stride;
+  }
+  r.w = a.cu[min(base + lane, nd)];
+  return r;
+}
+
+__device__ __forceinline__ int32_t doc_window_start(const FwdArgs& a, const DocWindow& r, int32_t gq) {
+  if (!a.cu) return r.w;
+  const int32_t lo = __popcll(__builtin_amdgcn_ballot_w64(r.w <= r.g_lo)) - 1;    // document of g_lo
+  const int32_t last = __popcll(__builtin_amdgcn_ballot_w64(r.w <= r.g_hi)) - 1;  // last boundary <= g_hi
+  int32_t start = __builtin_amdgcn_readlane(r.w, lo);
+  if (last >= 63) {  // more boundaries than the window holds (not reachable with validated shapes)
+    int32_t l = 0, h = a.num_docs;
+    while (h - l > 1) {
+      const int32_t mid = (l + h) >> 1;
+      if (a.cu[mid] <= gq) l = mid;
+      else h = mid;
+    }
+    return a.cu[l];
+  }
+  for (int32_t j = lo + 1; j <= last; ++j) {
+    const int32_t b = __builtin_amdgcn_readlane(r.w, j);
+    if (gq >= b) start = b;
+  }
+  return start;
+}
 
 // FP8: Q and K are e4m3 codes (scores S = (Q8 K8^T) * q_scale[h] * k_scale[chunk, g]
 // from the 32x32x64 fp8 MFMA, a K row held as 128 bytes), V and the rest as in bf16.
@@ -105,8 +162,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   }
 
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
-  const int32_t qstart = a.doc_start[gq];
-  const uint32_t span = (uint32_t)(gq - qstart);  // key j is allowed iff 0 <= j - start <= span
+  const DocWindow docw = doc_window(a, gq, lane);
   bf16x8 qf[D / 16];
   i32x8 qf8[2];  // fp8: lane half hi holds bytes 64 kk + 32 hi .. +31 of its query's row
   if constexpr (FP8) {
@@ -135,40 +191,47 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     return run_base + step_row0(t, s) * rstride;
   };
 
-  // staging: thread t moves chunks t, t + NT, ... of a step's [KB][D] tile
-  int32_t goff[PER_T], voff[PER_T], kgoff[PER_TK], koff[PER_TK];
-#pragma unroll
-  for (int i = 0; i < PER_T; ++i) {
-    const int idx = tid + i * NT, row = idx / (D / 8), cc = idx % (D / 8);
-    goff[i] = (int32_t)(row * rstride + cc * 8);
-    voff[i] = row * VS + cc * 8;
-  }
-#pragma unroll
-  for (int i = 0; i < PER_TK; ++i) {
-    const int idx = tid + i * NT, row = idx / KCPR, cc = idx % KCPR;
-    constexpr int EPC = 16 / (int)sizeof(KT);  // K elements per 16-byte chunk
-    kgoff[i] = (int32_t)(row * rstride + cc * EPC);
-    koff[i] = row * KS + cc * EPC;
-  }
+  // staging: thread t moves chunks t, t + NT, ... of a step's [KB][D] tile, i.e. one column chunk
+  // of rows r0, r0 + ROWS, r0 + 2 ROWS, ...  The distance between a thread's chunks is the same
+  // for every thread, so one 32-bit byte offset per thread serves all of them: the row distance
+  // goes into the (uniform) base pointer of each global load and into the immediate offset of
+  // each LDS store.
+  constexpr int EPC = 16 / (int)sizeof(KT);  // K elements per 16-byte chunk
+  constexpr int VROWS = NT / (D / 8), KROWS = NT / KCPR;
+  static_assert(NT % (D / 8) == 0 && NT % KCPR == 0, "a thread's chunks must share their column");
+  const uint32_t gvo = (uint32_t)(((tid / (D / 8)) * rstride + (tid % (D / 8)) * 8) * 2);
+  const uint32_t gko = (uint32_t)(((tid / KCPR) * rstride + (tid % KCPR) * EPC) * (int)sizeof(KT));
+  const int lvo = (tid / (D / 8)) * VS + (tid % (D / 8)) * 8;
+  const int lko = (tid / KCPR) * KS + (tid % KCPR) * EPC;
   K16 kreg[PER_TK];
   bf16x8 vreg[PER_T];
+  // (the empty asm, which touches no memory, keeps each load's 32-bit offset at its use: hoisted
+  // out of the loop, or shared by the loads, it becomes a 64-bit address computed per load)
   auto load_k = [&](int64_t off) {
-    const KT* src = (const KT*)a.k + off;
+    const char* src = (const char*)((const KT*)a.k + off);
 #pragma unroll
-    for (int i = 0; i < PER_TK; ++i) kreg[i] = *(const K16*)(src + kgoff[i]);
+    for (int i = 0; i < PER_TK; ++i) {
+      uint32_t o;
+      asm("" : "=v"(o) : "0"(gko), "s"(off), "n"(i));
+      kreg[i] = *(const K16*)(src + (int64_t)i * KROWS * rstride * (int)sizeof(KT) + o);
+    }
   };
   auto load_v = [&](int64_t off) {
-    const __bf16* src = a.v + off;
+    const char* src = (const char*)(a.v + off);
 #pragma unroll
-    for (int i = 0; i < PER_T; ++i) vreg[i] = *(const bf16x8*)(src + goff[i]);
+    for (int i = 0; i < PER_T; ++i) {
+      uint32_t o;
+      asm("" : "=v"(o) : "0"(gvo), "s"(off), "n"(i));
+      vreg[i] = *(const bf16x8*)(src + (int64_t)i * VROWS * rstride * 2 + o);
+    }
   };
   auto store_k = [&](int slot) {
 #pragma unroll
-    for (int i = 0; i < PER_TK; ++i) *(K16*)(&Ks[slot][koff[i]]) = kreg[i];
+    for (int i = 0; i < PER_TK; ++i) *(K16*)(&Ks[slot][lko + i * KROWS * KS]) = kreg[i];
   };
   auto store_v = [&](int slot) {
 #pragma unroll
-    for (int i = 0; i < PER_T; ++i) *(bf16x8*)(&Vs[slot][voff[i]]) = vreg[i];
+    for (int i = 0; i < PER_T; ++i) *(bf16x8*)(&Vs[slot][lvo + i * VROWS * VS]) = vreg[i];
   };
   // S^T = K Q^T for the two 32-key blocks of a step held in K slot `slot`
   auto scores = [&](int slot, f32x16 (&sc)[KB / 32]) {
@@ -226,23 +289,27 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   f32x16 sc[KB / 32];
   scores(0, sc);
   __syncthreads();  // every wave has read K slot 0 before iteration 0 refills it
+  const int32_t qstart = doc_window_start(a, docw, gq);  // first needed by the masks of step 0
+  const uint32_t span = (uint32_t)(gq - qstart);  // key j is allowed iff 0 <= j - start <= span
 
-  for (int s = 0; s < total; ++s) {
+  // one 64-key step: softmax and PV of step s from `sc`, scores of step s + 1 into `sn`; the
+  // loop below runs it twice per iteration with the two score arrays swapped (no copy)
+  auto step = [&](int s, f32x16 (&sc)[KB / 32], f32x16 (&sn)[KB / 32]) __attribute__((always_inline)) {
     const hsap_tile tile = tile_at(s);
     const float sl = FP8 ? head_scale * a.k_scale[tile.chunk * a.hkv + g] : head_scale;
     if (s + 2 < total) load_k(step_off(tile_at(s + 2), s + 2));
     if (s + 1 < total) load_v(step_off(tile_at(s + 1), s + 1));
     // scores of the next step: independent of this step's softmax
-    f32x16 sn[KB / 32];
     if (s + 1 < total) scores((s + 1) & 1, sn);
 
     if (tile.kind == HSAP_TILE_MASKED) {
-      const int32_t rel0 = (int32_t)global_pos(a.geom, tile.chunk, step_row0(tile, s)) - qstart;
+      // key row of register j: rel0 + 32 nb + c_row(j, hi), with the lane's 4 hi folded in once
+      const int32_t rel0 = (int32_t)global_pos(a.geom, tile.chunk, step_row0(tile, s)) - qstart + 4 * hi;
 #pragma unroll
       for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
         for (int j = 0; j < 16; ++j)
-          if ((uint32_t)(rel0 + 32 * nb + c_row(j, hi)) > span) sc[nb][j] = NEG_INF;
+          if ((uint32_t)(rel0 + (32 * nb + c_row(j, 0))) > span) sc[nb][j] = NEG_INF;
     }
     // online softmax (this lane's row = its query; lanes l and l ^ 32 share it)
     float mx = sc[0][0];
@@ -292,8 +359,11 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     if (s + 2 < total) store_k(s & 1);
     if (s + 1 < total) store_v((s + 1) & 1);
     __syncthreads();
-#pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb) sc[nb] = sn[nb];
+  };
+  f32x16 sn[KB / 32];
+  for (int s = 0; s < total; s += 2) {
+    step(s, sc, sn);
+    if (s + 1 < total) step(s + 1, sn, sc);
   }
 
   l_run = pair_sum(l_run);
@@ -370,8 +440,7 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   }
 
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
-  const int32_t qstart = a.doc_start[gq];
-  const uint32_t span = (uint32_t)(gq - qstart);
+  const DocWindow docw = doc_window(a, gq, lane);
   bf16x8 qf[D / 16];
   {
     const __bf16* qp = a.q + (qrow * a.hq + h) * D + 8 * hi;
@@ -476,6 +545,8 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   f32x16 sc[KB / 32];
   scores(Ks[0], sc);
   hsap_lds_barrier();  // every wave has read K slot 0 before step 0 refills it
+  const int32_t qstart = doc_window_start(a, docw, gq);
+  const uint32_t span = (uint32_t)(gq - qstart);
 
   int sk = 0;  // s % 3
   for (int s = 0; s < total; ++s) {
@@ -490,12 +561,13 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     if (s + 1 < total) scores(Ks[s1], sn);
 
     if (tile >> 31) {  // MASKED
-      const int32_t rel0 = (int32_t)global_pos(a.geom, chunk_of(tile), step_row0(tile, s)) - qstart;
+      // key row of register j: rel0 + 32 nb + c_row(j, hi), with the lane's 4 hi folded in once
+      const int32_t rel0 = (int32_t)global_pos(a.geom, chunk_of(tile), step_row0(tile, s)) - qstart + 4 * hi;
 #pragma unroll
       for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
         for (int j = 0; j < 16; ++j)
-          if ((uint32_t)(rel0 + 32 * nb + c_row(j, hi)) > span) sc[nb][j] = NEG_INF;
+          if ((uint32_t)(rel0 + (32 * nb + c_row(j, 0))) > span) sc[nb][j] = NEG_INF;
     }
     float mx = sc[0][0];
 #pragma unroll
@@ -615,7 +687,8 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
               "no forward kernel for head_dim=%d BM=%d BN=%d (BM in {64, 128}, or 256 with d = 128; BN in {64, 128})",
               d, bm, bn);
   if (num_runs == 0) return HSAP_OK;
-  if (!q || !k || !v || !doc_start || !tiles || !runs) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (!q || !k || !v || !(doc_start || a.cu) || !tiles || !runs)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v) & 15)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k and v must be 16-byte aligned");
   a.q = (const __bf16*)q;
@@ -709,21 +782,29 @@ extern "C" hsap_status hsap_partial_attn_fwd_fp8(const hsap_attn_desc* desc, con
 
 namespace hsap {
 
-hsap_status partial_attn_fwd_final(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
-                                   const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
-                                   int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots, void* o_out,
-                                   float* lse_out, hipStream_t stream) {
-  if (num_slots < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_slots < 1");
-  if (num_runs > 0 && (!o_part || !lse_part || !o_out || !lse_out)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
-  if ((uintptr_t)o_part & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_part must be 16-byte aligned");
+hsap_status executor_forward(const hsap_attn_desc* desc, bool fused, const void* q, const void* k, const void* v,
+                             const int32_t* cu_seqlens, int32_t num_docs, const hsap_tile* tiles,
+                             const hsap_run* runs, int64_t num_runs, float* o_part, float* lse_part,
+                             int32_t num_slots, void* o_out, float* lse_out, hipStream_t stream) {
+  if (!cu_seqlens || num_docs < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "no cumulative lengths");
+  if (num_runs > 0 && (!o_out || !lse_out)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if ((uintptr_t)o_out & 7) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_out must be 8-byte aligned");
   FwdArgs a{};
+  a.o_out = (__bf16*)o_out;
+  a.lse_out = lse_out;
+  a.cu = cu_seqlens;
+  a.num_docs = num_docs;
+  if (fused) {
+    a.num_slots = 1;
+    return forward<true>(desc, q, k, v, nullptr, tiles, runs, num_runs, a, stream);
+  }
+  if (num_slots < 1) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_slots < 1");
+  if (num_runs > 0 && (!o_part || !lse_part)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if ((uintptr_t)o_part & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_part must be 16-byte aligned");
   a.o_part = o_part;
   a.lse_part = lse_part;
   a.num_slots = num_slots;
-  a.o_out = (__bf16*)o_out;
-  a.lse_out = lse_out;
-  return forward<false>(desc, q, k, v, doc_start, tiles, runs, num_runs, a, stream);
+  return forward<false>(desc, q, k, v, nullptr, tiles, runs, num_runs, a, stream);
 }
 
 }  // namespace hsap

@@ -56,7 +56,7 @@ struct hsap_executor {
 
   // device side
   DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu | final_tile]
-  int32_t* doc_start = nullptr;
+  int32_t* doc_start = nullptr;  // start(t) per position, for the backward only
   DevBuf o_part, lse_part;
   float* delta = nullptr;
 
@@ -70,6 +70,8 @@ struct hsap_executor {
   const hsap_tile* d_tiles_all = nullptr;
   const hsap_run* d_runs_all = nullptr;
   const uint8_t* d_final_tile = nullptr;
+  const int32_t* d_cu = nullptr;  // the plan's cu_seqlens (the forwards search it for document starts)
+  int32_t num_docs = 0;
   std::vector<uint8_t> chunk_has_tiles;
 };
 
@@ -172,7 +174,8 @@ hsap_status hsap_executor_create(const hsap_attn_desc* desc, int32_t options, in
   hipError_t e = hipGetDevice(&ex->device);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ex->device);
   for (int i = 0; e == hipSuccess && i < 2; ++i) e = hipEventCreateWithFlags(&ex->uploaded[i], hipEventDisableTiming);
-  if (e == hipSuccess) e = hipMalloc((void**)&ex->doc_start, (size_t)g.N * sizeof(int32_t));
+  if (e == hipSuccess && (options & HSAP_EXEC_BACKWARD))
+    e = hipMalloc((void**)&ex->doc_start, (size_t)g.N * sizeof(int32_t));
   if (e == hipSuccess && (options & HSAP_EXEC_BACKWARD))
     e = hipMalloc((void**)&ex->delta, (size_t)g.n * desc->heads_q * sizeof(float));
   if (e != hipSuccess) {
@@ -338,10 +341,14 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   ex->d_tiles_all = RA ? (const hsap_tile*)(d + o_ta) : nullptr;
   ex->d_runs_all = RA ? (const hsap_run*)(d + o_ra) : nullptr;
   ex->d_final_tile = (const uint8_t*)(d + o_ft);
+  ex->d_cu = d + o_cu;
+  ex->num_docs = num_docs;
 
-  // 6. start(t) for every position
-  st = hsap_doc_start(d + o_cu, num_docs, ex->geom.N, ex->doc_start, hip_stream);
-  if (st != HSAP_OK) return st;
+  // 6. start(t) for every position, read by the backward's masks (the forwards search cu_seqlens)
+  if (ex->options & HSAP_EXEC_BACKWARD) {
+    st = hsap_doc_start(d + o_cu, num_docs, ex->geom.N, ex->doc_start, hip_stream);
+    if (st != HSAP_OK) return st;
+  }
   ex->planned = true;
   return HSAP_OK;
 }
@@ -360,9 +367,9 @@ hsap_status hsap_executor_partial_forward(hsap_executor* ex, const void* q, cons
   if (!ex) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL executor");
   if (!ex->planned) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "executor has no plan");
   if (!q || !k || !v || !o_out || !lse_out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
-  return partial_attn_fwd_final(&ex->desc, q, k, v, ex->doc_start, ex->d_tiles_q, ex->d_runs_q, ex->info.num_runs_q,
-                                (float*)ex->o_part.p, (float*)ex->lse_part.p, ex->info.num_parts, o_out, lse_out,
-                                (hipStream_t)hip_stream);
+  return executor_forward(&ex->desc, false, q, k, v, ex->d_cu, ex->num_docs, ex->d_tiles_q, ex->d_runs_q,
+                          ex->info.num_runs_q, (float*)ex->o_part.p, (float*)ex->lse_part.p, ex->info.num_parts,
+                          o_out, lse_out, (hipStream_t)hip_stream);
 }
 
 hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, void* hip_stream) {
@@ -391,8 +398,8 @@ hsap_status hsap_executor_forward(hsap_executor* ex, const void* q, const void* 
   if (!q || !k || !v || !o_out || !lse_out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if (fused) {
     if (!(ex->options & HSAP_EXEC_FUSED)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "fused forward needs HSAP_EXEC_FUSED");
-    return hsap_attn_fwd_fused(&ex->desc, q, k, v, ex->doc_start, ex->d_tiles_all, ex->d_runs_all,
-                               ex->info.num_runs_all, o_out, lse_out, hip_stream);
+    return executor_forward(&ex->desc, true, q, k, v, ex->d_cu, ex->num_docs, ex->d_tiles_all, ex->d_runs_all,
+                            ex->info.num_runs_all, nullptr, nullptr, 0, o_out, lse_out, (hipStream_t)hip_stream);
   }
   const hsap_status st = hsap_executor_partial_forward(ex, q, k, v, o_out, lse_out, hip_stream);
   if (st != HSAP_OK) return st;

@@ -77,13 +77,16 @@ hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const floa
                       int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, const uint8_t* skip,
                       int32_t block_m, hipStream_t stream);
 
-// hsap_partial_attn_fwd where runs whose slot is kFinalSlot write the final bf16 O and LSE of
-// their q-tile to o_out / lse_out (the q-tile's only part: nothing to merge).
+// The executor's forwards.  Document starts come from the cumulative lengths cu_seqlens
+// [num_docs + 1] on the device (no per-position start array).  fused: hsap_attn_fwd_fused over
+// runs that span every chunk.  Otherwise hsap_partial_attn_fwd, where runs whose slot is
+// kFinalSlot write the final bf16 O and LSE of their q-tile to o_out / lse_out (the q-tile's
+// only part: nothing to merge).
 constexpr int32_t kFinalSlot = -2;
-hsap_status partial_attn_fwd_final(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
-                                   const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
-                                   int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots, void* o_out,
-                                   float* lse_out, hipStream_t stream);
+hsap_status executor_forward(const hsap_attn_desc* desc, bool fused, const void* q, const void* k, const void* v,
+                             const int32_t* cu_seqlens, int32_t num_docs, const hsap_tile* tiles,
+                             const hsap_run* runs, int64_t num_runs, float* o_part, float* lse_part,
+                             int32_t num_slots, void* o_out, float* lse_out, hipStream_t stream);
 #endif
 
 }  // namespace hsap

@@ -40,6 +40,10 @@ CASES = [
     (1024, 1, "contiguous", 2, 2, 64, 64, 64, 300),
     (2048, 4, "zigzag", 4, 1, 128, 128, 64, 120),
     (4096, 4, "contiguous", 4, 2, 128, 128, 128, 1500),
+    # documents of 1..5 tokens: up to 31 boundaries among a wave's 32 queries (the forwards find
+    # document starts from cu_seqlens; the entry points read per-position starts)
+    (2048, 2, "zigzag", 2, 2, 128, 256, 128, 3),
+    (1024, 2, "contiguous", 2, 1, 64, 64, 64, 3),
 ]
 
 
@@ -52,18 +56,23 @@ def test_executor_matches_oracle_and_entry_points(case):
     N, P, layout, hq, hkv, d, bm, bn, mean = case
     cu = _cu(np.random.default_rng(N + P), N, mean)
     r = P - 1
-    c = Case(cu, N, P, layout, r, hq, hkv, d, bm, bn, seed=20 + r, backward=True)
+    bwd = bm <= 128  # the backward has no 256-row q-tile kernel
+    c = Case(cu, N, P, layout, r, hq, hkv, d, bm, bn, seed=20 + r, backward=bwd)
     ref = c.run_oracle()
+    if not bwd:
+        ref = {"fwd": ref}
     for split in (-1, 0, 1):
         _say("executor", case, "shard", r, "split", split)
         ex = c.run_executor(max_run_tiles=split)
         rep = {"o": max_abs(ex["o"], ref["fwd"]["o"]), "lse": max_abs(ex["lse"], ref["fwd"]["lse"]),
-               "o_fused": max_abs(ex["o_fused"], ref["fwd"]["o"]), "lse_fused": max_abs(ex["lse_fused"], ref["fwd"]["lse"]),
-               "dq": rel_max(ex["dq"], ref["dq"]), "dk": rel_max(ex["dk"], ref["dk"]), "dv": rel_max(ex["dv"], ref["dv"])}
+               "o_fused": max_abs(ex["o_fused"], ref["fwd"]["o"]), "lse_fused": max_abs(ex["lse_fused"], ref["fwd"]["lse"])}
+        if bwd:
+            rep.update(dq=rel_max(ex["dq"], ref["dq"]), dk=rel_max(ex["dk"], ref["dk"]), dv=rel_max(ex["dv"], ref["dv"]))
         _say(rep, ex["info"])
         assert rep["o"] <= O_ATOL and rep["o_fused"] <= O_ATOL, rep
         assert rep["lse"] <= LSE_ATOL and rep["lse_fused"] <= LSE_ATOL, rep
-        assert max(rep["dq"], rep["dk"], rep["dv"]) <= GRAD_RTOL, rep
+        if bwd:
+            assert max(rep["dq"], rep["dk"], rep["dv"]) <= GRAD_RTOL, rep
         assert np.array_equal(ex["o_staged"], ex["o"]) and np.array_equal(ex["lse_staged"], ex["lse"])
         info = ex["info"]
         plan = plan_shard(cu, N, P, layout, r, bm, bn)
@@ -76,8 +85,9 @@ def test_executor_matches_oracle_and_entry_points(case):
             assert info["num_parts"] == len(gpu["sa"].present)
             assert np.array_equal(ex["o"], gpu["o"]) and np.array_equal(ex["lse"], gpu["lse"])
             assert np.array_equal(ex["o_fused"], gpu["o_fused"]) and np.array_equal(ex["lse_fused"], gpu["lse_fused"])
-            assert np.array_equal(ex["dk"], _bf16(gpu["dk"])) and np.array_equal(ex["dv"], _bf16(gpu["dv"]))
-            assert np.array_equal(ex["dq"], gpu["dq_bf16"])
+            if bwd:
+                assert np.array_equal(ex["dk"], _bf16(gpu["dk"])) and np.array_equal(ex["dv"], _bf16(gpu["dv"]))
+                assert np.array_equal(ex["dq"], gpu["dq_bf16"])
 
 
 def test_executor_replans_other_batches():
