@@ -479,12 +479,13 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     return run_base + step_row0(p, s) * rstride;
   };
 
-  // direct staging: instruction u of wave w fills chunk positions p = 128 w + 64 u + lane
-  int32_t gsrc[2];
+  // direct staging: instruction u of wave w fills chunk positions p = 128 w + 64 u + lane; the
+  // lane's source is a 32-bit byte offset from the step's (scalar) base pointer
+  uint32_t gsrc[2];
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int p = 128 * w + 64 * u + lane, row = p >> 4;
-    gsrc[u] = (int32_t)(row * rstride + swz_chunk<CPR>(row, p & 15) * 8);
+    gsrc[u] = (uint32_t)((row * rstride + swz_chunk<CPR>(row, p & 15) * 8) * 2);
   }
   // issued from asm: the transfers are ordered by the explicit vmcnt waits of the ring below (the
   // compiler would otherwise wait for each one before any later LDS read).  No memory clobber:
@@ -494,12 +495,12 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const uint32_t m0v = (uint32_t)(uintptr_t)(dst + (128 * w + 64 * u) * 8);
-      const __bf16* gp = src + gsrc[u];
-      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(m0v)),
-                   "v"(gp)
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(__builtin_amdgcn_readfirstlane(m0v)),
+                   "v"(gsrc[u]), "s"(src)
                    : "m0");
     }
   };
+
   // operand offsets in a swizzled tile: K rows (row l32 of a 32-row block, chunk 2 kk + hi) and
   // V transpose reads (rows 8 k + tr_row of a 16-row block, columns 32 mb + tr_col)
   const int tr_row = 4 * hi + ((lane & 15) >> 2);
@@ -549,7 +550,9 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   const uint32_t span = (uint32_t)(gq - qstart);
 
   int sk = 0;  // s % 3
-  for (int s = 0; s < total; ++s) {
+  // one 64-key step (softmax and PV of step s from `sc`, scores of step s + 1 into `sn`), run twice
+  // per loop iteration with the score arrays swapped
+  auto step = [&](int s, f32x16 (&sc)[KB / 32], f32x16 (&sn)[KB / 32]) __attribute__((always_inline)) {
     // the window of tile (s + 3) / SUBS is needed now (rare vector load: every 64 tiles)
     if (s + 3 < total && ((s + 3) / SUBS) >> 6 > win_hi) load_window(win_hi + 1);
     const uint32_t tile = tile_at(s);
@@ -557,7 +560,6 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     const bool ldk = s + 3 < total, ldv = s + 2 < total;
     if (ldk) stage(a.k + step_off(tile_at(s + 3), s + 3), Ks[sk]);
     if (ldv) stage(a.v + step_off(tile_at(s + 2), s + 2), Vs[s2]);
-    f32x16 sn[KB / 32];
     if (s + 1 < total) scores(Ks[s1], sn);
 
     if (tile >> 31) {  // MASKED
@@ -612,9 +614,12 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     if (ldk && ldv) asm volatile("s_waitcnt vmcnt(4)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     else if (ldk || ldv) asm volatile("s_waitcnt vmcnt(2)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-#pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb) sc[nb] = sn[nb];
     sk = s1;
+  };
+  f32x16 sn[KB / 32];
+  for (int s = 0; s < total; s += 2) {
+    step(s, sc, sn);
+    if (s + 1 < total) step(s + 1, sn, sc);
   }
 
   l_run = pair_sum(l_run);
