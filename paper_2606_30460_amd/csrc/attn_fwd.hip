@@ -33,6 +33,10 @@
 
 namespace hsap {
 
+// Third word of a raw buffer descriptor on gfx9-family targets (32-bit data format; the format
+// is ignored by untyped loads, but a zero format makes them return zeros).
+constexpr int kBufferWord3 = 0x00020000;
+
 struct FwdArgs {
   const __bf16* q;
   const __bf16* k;
@@ -193,37 +197,34 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 
   // staging: thread t moves chunks t, t + NT, ... of a step's [KB][D] tile, i.e. one column chunk
   // of rows r0, r0 + ROWS, r0 + 2 ROWS, ...  The distance between a thread's chunks is the same
-  // for every thread, so one 32-bit byte offset per thread serves all of them: the row distance
-  // goes into the (uniform) base pointer of each global load and into the immediate offset of
-  // each LDS store.
+  // for every thread, so the loads are buffer loads over the step's rows: the lane's byte offset
+  // (loop-invariant, one VGPR) plus a uniform offset per chunk (SGPR), no address arithmetic per
+  // load; the LDS stores take the chunk distance as an immediate offset.  The descriptor spans
+  // exactly the step's KB rows, so the hardware range check bounds every access.
   constexpr int EPC = 16 / (int)sizeof(KT);  // K elements per 16-byte chunk
   constexpr int VROWS = NT / (D / 8), KROWS = NT / KCPR;
   static_assert(NT % (D / 8) == 0 && NT % KCPR == 0, "a thread's chunks must share their column");
-  const uint32_t gvo = (uint32_t)(((tid / (D / 8)) * rstride + (tid % (D / 8)) * 8) * 2);
-  const uint32_t gko = (uint32_t)(((tid / KCPR) * rstride + (tid % KCPR) * EPC) * (int)sizeof(KT));
+  const int gvo = (int)(((tid / (D / 8)) * rstride + (tid % (D / 8)) * 8) * 2);
+  const int gko = (int)(((tid / KCPR) * rstride + (tid % KCPR) * EPC) * (int)sizeof(KT));
   const int lvo = (tid / (D / 8)) * VS + (tid % (D / 8)) * 8;
   const int lko = (tid / KCPR) * KS + (tid % KCPR) * EPC;
+  const int step_bytes_k = (int)(KB * rstride * (int)sizeof(KT)), step_bytes_v = (int)(KB * rstride * 2);
   K16 kreg[PER_TK];
   bf16x8 vreg[PER_T];
-  // (the empty asm, which touches no memory, keeps each load's 32-bit offset at its use: hoisted
-  // out of the loop, or shared by the loads, it becomes a 64-bit address computed per load)
   auto load_k = [&](int64_t off) {
-    const char* src = (const char*)((const KT*)a.k + off);
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc((void*)((const KT*)a.k + off), (short)0, step_bytes_k, kBufferWord3);
 #pragma unroll
-    for (int i = 0; i < PER_TK; ++i) {
-      uint32_t o;
-      asm("" : "=v"(o) : "0"(gko), "s"(off), "n"(i));
-      kreg[i] = *(const K16*)(src + (int64_t)i * KROWS * rstride * (int)sizeof(KT) + o);
-    }
+    for (int i = 0; i < PER_TK; ++i)
+      kreg[i] = __builtin_bit_cast(
+          K16, __builtin_amdgcn_raw_buffer_load_b128(r, gko, (int)(i * KROWS * rstride * (int)sizeof(KT)), 0));
   };
   auto load_v = [&](int64_t off) {
-    const char* src = (const char*)(a.v + off);
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(a.v + off), (short)0, step_bytes_v, kBufferWord3);
 #pragma unroll
-    for (int i = 0; i < PER_T; ++i) {
-      uint32_t o;
-      asm("" : "=v"(o) : "0"(gvo), "s"(off), "n"(i));
-      vreg[i] = *(const bf16x8*)(src + (int64_t)i * VROWS * rstride * 2 + o);
-    }
+    for (int i = 0; i < PER_T; ++i)
+      vreg[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, gvo, (int)(i * VROWS * rstride * 2), 0));
   };
   auto store_k = [&](int slot) {
 #pragma unroll
