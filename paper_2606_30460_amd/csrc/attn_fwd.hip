@@ -295,13 +295,15 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 
   // one 64-key step: softmax and PV of step s from `sc`, scores of step s + 1 into `sn`; the
   // loop below runs it twice per iteration with the two score arrays swapped (no copy)
-  auto step = [&](int s, f32x16 (&sc)[KB / 32], f32x16 (&sn)[KB / 32]) __attribute__((always_inline)) {
+  // (`par` is s % 2 as a compile-time constant, so every LDS slot address is an immediate)
+  auto step = [&](int s, auto par, f32x16 (&sc)[KB / 32], f32x16 (&sn)[KB / 32]) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(par)::value;
     const hsap_tile tile = tile_at(s);
     const float sl = FP8 ? head_scale * a.k_scale[tile.chunk * a.hkv + g] : head_scale;
     if (s + 2 < total) load_k(step_off(tile_at(s + 2), s + 2));
     if (s + 1 < total) load_v(step_off(tile_at(s + 1), s + 1));
     // scores of the next step: independent of this step's softmax
-    if (s + 1 < total) scores((s + 1) & 1, sn);
+    if (s + 1 < total) scores(PAR ^ 1, sn);
 
     if (tile.kind == HSAP_TILE_MASKED) {
       // key row of register j: rel0 + 32 nb + c_row(j, hi), with the lane's 4 hi folded in once
@@ -343,7 +345,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     l_run += rs;  // the half-row sums of lanes l and l ^ 32 are combined once, at the end
 
     // O^T += V^T P^T, 16 keys per MFMA
-    const __bf16* V = Vs[s & 1];
+    const __bf16* V = Vs[PAR];
 #pragma unroll
     for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
@@ -357,14 +359,14 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
         }
       }
 
-    if (s + 2 < total) store_k(s & 1);
-    if (s + 1 < total) store_v((s + 1) & 1);
+    if (s + 2 < total) store_k(PAR);
+    if (s + 1 < total) store_v(PAR ^ 1);
     __syncthreads();
   };
   f32x16 sn[KB / 32];
   for (int s = 0; s < total; s += 2) {
-    step(s, sc, sn);
-    if (s + 1 < total) step(s + 1, sn, sc);
+    step(s, std::integral_constant<int, 0>{}, sc, sn);
+    if (s + 1 < total) step(s + 1, std::integral_constant<int, 1>{}, sn, sc);
   }
 
   l_run = pair_sum(l_run);
@@ -397,24 +399,29 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Direct-to-LDS forward for d = 128, BM = 256: eight waves (wave w owns query
-// rows 32w..32w+31), one workgroup per CU.  K and V steps go from global
-// memory straight into LDS (global_load_lds, no staging registers) in a
-// three-slot ring of unpadded XOR-swizzled [64][128] tiles: K three steps
-// ahead of its use in the scores, V two steps ahead of its use in PV, so a
-// load has two steps to arrive.  Each wave moves 128 of a tile's 1024
-// 16-byte chunks per tile, 64 per instruction; a lane's source chunk is the
-// one the swizzle places at its destination.
+// Direct-to-LDS forward for d = 128: WAVES waves (wave w owns query rows
+// 32w..32w+31; BM = 32 WAVES).  K and V steps go from global memory straight
+// into LDS (global_load_lds, no staging registers) in a ring of unpadded
+// XOR-swizzled [64][128] tiles.  Eight waves (BM = 256, one workgroup per CU):
+// three slots, K three steps ahead of its use in the scores and V two ahead of
+// its use in PV, so a transfer has two steps to arrive.  Four waves (BM = 128,
+// two workgroups per CU in 2 x 64 KB of LDS): two slots, K two steps ahead and
+// V one, so a transfer has one step.  Each wave moves 1024 / WAVES of a tile's
+// 1024 16-byte chunks, 64 per instruction; a lane's source chunk is the one
+// the swizzle places at its destination.
 // ---------------------------------------------------------------------------
-template <int BN, bool FUSED>
-__global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
-  constexpr int D = 128, KB = 64, SUBS = BN / KB, CPR = D / 8, NSLOT = 3, TILE = KB * D;
+template <int BN, int WAVES, bool FUSED>
+__global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
+  static_assert(WAVES == 4 || WAVES == 8, "four or eight waves");
+  constexpr int D = 128, KB = 64, SUBS = BN / KB, CPR = D / 8, TILE = KB * D;
+  constexpr int NSLOT = WAVES == 8 ? 3 : 2;  // ring depth
+  constexpr int WCH = TILE / 8 / WAVES;      // 16-byte chunks a wave moves per tile
+  constexpr int U = WCH / 64;                // transfer instructions per wave per tile
   constexpr float NEG_INF = -__builtin_inff();
   constexpr float RESCALE_SLACK = 8.f;
   __shared__ __attribute__((aligned(16))) __bf16 Ks[NSLOT][TILE];
   __shared__ __attribute__((aligned(16))) __bf16 Vs[NSLOT][TILE];
   typedef __attribute__((address_space(3))) void* lds_void;
-  typedef __attribute__((address_space(1))) void* glb_void;
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
@@ -426,7 +433,7 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   if (!final_out && (slot < 0 || slot >= a.num_slots)) return;
   const int g = h / a.group;
   const int64_t n = a.geom.n;
-  const int64_t qrow = (int64_t)run.tile * 256 + 32 * w + l32;
+  const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;
 
   if (run.count == 0) {
     if (final_out) {
@@ -480,26 +487,28 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     return run_base + step_row0(p, s) * rstride;
   };
 
-  // direct staging: instruction u of wave w fills chunk positions p = 128 w + 64 u + lane; the
+  // direct staging: instruction u of wave w fills chunk positions p = WCH w + 64 u + lane; the
   // lane's source is a 32-bit byte offset from the step's (scalar) base pointer
-  uint32_t gsrc[2];
+  uint32_t gsrc[U];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int p = 128 * w + 64 * u + lane, row = p >> 4;
+  for (int u = 0; u < U; ++u) {
+    const int p = WCH * w + 64 * u + lane, row = p >> 4;
     gsrc[u] = (uint32_t)((row * rstride + swz_chunk<CPR>(row, p & 15) * 8) * 2);
   }
   // issued from asm: the transfers are ordered by the explicit vmcnt waits of the ring below (the
   // compiler would otherwise wait for each one before any later LDS read).  No memory clobber:
   // volatile asm keeps its order against the ring's barriers (which do clobber memory), and the
   // tile descriptors stay scalar loads.
+  // (M0, the LDS destination, is the slot's 32-bit LDS address plus the wave's chunk range: scalar
+  // arithmetic only, with the wave index taken as uniform)
+  const int wu = __builtin_amdgcn_readfirstlane(w);
   auto stage = [&](const __bf16* src, __bf16* dst) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(lds_void)dst + (uint32_t)(WCH * wu * 16);
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const uint32_t m0v = (uint32_t)(uintptr_t)(dst + (128 * w + 64 * u) * 8);
-      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(__builtin_amdgcn_readfirstlane(m0v)),
-                   "v"(gsrc[u]), "s"(src)
+    for (int u = 0; u < U; ++u)
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds + 64 * 16 * u), "v"(gsrc[u]),
+                   "s"(src)
                    : "m0");
-    }
   };
 
   // operand offsets in a swizzled tile: K rows (row l32 of a 32-row block, chunk 2 kk + hi) and
@@ -531,18 +540,14 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
 
-  // prologue: K(0..2) and V(0..1) in flight, wait for all, scores of step 0
-  {
-    const uint32_t t0 = tile_at(0);
-    stage(a.k + step_off(t0, 0), Ks[0]);
-    stage(a.v + step_off(t0, 0), Vs[0]);
-    if (total > 1) {
-      const uint32_t t1 = tile_at(1);
-      stage(a.k + step_off(t1, 1), Ks[1]);
-      stage(a.v + step_off(t1, 1), Vs[1]);
+  // prologue: K(0 .. NSLOT - 1) and V(0 .. NSLOT - 2) in flight, wait for all, scores of step 0
+#pragma unroll
+  for (int j = 0; j < NSLOT; ++j)
+    if (j < total) {
+      const uint32_t t = tile_at(j);
+      stage(a.k + step_off(t, j), Ks[j]);
+      if (j < NSLOT - 1) stage(a.v + step_off(t, j), Vs[j]);
     }
-    if (total > 2) stage(a.k + step_off(tile_at(2), 2), Ks[2]);
-  }
   asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   f32x16 sc[KB / 32];
   scores(Ks[0], sc);
@@ -550,17 +555,23 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   const int32_t qstart = doc_window_start(a, docw, gq);
   const uint32_t span = (uint32_t)(gq - qstart);
 
-  int sk = 0;  // s % 3
+  int sk = 0;  // s % NSLOT
   // one 64-key step (softmax and PV of step s from `sc`, scores of step s + 1 into `sn`), run twice
   // per loop iteration with the score arrays swapped
-  auto step = [&](int s, f32x16 (&sc)[KB / 32], f32x16 (&sn)[KB / 32]) __attribute__((always_inline)) {
-    // the window of tile (s + 3) / SUBS is needed now (rare vector load: every 64 tiles)
-    if (s + 3 < total && ((s + 3) / SUBS) >> 6 > win_hi) load_window(win_hi + 1);
+  // (`par` is s % 2 as a compile-time constant: with two slots every slot index is one)
+  auto step = [&](int s, auto par, f32x16 (&sc)[KB / 32], f32x16 (&sn)[KB / 32]) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(par)::value;
+    // the window of tile (s + NSLOT) / SUBS is needed now (rare vector load: every 64 tiles)
+    if (s + NSLOT < total && ((s + NSLOT) / SUBS) >> 6 > win_hi) load_window(win_hi + 1);
     const uint32_t tile = tile_at(s);
-    const int s1 = sk == 2 ? 0 : sk + 1, s2 = s1 == 2 ? 0 : s1 + 1;  // (s + 1) % 3, (s + 2) % 3
-    const bool ldk = s + 3 < total, ldv = s + 2 < total;
-    if (ldk) stage(a.k + step_off(tile_at(s + 3), s + 3), Ks[sk]);
-    if (ldv) stage(a.v + step_off(tile_at(s + 2), s + 2), Vs[s2]);
+    // s % NSLOT, (s + 1) % NSLOT and (s + NSLOT - 1) % NSLOT: this step's slot, the slot of the
+    // next scores and of V's refill
+    const int s0 = NSLOT == 2 ? PAR : sk;
+    const int s1 = NSLOT == 2 ? PAR ^ 1 : (sk == NSLOT - 1 ? 0 : sk + 1);
+    const int sv = NSLOT == 2 ? PAR ^ 1 : (sk == 0 ? NSLOT - 1 : sk - 1);
+    const bool ldk = s + NSLOT < total, ldv = s + NSLOT - 1 < total;
+    if (ldk) stage(a.k + step_off(tile_at(s + NSLOT), s + NSLOT), Ks[s0]);
+    if (ldv) stage(a.v + step_off(tile_at(s + NSLOT - 1), s + NSLOT - 1), Vs[sv]);
     if (s + 1 < total) scores(Ks[s1], sn);
 
     if (tile >> 31) {  // MASKED
@@ -598,7 +609,7 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
       }
     l_run += rs;
 
-    const __bf16* V = Vs[sk];
+    const __bf16* V = Vs[s0];
 #pragma unroll
     for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
@@ -610,17 +621,23 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
           o[mb] = mfma32(av, pb[nb][half], o[mb]);
         }
       }
-    // the loads issued one step ago (K(s + 2), V(s + 1)) must have landed before the next step;
-    // this step's own loads stay in flight
-    if (ldk && ldv) asm volatile("s_waitcnt vmcnt(4)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    else if (ldk || ldv) asm volatile("s_waitcnt vmcnt(2)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    // K(s + 2) and V(s + 1) must have landed before the next step.  Three slots: they were
+    // issued one step ago, and this step's own transfers (U instructions each) stay in flight.
+    // Two slots: they are this step's transfers.
+    if constexpr (NSLOT == 3) {
+      static_assert(U == 2, "the waits below count two instructions per tile");
+      if (ldk && ldv) asm volatile("s_waitcnt vmcnt(4)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      else if (ldk || ldv) asm volatile("s_waitcnt vmcnt(2)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    }
     sk = s1;
   };
   f32x16 sn[KB / 32];
   for (int s = 0; s < total; s += 2) {
-    step(s, sc, sn);
-    if (s + 1 < total) step(s + 1, sn, sc);
+    step(s, std::integral_constant<int, 0>{}, sc, sn);
+    if (s + 1 < total) step(s + 1, std::integral_constant<int, 1>{}, sn, sc);
   }
 
   l_run = pair_sum(l_run);
@@ -651,11 +668,11 @@ __global__ __launch_bounds__(512, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   }
 }
 
-template <int BN, bool FUSED>
+template <int BN, int WAVES, bool FUSED>
 static hsap_status launch_dl(const FwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_fwd_dl_kernel<BN, FUSED>), dim3((unsigned)blocks), dim3(512), 0, stream, a);
+  hipLaunchKernelGGL((attn_fwd_dl_kernel<BN, WAVES, FUSED>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
   return HSAP_OK;
@@ -721,7 +738,10 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   } else {
 #define HSAP_FWD_CASE(D_, BN_, W_) \
   if (d == D_ && bn == BN_ && bm == 32 * W_) return launch<D_, BN_, W_, FUSED>(a, num_runs, s);
-  if (d == 128 && bm == 256) return bn == 128 ? launch_dl<128, FUSED>(a, num_runs, s) : launch_dl<64, FUSED>(a, num_runs, s);
+  if (d == 128 && bm == 256)
+    return bn == 128 ? launch_dl<128, 8, FUSED>(a, num_runs, s) : launch_dl<64, 8, FUSED>(a, num_runs, s);
+  if (d == 128 && bm == 128)
+    return bn == 128 ? launch_dl<128, 4, FUSED>(a, num_runs, s) : launch_dl<64, 4, FUSED>(a, num_runs, s);
   HSAP_FWD_CASE(128, 128, 4)
   HSAP_FWD_CASE(128, 64, 4)
   HSAP_FWD_CASE(128, 128, 2)
