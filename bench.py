@@ -403,6 +403,15 @@ def fwd_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def fwd_kernel_name(res) -> str:
+    """The partial forward kernel the library dispatches for a workload's shapes (bf16 scores):
+    direct-to-LDS for head_dim 128 with 128- or 256-row q-tiles, register-staged otherwise."""
+    d, bm, bn = res["head_dim"], res["block_m"], res["block_n"]
+    if d == 128 and bm in (128, 256):
+        return "attn_fwd_dl_kernel<%d, %d, false>" % (bn, bm // 32)
+    return "attn_fwd_kernel<%d, %d, %d, false, false>" % (d, bn, bm // 32)
+
+
 def measured_traffic(workload: str):
     """HBM bytes per forward launch from the committed counter summary, or None.
 
@@ -510,7 +519,7 @@ def main():
                    "block_m": main_res["block_m"], "block_n": main_res["block_n"], "pass": "forward"
                    if not main_res["backward"] else "forward+backward"},
         "pct_of_bf16_peak": round(100.0 * main_res["tflops"] / PEAK_BF16_TFLOPS, 3),
-        "roofline": {"bound": "mfma", "kernel": "attn_fwd_kernel", "achieved": round(achieved, 3),
+        "roofline": {"bound": "mfma", "kernel": fwd_kernel_name(main_res), "achieved": round(achieved, 3),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
                      "traffic": measured_traffic(args.workload), "kernel_source_sha256_16": fwd_source_hash()},
         "cpu_baseline": cpu,
