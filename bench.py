@@ -4,10 +4,15 @@
 One step is one pass of the whole path for one packed batch, inputs resident
 in HBM, driven by the step executor (hsap_executor_*):
   host planner (tile list and runs, C++) -> one async upload of the lists
-  -> document starts -> partial attention of the shard against every K/V
-  chunk -> LSE merge (and, for a forward+backward workload, the backward
+  -> partial attention of the shard against every K/V chunk -> LSE merge
+  (and, for a forward+backward workload, the document starts, the backward
   preprocess and the partial attention backward, which stores the final bf16
   dQ/dK/dV from its registers).
+
+Timing: about 60 ms of untimed steps first (the GPU's clocks settle under
+sustained load), then the warm-up steps, then the timed steps with nothing
+between the launches; a second pass of the same steps with events around
+each stage gives the per-kernel breakdown.
 
 Default workload: 32768-token packed sequence, log-normal documents, 32
 heads of 128, sequence-parallel degree 8 (contiguous), shard 3, forward.
@@ -32,6 +37,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+SETTLE_S = 0.06             # untimed sustained load before the warm-up steps (clocks reach steady state)
+SETTLE_MAX_STEPS = 4000
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 METRIC = "useful doc-masked attention TFLOP/s per shard; % of bf16 MFMA peak"
 
@@ -131,6 +138,16 @@ def measure(name: str, steps: int, warmup: int, backward=None):
             if e:
                 e[3].record()
 
+    # Settle: under sustained load the GPU's clocks take some tens of milliseconds to reach their
+    # steady state (the first ~150 c2 steps run up to a third slower than the later ones, which a
+    # training job never sees after its first moments).  Run the same step untimed for about
+    # SETTLE_S, in bursts of 10 with a synchronisation between bursts, then the warm-up steps.
+    settle_steps, t_settle = 0, time.perf_counter()
+    while time.perf_counter() - t_settle < SETTLE_S and settle_steps < SETTLE_MAX_STEPS:
+        for _ in range(10):
+            one_step(None)
+        settle_steps += 10
+        torch.cuda.synchronize()
     for _ in range(warmup):
         one_step(None)
     torch.cuda.synchronize()
@@ -200,6 +217,7 @@ def measure(name: str, steps: int, warmup: int, backward=None):
         "merge_bytes": merge_bytes,
         "merge_gbs": merge_bytes / (merge_ms.mean() * 1e-3) / 1e9,
         "planner_host_ms": plan_ms,
+        "settle_steps": settle_steps,
     }
     if fused_ms is not None:
         res.update({"fused_fwd_kernel_ms": fused_ms, "fused_fwd_tflops": fwd_flops / (fused_ms * 1e-3) / 1e12})
