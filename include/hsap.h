@@ -506,7 +506,7 @@ hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, vo
  * chunk, then the backward), keeping the host cost of a step small next to
  * its kernels.
  *
- * An executor owns: two pinned staging buffers for the planner's lists, one
+ * An executor owns: a ring of 16 pinned staging buffers for the planner's lists, one
  * device list buffer, the fp32 partial outputs of the forward (grown to the
  * largest plan seen) and, with HSAP_EXEC_BACKWARD, the device doc_start
  * array and the backward's delta.  The forwards take document starts from
@@ -571,8 +571,9 @@ void hsap_executor_destroy(hsap_executor* ex);
  * MAJOR_Q_ALL runs; then one asynchronous upload of every list and
  * cu_seqlens from a pinned staging buffer, and (HSAP_EXEC_BACKWARD only)
  * hsap_doc_start, on `stream`.
- * The host blocks only while the staging buffer it is about to reuse is
- * still being uploaded (two plans in flight).
+ * The host blocks only when the staging buffer it is about to reuse may not
+ * have been uploaded yet: it waits for an event recorded after every 8th
+ * upload (events cost the stream a gap each), at most 16 plans in flight.
  *   cu_seqlens  host int32 [num_docs + 1] for the executor's N (rules of
  *               hsap_plan); read before the call returns.
  */

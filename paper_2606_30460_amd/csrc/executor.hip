@@ -21,6 +21,16 @@ int fwd_resident_per_cu(int bm, int d) {
   return std::min(by_waves, std::max(1, 160 * 1024 / lds));
 }
 
+// Pinned staging buffers for the list uploads, used in a ring.  The host may rewrite a buffer only
+// once the copy out of it has run; an event tells it so, but an event marker costs the stream a
+// gap of several microseconds, so one is recorded only after every kEventEvery-th upload: before
+// rewriting the buffer of upload u - kStaging, the host waits for the first event recorded at or
+// after that upload (the stream runs in order).  kEventEvery <= kStaging keeps that event in the
+// past.
+constexpr int kStaging = 16;
+constexpr int kEventEvery = 8;
+static_assert(kEventEvery <= kStaging, "the awaited event must precede the upload that waits");
+
 // Device or pinned allocation that grows (never shrinks) to the largest size asked for.
 struct DevBuf {
   void* p = nullptr;
@@ -48,11 +58,12 @@ struct hsap_executor {
   std::vector<int32_t> slot_map;
   std::vector<uint8_t> final_tile;  // per q-tile: 1 when its only part is written final by the partial forward
 
-  // pinned staging, double-buffered; `uploaded[i]` follows the copy out of pinned[i]
-  DevBuf pinned[2];
-  hipEvent_t uploaded[2] = {nullptr, nullptr};
-  bool recorded[2] = {false, false};
-  int next_slot = 0;
+  // pinned staging ring; upload u uses pinned[u % kStaging], and when u % kEventEvery is
+  // kEventEvery - 1 an event recorded after its copy sits in uploaded[u % kStaging]
+  DevBuf pinned[kStaging];
+  hipEvent_t uploaded[kStaging] = {};
+  int64_t event_upload[kStaging];  // the upload each event follows (-1: none yet)
+  int64_t uploads = 0;             // uploads issued so far
 
   // device side
   DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu | final_tile]
@@ -116,7 +127,7 @@ hsap_status grow_pinned(DevBuf& b, size_t bytes) {
 }
 
 void release(hsap_executor* ex) {
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < kStaging; ++i) {
     if (ex->pinned[i].p) hipHostFree(ex->pinned[i].p);
     if (ex->uploaded[i]) hipEventDestroy(ex->uploaded[i]);
   }
@@ -173,7 +184,9 @@ hsap_status hsap_executor_create(const hsap_attn_desc* desc, int32_t options, in
   int cus = 0;
   hipError_t e = hipGetDevice(&ex->device);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ex->device);
-  for (int i = 0; e == hipSuccess && i < 2; ++i) e = hipEventCreateWithFlags(&ex->uploaded[i], hipEventDisableTiming);
+  for (int i = 0; i < kStaging; ++i) ex->event_upload[i] = -1;
+  for (int i = 0; e == hipSuccess && i < kStaging; ++i)
+    e = hipEventCreateWithFlags(&ex->uploaded[i], hipEventDisableTiming);
   if (e == hipSuccess && (options & HSAP_EXEC_BACKWARD))
     e = hipMalloc((void**)&ex->doc_start, (size_t)g.N * sizeof(int32_t));
   if (e == hipSuccess && (options & HSAP_EXEC_BACKWARD))
@@ -305,9 +318,12 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   const size_t w_ft = words16(((size_t)ex->nq + 3) / 4);
   const size_t o_rq = w_tq, o_tk = o_rq + w_rq, o_rk = o_tk + w_tk, o_ta = o_rk + w_rk, o_ra = o_ta + w_ta,
                o_cu = o_ra + w_ra, o_ft = o_cu + w_cu, words = o_ft + w_ft;
-  const int slot = ex->next_slot;
-  if (ex->recorded[slot]) {
-    const hipError_t e = hipEventSynchronize(ex->uploaded[slot]);
+  const int64_t u = ex->uploads;
+  const int slot = (int)(u % kStaging);
+  if (u >= kStaging) {  // the buffer last served upload u - kStaging
+    const int64_t prev = u - kStaging, ev = prev + (kEventEvery - 1 - prev % kEventEvery);
+    if (ex->event_upload[ev % kStaging] != ev) HSAP_FAIL(HSAP_ERR_HIP, "executor: staging event bookkeeping");
+    const hipError_t e = hipEventSynchronize(ex->uploaded[ev % kStaging]);
     if (e != hipSuccess) return hip_fail("staging wait", e);
   }
   st = grow_pinned(ex->pinned[slot], words * 4);
@@ -328,10 +344,12 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   std::memcpy(h + o_ft, ex->final_tile.data(), (size_t)ex->nq);
   hipError_t e = hipMemcpyAsync(ex->lists.p, h, words * 4, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail("list upload", e);
-  e = hipEventRecord(ex->uploaded[slot], stream);
-  if (e != hipSuccess) return hip_fail("event record", e);
-  ex->recorded[slot] = true;
-  ex->next_slot = slot ^ 1;
+  if (u % kEventEvery == kEventEvery - 1) {
+    e = hipEventRecord(ex->uploaded[slot], stream);
+    if (e != hipSuccess) return hip_fail("event record", e);
+    ex->event_upload[slot] = u;
+  }
+  ex->uploads = u + 1;
 
   int32_t* d = (int32_t*)ex->lists.p;
   ex->d_tiles_q = (const hsap_tile*)d;

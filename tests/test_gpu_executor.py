@@ -131,6 +131,44 @@ def test_executor_replans_other_batches():
     assert np.array_equal(results[0][0], results[3][0]) and np.array_equal(results[0][1], results[3][1])
 
 
+def test_executor_many_plans_in_flight():
+    """Forty plans of three different batches issued back to back with no synchronisation (the
+    host runs ahead and reuses its pinned staging buffers while earlier uploads may still be in
+    flight), each forward into its own outputs: every result equals, bit for bit, the first
+    result of the same batch, and those meet the oracle."""
+    N, P, layout, hq, hkv, d, bm, bn = 2048, 2, "contiguous", 2, 2, 128, 128, 128
+    r = 1
+    rng = np.random.default_rng(11)
+    batches = [_cu(rng, N, 40), _cu(rng, N, 300), np.array([0, N], dtype=np.int32)]
+    s = L.shard_desc(N, P, layout, r, bm, bn)
+    desc = L.attn_desc(s, hq, hkv, d, 1.0 / np.sqrt(d))
+    ex = L.Executor(desc, backward=False, fused=False, max_run_tiles=-1)
+    dev = torch.device("cuda")
+    c0 = Case(batches[0], N, P, layout, r, hq, hkv, d, bm, bn, seed=5)
+    q_sh = to_sharded(s, c0.q.to(dev))[r].contiguous()
+    k_sh, v_sh = to_sharded(s, c0.k.to(dev)), to_sharded(s, c0.v.to(dev))
+    n = N // P
+    outs = []
+    try:
+        for i in range(40):
+            ex.plan(batches[i % 3])
+            o = torch.full((n, hq, d), float("nan"), dtype=torch.bfloat16, device=dev)
+            lse = torch.full((hq, n), float("nan"), dtype=torch.float32, device=dev)
+            ex.forward(q_sh, k_sh, v_sh, o, lse)
+            outs.append((o, lse))
+        torch.cuda.synchronize()
+    finally:
+        ex.close()
+    got = [(o.float().cpu().numpy(), lse.cpu().numpy()) for o, lse in outs]
+    for b in range(3):
+        ref = Case(batches[b], N, P, layout, r, hq, hkv, d, bm, bn, seed=5).run_oracle()
+        rep = {"o": max_abs(got[b][0], ref["o"]), "lse": max_abs(got[b][1], ref["lse"])}
+        _say("batch", b, rep)
+        assert rep["o"] <= O_ATOL and rep["lse"] <= LSE_ATOL, rep
+        for i in range(b + 3, 40, 3):
+            assert np.array_equal(got[i][0], got[b][0]) and np.array_equal(got[i][1], got[b][1]), (b, i)
+
+
 def test_executor_rejects_misuse():
     s = L.shard_desc(2048, 2, "contiguous", 0, 128, 128)
     desc = L.attn_desc(s, 2, 2, 128, 0.1)
