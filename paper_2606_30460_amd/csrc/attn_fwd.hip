@@ -305,60 +305,72 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
     // scores of the next step: independent of this step's softmax
     if (s + 1 < total) scores(PAR ^ 1, sn);
 
+    // Masked tile: a step whose keys no query of the wave may see is skipped (all its
+    // probabilities would be 0: the running max, sum and O stay as they are), and one whose keys
+    // every query of the wave may see needs no per-element mask.
+    bool live = true;
     if (tile.kind == HSAP_TILE_MASKED) {
-      // key row of register j: rel0 + 32 nb + c_row(j, hi), with the lane's 4 hi folded in once
-      const int32_t rel0 = (int32_t)global_pos(a.geom, tile.chunk, step_row0(tile, s)) - qstart + 4 * hi;
+      const int32_t r = (int32_t)global_pos(a.geom, tile.chunk, step_row0(tile, s)) - qstart;  // offset of key 0
+      const bool none = r > (int32_t)span || r + (KB - 1) < 0;
+      const bool all = r >= 0 && r + (KB - 1) <= (int32_t)span;
+      live = __builtin_amdgcn_ballot_w64(!none) != 0;
+      if (live && __builtin_amdgcn_ballot_w64(!all) != 0) {
+        // key row of register j: r + 32 nb + c_row(j, hi), with the lane's 4 hi folded in once
+        const int32_t rel0 = r + 4 * hi;
+#pragma unroll
+        for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j)
+            if ((uint32_t)(rel0 + (32 * nb + c_row(j, 0))) > span) sc[nb][j] = NEG_INF;
+      }
+    }
+    if (live) {
+      // online softmax (this lane's row = its query; lanes l and l ^ 32 share it)
+      float mx = sc[0][0];
 #pragma unroll
       for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if ((uint32_t)(rel0 + (32 * nb + c_row(j, 0))) > span) sc[nb][j] = NEG_INF;
-    }
-    // online softmax (this lane's row = its query; lanes l and l ^ 32 share it)
-    float mx = sc[0][0];
+        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
+      const float m_new = fmaxf(m_run, pair_max(mx) * sl);
+      // The reference max only has to bound the scores loosely: O / l and
+      // m + log2(l) do not depend on it.  Rescale only when some row's max rose
+      // by more than RESCALE_SLACK (p then stays below 2^RESCALE_SLACK).
+      if (__builtin_amdgcn_ballot_w64(m_new > m_run + RESCALE_SLACK) != 0) {
+        const float alpha = fast_exp2(m_run - (m_new == NEG_INF ? 0.f : m_new));
+        l_run *= alpha;
 #pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
-    const float m_new = fmaxf(m_run, pair_max(mx) * sl);
-    // The reference max only has to bound the scores loosely: O / l and
-    // m + log2(l) do not depend on it.  Rescale only when some row's max rose
-    // by more than RESCALE_SLACK (p then stays below 2^RESCALE_SLACK).
-    if (__builtin_amdgcn_ballot_w64(m_new > m_run + RESCALE_SLACK) != 0) {
-      const float alpha = fast_exp2(m_run - (m_new == NEG_INF ? 0.f : m_new));
-      l_run *= alpha;
-#pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
-      m_run = m_new;
-    }
-    const float m_use = m_run == NEG_INF ? 0.f : m_run;
-    float rs = 0.f;
-    bf16x8 pb[KB / 32][2];
-#pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const float p = fast_exp2(__builtin_fmaf(sc[nb][j], sl, -m_use));
-        rs += p;
-        pb[nb][j >> 3][j & 7] = (__bf16)p;
+        for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+        m_run = m_new;
       }
-    l_run += rs;  // the half-row sums of lanes l and l ^ 32 are combined once, at the end
-
-    // O^T += V^T P^T, 16 keys per MFMA
-    const __bf16* V = Vs[PAR];
+      const float m_use = m_run == NEG_INF ? 0.f : m_run;
+      float rs = 0.f;
+      bf16x8 pb[KB / 32][2];
 #pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb)
+      for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int r0 = 32 * nb + 16 * half + tr_row;
-#pragma unroll
-        for (int mb = 0; mb < D / 32; ++mb) {
-          const __bf16* vp = V + r0 * VS + 32 * mb + tr_col;
-          const bf16x8 av = cat4(ds_read_tr16(vp), ds_read_tr16(vp + 8 * VS));
-          o[mb] = mfma32(av, pb[nb][half], o[mb]);
+        for (int j = 0; j < 16; ++j) {
+          const float p = fast_exp2(__builtin_fmaf(sc[nb][j], sl, -m_use));
+          rs += p;
+          pb[nb][j >> 3][j & 7] = (__bf16)p;
         }
-      }
+      l_run += rs;  // the half-row sums of lanes l and l ^ 32 are combined once, at the end
 
+      // O^T += V^T P^T, 16 keys per MFMA
+      const __bf16* V = Vs[PAR];
+#pragma unroll
+      for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int r0 = 32 * nb + 16 * half + tr_row;
+#pragma unroll
+          for (int mb = 0; mb < D / 32; ++mb) {
+            const __bf16* vp = V + r0 * VS + 32 * mb + tr_col;
+            const bf16x8 av = cat4(ds_read_tr16(vp), ds_read_tr16(vp + 8 * VS));
+            o[mb] = mfma32(av, pb[nb][half], o[mb]);
+          }
+        }
+
+    }
     if (s + 2 < total) store_k(PAR);
     if (s + 1 < total) store_v(PAR ^ 1);
     __syncthreads();
@@ -574,53 +586,65 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     if (ldv) stage(a.v + step_off(tile_at(s + NSLOT - 1), s + NSLOT - 1), Vs[sv]);
     if (s + 1 < total) scores(Ks[s1], sn);
 
+    // Masked tile: a step whose keys no query of the wave may see is skipped (all its
+    // probabilities would be 0: the running max, sum and O stay as they are), and one whose keys
+    // every query of the wave may see needs no per-element mask.
+    bool live = true;
     if (tile >> 31) {  // MASKED
-      // key row of register j: rel0 + 32 nb + c_row(j, hi), with the lane's 4 hi folded in once
-      const int32_t rel0 = (int32_t)global_pos(a.geom, chunk_of(tile), step_row0(tile, s)) - qstart + 4 * hi;
+      const int32_t r = (int32_t)global_pos(a.geom, chunk_of(tile), step_row0(tile, s)) - qstart;  // offset of key 0
+      const bool none = r > (int32_t)span || r + (KB - 1) < 0;
+      const bool all = r >= 0 && r + (KB - 1) <= (int32_t)span;
+      live = __builtin_amdgcn_ballot_w64(!none) != 0;
+      if (live && __builtin_amdgcn_ballot_w64(!all) != 0) {
+        // key row of register j: r + 32 nb + c_row(j, hi), with the lane's 4 hi folded in once
+        const int32_t rel0 = r + 4 * hi;
+#pragma unroll
+        for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j)
+            if ((uint32_t)(rel0 + (32 * nb + c_row(j, 0))) > span) sc[nb][j] = NEG_INF;
+      }
+    }
+    if (live) {
+      float mx = sc[0][0];
 #pragma unroll
       for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if ((uint32_t)(rel0 + (32 * nb + c_row(j, 0))) > span) sc[nb][j] = NEG_INF;
-    }
-    float mx = sc[0][0];
+        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
+      const float m_new = fmaxf(m_run, pair_max(mx) * a.scale_log2);
+      if (__builtin_amdgcn_ballot_w64(m_new > m_run + RESCALE_SLACK) != 0) {
+        const float alpha = fast_exp2(m_run - (m_new == NEG_INF ? 0.f : m_new));
+        l_run *= alpha;
 #pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
-    const float m_new = fmaxf(m_run, pair_max(mx) * a.scale_log2);
-    if (__builtin_amdgcn_ballot_w64(m_new > m_run + RESCALE_SLACK) != 0) {
-      const float alpha = fast_exp2(m_run - (m_new == NEG_INF ? 0.f : m_new));
-      l_run *= alpha;
-#pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
-      m_run = m_new;
-    }
-    const float m_use = m_run == NEG_INF ? 0.f : m_run;
-    float rs = 0.f;
-    bf16x8 pb[KB / 32][2];
-#pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const float p = fast_exp2(__builtin_fmaf(sc[nb][j], a.scale_log2, -m_use));
-        rs += p;
-        pb[nb][j >> 3][j & 7] = (__bf16)p;
+        for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+        m_run = m_new;
       }
-    l_run += rs;
-
-    const __bf16* V = Vs[s0];
+      const float m_use = m_run == NEG_INF ? 0.f : m_run;
+      float rs = 0.f;
+      bf16x8 pb[KB / 32][2];
 #pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb)
+      for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int rb = (32 * nb + 16 * half) * D;
-#pragma unroll
-        for (int mb = 0; mb < D / 32; ++mb) {
-          const bf16x8 av = cat4(ds_read_tr16(V + rb + troff[mb][0]), ds_read_tr16(V + rb + 8 * D + troff[mb][1]));
-          o[mb] = mfma32(av, pb[nb][half], o[mb]);
+        for (int j = 0; j < 16; ++j) {
+          const float p = fast_exp2(__builtin_fmaf(sc[nb][j], a.scale_log2, -m_use));
+          rs += p;
+          pb[nb][j >> 3][j & 7] = (__bf16)p;
         }
-      }
+      l_run += rs;
+
+      const __bf16* V = Vs[s0];
+#pragma unroll
+      for (int nb = 0; nb < KB / 32; ++nb)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int rb = (32 * nb + 16 * half) * D;
+#pragma unroll
+          for (int mb = 0; mb < D / 32; ++mb) {
+            const bf16x8 av = cat4(ds_read_tr16(V + rb + troff[mb][0]), ds_read_tr16(V + rb + 8 * D + troff[mb][1]));
+            o[mb] = mfma32(av, pb[nb][half], o[mb]);
+          }
+        }
+    }
     // K(s + 2) and V(s + 1) must have landed before the next step.  Three slots: they were
     // issued one step ago, and this step's own transfers (U instructions each) stay in flight.
     // Two slots: they are this step's transfers.
