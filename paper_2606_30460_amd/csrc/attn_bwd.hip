@@ -20,6 +20,8 @@
 // the next sub-tile's rows loading into registers while the current one
 // computes.  Each (chunk, k-tile, K/V head) block of dK/dV has one owner.
 //
+#include <type_traits>
+
 #include "hsap_internal.h"
 #include "mfma.h"
 
@@ -310,8 +312,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
   constexpr int NT = 64 * WAVES;
   constexpr int CPR = D / 8;
   constexpr int MB = D / 32;
-  constexpr int CHUNKS = KB * CPR;
-  constexpr int PER_T = CHUNKS / NT;
+  constexpr int CHUNKS = KB * CPR;           // 16-byte chunks per K (or V) step
   static_assert(CHUNKS % NT == 0, "step must split evenly over the threads");
   constexpr float LOG2E = 1.44269504088896340736f;
   constexpr float NEG_INF = -__builtin_inff();
@@ -361,87 +362,130 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
 
   const int64_t rstride = (int64_t)a.hkv * D;
   const int total = run.count * SUBS;
-  int32_t goff[PER_T], loff[PER_T];
-#pragma unroll
-  for (int i = 0; i < PER_T; ++i) {
-    const int idx = tid + i * NT, row = idx / CPR, cc = idx % CPR;
-    goff[i] = (int32_t)(row * rstride + cc * 8);
-    loff[i] = swz<CPR>(row, cc * 8);
-  }
-  bf16x8 kreg[PER_T], vreg[PER_T];
-  auto step_row0 = [&](const hsap_tile& t, int s) { return (int64_t)t.k_tile * BN + (s % SUBS) * KB; };
-  // the step's rows in the sharded K/V buffers: chunk t.chunk, K/V head g
-  auto load_step = [&](const hsap_tile& t, int s) {
-    const int64_t off = (((int64_t)t.chunk * n + step_row0(t, s)) * a.hkv + g) * D;
-    const __bf16* kb = a.k + off;
-    const __bf16* vb = a.v + off;
-#pragma unroll
-    for (int i = 0; i < PER_T; ++i) {
-      kreg[i] = *(const bf16x8*)(kb + goff[i]);
-      vreg[i] = *(const bf16x8*)(vb + goff[i]);
+  // The run's tile descriptors, packed one per lane (k_tile | chunk << 23 | kind << 31) in windows
+  // of 64 tiles (window v in win0 or win1 by parity), read with v_readlane: the loop issues no
+  // vector load besides the transfers (one would wait for every transfer in flight).
+  uint32_t win0 = 0u, win1 = 0u;
+  int win_hi = -1;
+  auto load_window = [&](int v) {
+    const int i = 64 * v + lane;
+    uint32_t p = 0;
+    if (i < run.count) {
+      const hsap_tile t = a.tiles[run.first + i];
+      p = (uint32_t)t.k_tile | ((uint32_t)t.chunk << 23) | ((uint32_t)t.kind << 31);
     }
+    if (v & 1) win1 = p;
+    else win0 = p;
+    win_hi = v;
   };
-  auto store_step = [&](int buf) {
+  auto tile_at = [&](int s) -> uint32_t {
+    const int idx = s / SUBS;
+    return __builtin_amdgcn_readlane(((idx >> 6) & 1) ? win1 : win0, idx & 63);
+  };
+  auto chunk_of = [](uint32_t p) { return (int32_t)((p >> 23) & 0xFFu); };
+  auto step_row0 = [&](uint32_t p, int s) { return (int64_t)(p & 0x7FFFFFu) * BN + (s % SUBS) * KB; };
+  // the step's first row in the sharded K/V buffers: chunk of the tile, K/V head g
+  auto step_off = [&](uint32_t p, int s) { return (((int64_t)chunk_of(p) * n + step_row0(p, s)) * a.hkv + g) * D; };
+  load_window(0);
+
+  // K and V steps go from global memory straight into LDS (global_load_lds) in a two-slot ring of
+  // swizzled tiles: the next step's transfers are issued at the start of a step into the slot the
+  // previous step read, and have landed at the step's closing barrier.  Instruction u of wave w
+  // fills chunk positions p = WCH w + 64 u + lane; the lane's source is the chunk the swizzle
+  // places there, a 32-bit byte offset from the step's scalar base.
+  constexpr int WCH = CHUNKS / WAVES, U = WCH / 64;
+  static_assert(WCH % 64 == 0, "a wave moves whole instructions of a tile");
+  uint32_t gsrc[U];
 #pragma unroll
-    for (int i = 0; i < PER_T; ++i) {
-      *(bf16x8*)(&Ks[buf][loff[i]]) = kreg[i];
-      *(bf16x8*)(&Vs[buf][loff[i]]) = vreg[i];
-    }
+  for (int u = 0; u < U; ++u) {
+    const int p = WCH * w + 64 * u + lane, row = p / CPR;
+    gsrc[u] = (uint32_t)((row * rstride + swz_chunk<CPR>(row, p % CPR) * 8) * 2);
+  }
+  typedef __attribute__((address_space(3))) void* lds_void;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  auto stage = [&](const __bf16* src, __bf16* dst) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(lds_void)dst + (uint32_t)(WCH * wu * 16);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds + 64 * 16 * u), "v"(gsrc[u]),
+                   "s"(src)
+                   : "m0");
   };
 
   f32x16 dq[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) dq[mb] = f32x16{};
 
-  hsap_tile cur = a.tiles[run.first];
-  load_step(cur, 0);
-  store_step(0);
-  hsap_tile nxt = cur;
-  if (run.count > 1) nxt = a.tiles[run.first + 1];
-  __syncthreads();
+  {
+    const int64_t off = step_off(tile_at(0), 0);
+    stage(a.k + off, Ks[0]);
+    stage(a.v + off, Vs[0]);
+  }
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
 
-  for (int s = 0; s < total; ++s) {
-    const int buf = s & 1;
-    const hsap_tile tile = cur;
+  // one 64-key step from slot PAR (= s % 2, a compile-time constant, so every slot address is an
+  // immediate); the next step's transfers go to the other slot
+  auto step = [&](int s, auto par) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(par)::value;
+    if (s + 1 < total && ((s + 1) / SUBS) >> 6 > win_hi) load_window(win_hi + 1);
+    const uint32_t tile = tile_at(s);
     if (s + 1 < total) {
-      if ((s + 1) % SUBS == 0) {
-        cur = nxt;
-        if ((s + 1) / SUBS + 1 < run.count) nxt = a.tiles[run.first + (s + 1) / SUBS + 1];
-      }
-      load_step(cur, s + 1);
+      const int64_t off = step_off(tile_at(s + 1), s + 1);
+      stage(a.k + off, Ks[PAR ^ 1]);
+      stage(a.v + off, Vs[PAR ^ 1]);
     }
-    const __bf16* K = Ks[buf];
-    const __bf16* V = Vs[buf];
-    const bool masked = tile.kind == HSAP_TILE_MASKED;
-    const int32_t rel0 = masked ? (int32_t)global_pos(a.geom, tile.chunk, step_row0(tile, s)) - qstart : 0;
+    const __bf16* K = Ks[PAR];
+    const __bf16* V = Vs[PAR];
+    // Masked tile: a step whose keys no query of the wave may see contributes nothing (skipped);
+    // one whose keys every query of the wave may see needs no per-element mask.
+    bool live = true, need_mask = false;
+    int32_t rel0 = 0;  // key row of register j: rel0 + 32 nb + c_row(j, 0)
+    if (tile >> 31) {
+      const int32_t r = (int32_t)global_pos(a.geom, chunk_of(tile), step_row0(tile, s)) - qstart;
+      const bool none = r > (int32_t)span || r + (KB - 1) < 0;
+      const bool all = r >= 0 && r + (KB - 1) <= (int32_t)span;
+      live = __builtin_amdgcn_ballot_w64(!none) != 0;
+      need_mask = live && __builtin_amdgcn_ballot_w64(!all) != 0;
+      rel0 = r + 4 * hi;
+    }
+    if (live) {
 #pragma unroll
-    for (int nb = 0; nb < KB / 32; ++nb) {
-      f32x16 st{}, dpt{};
+      for (int nb = 0; nb < KB / 32; ++nb) {
+        f32x16 st{}, dpt{};
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        st = mfma32(*(const bf16x8*)(K + 32 * nb * D + rowoff[kk]), qf[kk], st);
-        dpt = mfma32(*(const bf16x8*)(V + 32 * nb * D + rowoff[kk]), of[kk], dpt);
-      }
-      bf16x8 sb[2];
+        for (int kk = 0; kk < D / 16; ++kk) {
+          st = mfma32(*(const bf16x8*)(K + 32 * nb * D + rowoff[kk]), qf[kk], st);
+          dpt = mfma32(*(const bf16x8*)(V + 32 * nb * D + rowoff[kk]), of[kk], dpt);
+        }
+        float p[16];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        float p = fast_exp2(__builtin_fmaf(st[j], a.scale_log2, -lse2));
-        if (masked && (uint32_t)(rel0 + 32 * nb + c_row(j, hi)) > span) p = 0.f;
-        sb[j >> 3][j & 7] = (__bf16)(p * (dpt[j] - dlt));
-      }
-      // dQ^T += K^T dS^T, 16 keys per MFMA
+        for (int j = 0; j < 16; ++j) p[j] = fast_exp2(__builtin_fmaf(st[j], a.scale_log2, -lse2));
+        if (need_mask) {  // uniform branch: the mask costs nothing on steps that need none
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int rb = (32 * nb + 16 * half) * D;
+          for (int j = 0; j < 16; ++j)
+            if ((uint32_t)(rel0 + (32 * nb + c_row(j, 0))) > span) p[j] = 0.f;
+        }
+        bf16x8 sb[2];
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          const bf16x8 ka = cat4(ds_read_tr16(K + rb + troff[mb][0]), ds_read_tr16(K + rb + 8 * D + troff[mb][1]));
-          dq[mb] = mfma32(ka, sb[half], dq[mb]);
+        for (int j = 0; j < 16; ++j) sb[j >> 3][j & 7] = (__bf16)(p[j] * (dpt[j] - dlt));
+        // dQ^T += K^T dS^T, 16 keys per MFMA
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int rb = (32 * nb + 16 * half) * D;
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const bf16x8 ka = cat4(ds_read_tr16(K + rb + troff[mb][0]), ds_read_tr16(K + rb + 8 * D + troff[mb][1]));
+            dq[mb] = mfma32(ka, sb[half], dq[mb]);
+          }
         }
       }
     }
-    if (s + 1 < total) store_step(buf ^ 1);
-    __syncthreads();
+    // every read of slot PAR is done and the transfers into slot PAR ^ 1 have landed
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  };
+  for (int s = 0; s < total; s += 2) {
+    step(s, std::integral_constant<int, 0>{});
+    if (s + 1 < total) step(s + 1, std::integral_constant<int, 1>{});
   }
 
   // dQ^T: this lane's query, d = 32 mb + 8 grp + 4 hi + e for register j = 4 grp + e
