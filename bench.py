@@ -349,7 +349,7 @@ def all_shards_analysis(name: str, layouts=None, reps: int = 5) -> dict:
     return out
 
 
-def fp8_analysis(name: str, reps: int = 20) -> dict:
+def fp8_analysis(name: str, reps: int = 50) -> dict:
     """The fp8 score variant on the workload's shard: e4m3 quantisation of Q and of every chunk's K
     (hsap_quantize_fp8), then the partial forward with fp8 scores (hsap_partial_attn_fwd_fp8) over
     the same plan as the bf16 partial forward, which is timed beside it; back-to-back launches
@@ -378,9 +378,12 @@ def fp8_analysis(name: str, reps: int = 20) -> dict:
     work = torch.empty(w.sp_degree * max(w.heads_q, w.heads_kv) * L.QUANT_SPLIT, dtype=torch.float32, device=dev)
     bufs = sa.alloc_forward()
 
-    def timed(fn):
-        for _ in range(3):
-            fn()
+    def timed(fn):  # about 30 ms of launches first (clocks settle under sustained load)
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 0.03:
+            for _ in range(5):
+                fn()
+            torch.cuda.synchronize()
         e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         e[0].record()
         for _ in range(reps):

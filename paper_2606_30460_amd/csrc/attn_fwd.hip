@@ -37,6 +37,10 @@ namespace hsap {
 // is ignored by untyped loads, but a zero format makes them return zeros).
 constexpr int kBufferWord3 = 0x00020000;
 
+// The direct-to-LDS kernel packs a tile descriptor as k_tile | chunk << 23 | kind << 31.
+constexpr int kMaxDlChunks = 256;
+constexpr int64_t kMaxDlKTiles = int64_t(1) << 23;
+
 struct FwdArgs {
   const __bf16* q;
   const __bf16* k;
@@ -422,17 +426,24 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 // 1024 16-byte chunks, 64 per instruction; a lane's source chunk is the one
 // the swizzle places at its destination.
 // ---------------------------------------------------------------------------
-template <int BN, int WAVES, bool FUSED>
+// FP8: Q and K are e4m3 codes (scores from the 32x32x64 fp8 MFMA times q_scale[h] *
+// k_scale[chunk, g]); K tiles are [64][128 bytes], swizzled over their 8 chunks per row.
+template <int BN, int WAVES, bool FUSED, bool FP8 = false>
 __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   static_assert(WAVES == 4 || WAVES == 8, "four or eight waves");
+  using KT = std::conditional_t<FP8, uint8_t, __bf16>;  // K element
   constexpr int D = 128, KB = 64, SUBS = BN / KB, CPR = D / 8, TILE = KB * D;
+  constexpr int KCPR = D * (int)sizeof(KT) / 16;        // 16-byte chunks per K row
   constexpr int NSLOT = WAVES == 8 ? 3 : 2;  // ring depth
-  constexpr int WCH = TILE / 8 / WAVES;      // 16-byte chunks a wave moves per tile
-  constexpr int U = WCH / 64;                // transfer instructions per wave per tile
+  constexpr int WCH = TILE / 8 / WAVES;      // 16-byte chunks of a V tile a wave moves
+  constexpr int U = WCH / 64;                // transfer instructions per wave per V tile
+  constexpr int WCHK = KB * KCPR / WAVES, UK = WCHK / 64;  // the same for a K tile
+  static_assert(WCHK % 64 == 0, "a wave moves whole instructions of a K tile");
   constexpr float NEG_INF = -__builtin_inff();
   constexpr float RESCALE_SLACK = 8.f;
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[NSLOT][TILE];
+  __shared__ __attribute__((aligned(16))) KT Ks[NSLOT][TILE];
   __shared__ __attribute__((aligned(16))) __bf16 Vs[NSLOT][TILE];
+  __shared__ float kscale_s[FP8 ? kMaxDlChunks : 1];  // fp8: K scale of each chunk for this head's K/V head
   typedef __attribute__((address_space(3))) void* lds_void;
 
   const int tid = threadIdx.x;
@@ -462,11 +473,24 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   const int32_t gq = (int32_t)global_pos(a.geom, a.shard, qrow);
   const DocWindow docw = doc_window(a, gq, lane);
   bf16x8 qf[D / 16];
-  {
+  i32x8 qf8[2];  // fp8: lane half hi holds bytes 64 kk + 32 hi .. +31 of its query's row
+  if constexpr (FP8) {
+    const uint8_t* qp = (const uint8_t*)a.q + (qrow * a.hq + h) * D + 32 * hi;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const uint4 lo = *(const uint4*)(qp + 64 * kk), hi4 = *(const uint4*)(qp + 64 * kk + 16);
+      qf8[kk] = i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi4.x, (int)hi4.y, (int)hi4.z, (int)hi4.w};
+    }
+  } else {
     const __bf16* qp = a.q + (qrow * a.hq + h) * D + 8 * hi;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
   }
+  // exp2 argument scale of this head (fp8: times the chunk's K scale each step, from LDS, filled
+  // here and visible after the prologue's barrier)
+  const float head_scale = FP8 ? a.scale_log2 * a.q_scale[h] : a.scale_log2;
+  if constexpr (FP8)
+    for (int c = tid; c < a.geom.P; c += 64 * WAVES) kscale_s[c] = a.k_scale[c * a.hkv + (h / a.group)];
   const int64_t rstride = (int64_t)a.hkv * D;
   const int total = run.count * SUBS;
   // The run's tile descriptors, packed one per lane (k_tile | chunk << 23 | kind << 31) in
@@ -501,11 +525,16 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
 
   // direct staging: instruction u of wave w fills chunk positions p = WCH w + 64 u + lane; the
   // lane's source is a 32-bit byte offset from the step's (scalar) base pointer
-  uint32_t gsrc[U];
+  uint32_t gsrc[U], gsrck[UK];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int p = WCH * w + 64 * u + lane, row = p >> 4;
     gsrc[u] = (uint32_t)((row * rstride + swz_chunk<CPR>(row, p & 15) * 8) * 2);
+  }
+#pragma unroll
+  for (int u = 0; u < UK; ++u) {
+    const int p = WCHK * w + 64 * u + lane, row = p / KCPR;
+    gsrck[u] = (uint32_t)(row * rstride * (int)sizeof(KT) + swz_chunk<KCPR>(row, p % KCPR) * 16);
   }
   // issued from asm: the transfers are ordered by the explicit vmcnt waits of the ring below (the
   // compiler would otherwise wait for each one before any later LDS read).  No memory clobber:
@@ -522,6 +551,15 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
                    "s"(src)
                    : "m0");
   };
+  auto stage_k = [&](const KT* src, KT* dst) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(lds_void)dst + (uint32_t)(WCHK * wu * 16);
+#pragma unroll
+    for (int u = 0; u < UK; ++u)
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds + 64 * 16 * u), "v"(gsrck[u]),
+                   "s"(src)
+                   : "m0");
+  };
+  const KT* kbase = (const KT*)a.k;
 
   // operand offsets in a swizzled tile: K rows (row l32 of a 32-row block, chunk 2 kk + hi) and
   // V transpose reads (rows 8 k + tr_row of a 16-row block, columns 32 mb + tr_col)
@@ -535,15 +573,33 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
 #pragma unroll
     for (int k = 0; k < 2; ++k) troff[mb][k] = swz<CPR>(8 * k + tr_row, 32 * mb + tr_col) - 8 * k * D;
 
-  auto scores = [&](const __bf16* K, f32x16 (&sc)[KB / 32]) {
+  // fp8 K reads: the K row's bytes 64 kk + 32 hi .. +31 (chunks 4 kk + 2 hi and the next) pair
+  // with the same bytes of the query's row; byte offsets in the swizzled tile for row l32 (a
+  // 32-row block further down keeps the swizzle)
+  int koff8[2][2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) koff8[kk][c] = l32 * 128 + swz_chunk<8>(l32, 4 * kk + 2 * hi + c) * 16;
+  auto scores = [&](const KT* K, f32x16 (&sc)[KB / 32]) {
 #pragma unroll
     for (int nb = 0; nb < KB / 32; ++nb) {
-      bf16x8 kf[D / 16];
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(K + 32 * nb * D + rowoff[kk]);
       sc[nb] = f32x16{};
+      if constexpr (FP8) {
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) sc[nb] = mfma32(kf[kk], qf[kk], sc[nb]);
+        for (int kk = 0; kk < 2; ++kk) {
+          const uint4 lo = *(const uint4*)(K + 32 * nb * 128 + koff8[kk][0]);
+          const uint4 hi4 = *(const uint4*)(K + 32 * nb * 128 + koff8[kk][1]);
+          const i32x8 kf{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi4.x, (int)hi4.y, (int)hi4.z, (int)hi4.w};
+          sc[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf, qf8[kk], sc[nb], 0, 0, 0, 127, 0, 127);
+        }
+      } else {
+        bf16x8 kf[D / 16];
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(K + 32 * nb * D + rowoff[kk]);
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) sc[nb] = mfma32(kf[kk], qf[kk], sc[nb]);
+      }
     }
   };
 
@@ -557,7 +613,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   for (int j = 0; j < NSLOT; ++j)
     if (j < total) {
       const uint32_t t = tile_at(j);
-      stage(a.k + step_off(t, j), Ks[j]);
+      stage_k(kbase + step_off(t, j), Ks[j]);
       if (j < NSLOT - 1) stage(a.v + step_off(t, j), Vs[j]);
     }
   asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
@@ -576,13 +632,14 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     // the window of tile (s + NSLOT) / SUBS is needed now (rare vector load: every 64 tiles)
     if (s + NSLOT < total && ((s + NSLOT) / SUBS) >> 6 > win_hi) load_window(win_hi + 1);
     const uint32_t tile = tile_at(s);
+    const float sl = FP8 ? head_scale * kscale_s[chunk_of(tile)] : head_scale;
     // s % NSLOT, (s + 1) % NSLOT and (s + NSLOT - 1) % NSLOT: this step's slot, the slot of the
     // next scores and of V's refill
     const int s0 = NSLOT == 2 ? PAR : sk;
     const int s1 = NSLOT == 2 ? PAR ^ 1 : (sk == NSLOT - 1 ? 0 : sk + 1);
     const int sv = NSLOT == 2 ? PAR ^ 1 : (sk == 0 ? NSLOT - 1 : sk - 1);
     const bool ldk = s + NSLOT < total, ldv = s + NSLOT - 1 < total;
-    if (ldk) stage(a.k + step_off(tile_at(s + NSLOT), s + NSLOT), Ks[s0]);
+    if (ldk) stage_k(kbase + step_off(tile_at(s + NSLOT), s + NSLOT), Ks[s0]);
     if (ldv) stage(a.v + step_off(tile_at(s + NSLOT - 1), s + NSLOT - 1), Vs[sv]);
     if (s + 1 < total) scores(Ks[s1], sn);
 
@@ -611,7 +668,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
       for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
         for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[nb][j]);
-      const float m_new = fmaxf(m_run, pair_max(mx) * a.scale_log2);
+      const float m_new = fmaxf(m_run, pair_max(mx) * sl);
       if (__builtin_amdgcn_ballot_w64(m_new > m_run + RESCALE_SLACK) != 0) {
         const float alpha = fast_exp2(m_run - (m_new == NEG_INF ? 0.f : m_new));
         l_run *= alpha;
@@ -626,7 +683,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
       for (int nb = 0; nb < KB / 32; ++nb)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const float p = fast_exp2(__builtin_fmaf(sc[nb][j], a.scale_log2, -m_use));
+          const float p = fast_exp2(__builtin_fmaf(sc[nb][j], sl, -m_use));
           rs += p;
           pb[nb][j >> 3][j & 7] = (__bf16)p;
         }
@@ -692,11 +749,12 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   }
 }
 
-template <int BN, int WAVES, bool FUSED>
+template <int BN, int WAVES, bool FUSED, bool FP8 = false>
 static hsap_status launch_dl(const FwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_fwd_dl_kernel<BN, WAVES, FUSED>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream, a);
+  hipLaunchKernelGGL((attn_fwd_dl_kernel<BN, WAVES, FUSED, FP8>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream,
+                     a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
   return HSAP_OK;
@@ -750,8 +808,15 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   a.hkv = desc->heads_kv;
   a.group = desc->heads_q / desc->heads_kv;
   a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
+  // head_dim 128 with 128- or 256-row q-tiles: the direct-to-LDS kernel, whose packed tile
+  // descriptors hold chunks below 256 and k-tiles below 2^23 (else the register-staged kernel)
+  const bool dl = d == 128 && (bm == 128 || bm == 256) && geom.P <= kMaxDlChunks && geom.n / bn < kMaxDlKTiles;
   if constexpr (FP8) {
     if ((uintptr_t)q & 15 || (uintptr_t)k & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "fp8 q and k must be 16-byte aligned");
+    if (dl && bm == 256)
+      return bn == 128 ? launch_dl<128, 8, FUSED, true>(a, num_runs, s) : launch_dl<64, 8, FUSED, true>(a, num_runs, s);
+    if (dl && bm == 128)
+      return bn == 128 ? launch_dl<128, 4, FUSED, true>(a, num_runs, s) : launch_dl<64, 4, FUSED, true>(a, num_runs, s);
     const int w = bm / 32;
     if (bn == 128) return w == 2 ? launch<128, 128, 2, FUSED, true>(a, num_runs, s)
                         : w == 4 ? launch<128, 128, 4, FUSED, true>(a, num_runs, s)
@@ -762,10 +827,13 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   } else {
 #define HSAP_FWD_CASE(D_, BN_, W_) \
   if (d == D_ && bn == BN_ && bm == 32 * W_) return launch<D_, BN_, W_, FUSED>(a, num_runs, s);
-  if (d == 128 && bm == 256)
+  if (dl && bm == 256)
     return bn == 128 ? launch_dl<128, 8, FUSED>(a, num_runs, s) : launch_dl<64, 8, FUSED>(a, num_runs, s);
-  if (d == 128 && bm == 128)
+  if (dl && bm == 128)
     return bn == 128 ? launch_dl<128, 4, FUSED>(a, num_runs, s) : launch_dl<64, 4, FUSED>(a, num_runs, s);
+  if (d == 128 && bm == 256)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "256-row q-tiles need sp_degree <= %d and fewer than 2^23 k-tiles per chunk",
+              kMaxDlChunks);
   HSAP_FWD_CASE(128, 128, 4)
   HSAP_FWD_CASE(128, 64, 4)
   HSAP_FWD_CASE(128, 128, 2)
