@@ -128,6 +128,18 @@ def test_forward_validates_before_launch(over, code):
     assert st == code, lib.hsap_last_error().decode()
 
 
+def test_forward_rejects_256_row_tiles_beyond_packed_descriptors():
+    # the direct-to-LDS kernel (the only 256-row one) packs a tile's chunk into 8 bits: more than
+    # 256 chunks are rejected before any launch (128-row tiles fall back to the register-staged
+    # kernel instead)
+    lib = L.lib()
+    fake = ctypes.c_void_p(4096)
+    d = _attn_desc(block_m=256, block_n=128, sp_degree=257, total_tokens=257 * 256)
+    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
+    assert st == L.HSAP_ERR_UNSUPPORTED, lib.hsap_last_error().decode()
+    assert "256" in lib.hsap_last_error().decode()
+
+
 def test_forward_rejects_null_and_misaligned():
     lib = L.lib()
     d = _attn_desc()
