@@ -429,7 +429,7 @@ def fwd_kernel_name(res) -> str:
     direct-to-LDS for head_dim 128 with 128- or 256-row q-tiles, register-staged otherwise."""
     d, bm, bn = res["head_dim"], res["block_m"], res["block_n"]
     if d == 128 and bm in (128, 256):
-        return "attn_fwd_dl_kernel<%d, %d, false>" % (bn, bm // 32)
+        return "attn_fwd_dl_kernel<%d, %d, false, false>" % (bn, bm // 32)
     return "attn_fwd_kernel<%d, %d, %d, false, false>" % (d, bn, bm // 32)
 
 

@@ -67,6 +67,17 @@ def test_forward_small(case):
         assert np.array_equal(gpu2["o"], gpu["o"]) and np.array_equal(gpu2["lse"], gpu["lse"])
 
 
+def test_forward_many_chunks():
+    # 260 chunks: beyond what the direct-to-LDS kernel's packed tile descriptors hold, so 128-row
+    # q-tiles of head_dim 128 run on the register-staged kernel; both shards' ends of the ring
+    N, P = 260 * 128, 260
+    cu = _rand_cu(np.random.default_rng(260), N, 1500)
+    for r in (3, P - 1):
+        _say("forward many chunks, shard", r)
+        c = Case(cu, N, P, "contiguous", r, 2, 2, 128, 128, 128, seed=r)
+        compare_forward(c.run_gpu(), c.run_oracle())
+
+
 @pytest.mark.parametrize("split", [0, 1, 3])
 def test_forward_split_runs(split):
     # long runs cut into pieces of at most `split` tiles (0: never) give the same result
