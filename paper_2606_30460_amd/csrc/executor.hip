@@ -57,6 +57,7 @@ struct hsap_executor {
   std::vector<int64_t> step_offsets, pairs;
   std::vector<int32_t> slot_map;
   std::vector<uint8_t> final_tile;  // per q-tile: 1 when its only part is written final by the partial forward
+  std::vector<int32_t> merged_tiles;  // the other q-tiles, in order: the merge's rows
 
   // pinned staging ring; upload u uses pinned[u % kStaging], and when u % kEventEvery is
   // kEventEvery - 1 an event recorded after its copy sits in uploaded[u % kStaging]
@@ -66,7 +67,7 @@ struct hsap_executor {
   int64_t uploads = 0;             // uploads issued so far
 
   // device side
-  DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu | final_tile]
+  DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu | merged_tiles]
   int32_t* doc_start = nullptr;  // start(t) per position, for the backward only
   DevBuf o_part, lse_part;
   float* delta = nullptr;
@@ -80,7 +81,7 @@ struct hsap_executor {
   const hsap_run* d_runs_k = nullptr;
   const hsap_tile* d_tiles_all = nullptr;
   const hsap_run* d_runs_all = nullptr;
-  const uint8_t* d_final_tile = nullptr;
+  const int32_t* d_merged_tiles = nullptr;
   const int32_t* d_cu = nullptr;  // the plan's cu_seqlens (the forwards search it for document starts)
   int32_t num_docs = 0;
   std::vector<uint8_t> chunk_has_tiles;
@@ -283,7 +284,11 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   ex->info.num_runs_q = RQ;
   ex->info.num_parts = parts;
   ex->info.final_q_tiles = 0;
-  for (uint8_t f : ex->final_tile) ex->info.final_q_tiles += f;
+  ex->merged_tiles.clear();
+  for (int64_t t = 0; t < ex->nq; ++t) {
+    if (ex->final_tile[(size_t)t]) ++ex->info.final_q_tiles;
+    else ex->merged_tiles.push_back((int32_t)t);
+  }
   ex->info.split_length = split;
   for (int32_t c = 0; c < P; ++c)
     if (ex->chunk_has_tiles[(size_t)c]) {
@@ -315,9 +320,9 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   const size_t w_tk = RK ? w_tq : 0, w_rk = words16((size_t)RK * 4);
   const size_t w_ta = RA ? w_tq : 0, w_ra = words16((size_t)RA * 4);
   const size_t w_cu = words16((size_t)num_docs + 1);
-  const size_t w_ft = words16(((size_t)ex->nq + 3) / 4);
+  const size_t w_mt = words16(ex->merged_tiles.size());
   const size_t o_rq = w_tq, o_tk = o_rq + w_rq, o_rk = o_tk + w_tk, o_ta = o_rk + w_rk, o_ra = o_ta + w_ta,
-               o_cu = o_ra + w_ra, o_ft = o_cu + w_cu, words = o_ft + w_ft;
+               o_cu = o_ra + w_ra, o_mt = o_cu + w_cu, words = o_mt + w_mt;
   const int64_t u = ex->uploads;
   const int slot = (int)(u % kStaging);
   if (u >= kStaging) {  // the buffer last served upload u - kStaging
@@ -341,7 +346,7 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
     std::memcpy(h + o_ra, ex->runs_all.data(), (size_t)RA * sizeof(hsap_run));
   }
   std::memcpy(h + o_cu, cu_seqlens, ((size_t)num_docs + 1) * sizeof(int32_t));
-  std::memcpy(h + o_ft, ex->final_tile.data(), (size_t)ex->nq);
+  std::memcpy(h + o_mt, ex->merged_tiles.data(), ex->merged_tiles.size() * sizeof(int32_t));
   hipError_t e = hipMemcpyAsync(ex->lists.p, h, words * 4, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail("list upload", e);
   if (u % kEventEvery == kEventEvery - 1) {
@@ -358,7 +363,7 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   ex->d_runs_k = RK ? (const hsap_run*)(d + o_rk) : nullptr;
   ex->d_tiles_all = RA ? (const hsap_tile*)(d + o_ta) : nullptr;
   ex->d_runs_all = RA ? (const hsap_run*)(d + o_ra) : nullptr;
-  ex->d_final_tile = (const uint8_t*)(d + o_ft);
+  ex->d_merged_tiles = d + o_mt;
   ex->d_cu = d + o_cu;
   ex->num_docs = num_docs;
 
@@ -405,7 +410,8 @@ hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, 
   }
   if (ex->info.final_q_tiles == ex->nq) return HSAP_OK;  // every q-tile was written final
   return lse_merge(parts, o_ptrs, l_ptrs, ex->geom.n, ex->desc.heads_q, ex->desc.head_dim, o_out, lse_out,
-                   ex->d_final_tile, ex->desc.shard.block_m, (hipStream_t)hip_stream);
+                   ex->d_merged_tiles, (int32_t)ex->merged_tiles.size(), ex->desc.shard.block_m,
+                   (hipStream_t)hip_stream);
 }
 
 hsap_status hsap_executor_forward(hsap_executor* ex, const void* q, const void* k, const void* v, int32_t fused,

@@ -71,11 +71,11 @@ hsap_status check_attn(const hsap_attn_desc* d, Geom* g);
 // of 4, dst 16-byte aligned).
 hsap_status zero_fill(void* dst, int64_t bytes, hipStream_t stream);
 
-// hsap_lse_merge with an optional per-q-tile skip flag (skip[row / block_m] != 0: the rows are
-// already final and are neither read nor written).
+// hsap_lse_merge over the rows of the BM-row q-tiles listed in tiles[0 .. num_tiles-1] (device
+// int32), or over every row when tiles is NULL; rows of other q-tiles are neither read nor written.
 hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const float* const* lse_parts, int64_t n,
-                      int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, const uint8_t* skip,
-                      int32_t block_m, hipStream_t stream);
+                      int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, const int32_t* tiles,
+                      int32_t num_tiles, int32_t block_m, hipStream_t stream);
 
 // The executor's forwards.  Document starts come from the cumulative lengths cu_seqlens
 // [num_docs + 1] on the device (no per-position start array).  fused: hsap_attn_fwd_fused over

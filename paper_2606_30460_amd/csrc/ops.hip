@@ -25,9 +25,20 @@ struct MergeArgs {
   int64_t n;
   __bf16* o_out;
   float* lse_out;
-  const uint8_t* skip;  // per BM-row q-tile: 1 = rows already final, not merged (NULL: merge every row)
+  // Rows to merge: with `tiles` NULL every row 0..n-1; otherwise the BM-row q-tiles listed in
+  // tiles[0 .. num_tiles-1], as "merge rows" v = 0 .. num_tiles * BM - 1 standing for shard row
+  // tiles[v / BM] * BM + v % BM (the other q-tiles' rows are already final: not read, not written).
+  const int32_t* tiles;
+  int64_t rows;  // merge rows: n, or num_tiles * BM
   int32_t bm;
 };
+
+// shard row of merge row v
+__device__ __forceinline__ int64_t merge_row(const MergeArgs& a, int64_t v) {
+  if (!a.tiles) return v;
+  const int64_t t = v / a.bm;
+  return (int64_t)a.tiles[t] * a.bm + (v - t * a.bm);
+}
 
 // Few parts (num_parts <= PR): one wave merges one head's 16 consecutive rows.
 // Lane i reads (and finally writes) the LSE of row i & 15, so each part's LSE
@@ -45,7 +56,7 @@ __global__ __launch_bounds__(256) void lse_merge_few_kernel(MergeArgs a) {
   constexpr float LOG2E = 1.44269504088896340736f;
   constexpr float LN2 = 0.69314718055994530942f;
   const int lane = threadIdx.x & 63;
-  const int64_t groups_per_head = (a.n + 15) / 16;
+  const int64_t groups_per_head = (a.rows + 15) / 16;
   const int64_t groups = groups_per_head * a.hq;
   const int64_t wave0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) / 64;
   const int64_t waves = (int64_t)gridDim.x * 4;
@@ -53,12 +64,13 @@ __global__ __launch_bounds__(256) void lse_merge_few_kernel(MergeArgs a) {
   const int d0 = 4 * (lane % (D / 4));      // its 4 consecutive d
   for (int64_t grp = wave0; grp < groups; grp += waves) {
     const int64_t h = grp / groups_per_head;
-    const int64_t r0 = (grp - h * groups_per_head) * 16;
-    if (a.skip && a.skip[r0 / a.bm]) continue;  // a 16-row group never straddles q-tiles (BM % 16 == 0)
+    const int64_t v0 = (grp - h * groups_per_head) * 16;
+    // a 16-row group never straddles listed q-tiles (BM % 16 == 0): its shard rows are r0 + 0..15
+    const int64_t r0 = merge_row(a, v0);
     // LSE of row r0 + (lane & 15) for every part; max and result in natural-log units, only
     // differences scaled to log2 units, so a row with one finite part keeps its LSE exactly
     const int64_t my_row = r0 + (lane & 15);
-    const bool row_ok = my_row < a.n;
+    const bool row_ok = v0 + (lane & 15) < a.rows;
     float l[PR];
 #pragma unroll
     for (int p = 0; p < PR; ++p) l[p] = (p < a.num_parts && row_ok) ? a.lse[p][h * a.n + my_row] : NEG_INF;
@@ -77,15 +89,16 @@ __global__ __launch_bounds__(256) void lse_merge_few_kernel(MergeArgs a) {
     for (int k = 0; k < STEPS; ++k) {
       const int j = RPI * k + sub;  // row within the group; its weights live in lane j
       const int64_t row = r0 + j;
+      const bool in = v0 + j < a.rows;
       float w[PR];
       f32x4 x[PR];
 #pragma unroll
       for (int p = 0; p < PR; ++p) {
         w[p] = __int_as_float(__builtin_amdgcn_ds_bpermute(4 * j, __float_as_int(wl[p])));
-        x[p] = (w[p] > 0.f && row < a.n) ? *(const f32x4*)(a.o[p] + (row * a.hq + h) * D + d0)
-                                         : f32x4{0.f, 0.f, 0.f, 0.f};
+        x[p] = (w[p] > 0.f && in) ? *(const f32x4*)(a.o[p] + (row * a.hq + h) * D + d0)
+                                  : f32x4{0.f, 0.f, 0.f, 0.f};
       }
-      if (row >= a.n) continue;
+      if (!in) continue;
       f32x4 acc{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int p = 0; p < PR; ++p) acc += w[p] * x[p];
@@ -106,7 +119,7 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
   constexpr float NEG_INF = -__builtin_inff();
   constexpr float LOG2E = 1.44269504088896340736f;
   constexpr float LN2 = 0.69314718055994530942f;
-  const int64_t items = a.n * a.hq;
+  const int64_t items = a.rows * a.hq;
   const int part = (int)(threadIdx.x % TPR);
   const int64_t stride = (int64_t)gridDim.x * (256 / TPR);
   const int64_t base = ((int64_t)blockIdx.x * 256 + threadIdx.x) / TPR;
@@ -114,10 +127,12 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
   bool live[ITEMS];
 #pragma unroll
   for (int it = 0; it < ITEMS; ++it) {
-    rh[it] = base + it * stride;  // rh = row * hq + head
-    const int64_t row = rh[it] / a.hq;
-    live[it] = rh[it] < items && !(a.skip && a.skip[row / a.bm]);
-    li[it] = (int64_t)(rh[it] - row * a.hq) * a.n + row;  // index into [Hq, n]
+    const int64_t vh = base + it * stride;  // merge row * hq + head
+    live[it] = vh < items;
+    const int64_t v = live[it] ? vh / a.hq : 0;
+    const int64_t row = merge_row(a, v);
+    rh[it] = row * a.hq + (vh - v * a.hq);  // shard row * hq + head
+    li[it] = (int64_t)(vh - v * a.hq) * a.n + row;  // index into [Hq, n]
   }
   // pass 1: running max (natural-log units) and sum of exp(LSE - max) over the parts
   float mx[ITEMS], sum[ITEMS];
@@ -366,7 +381,7 @@ extern "C" {
 hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const float* const* lse_parts, int64_t n,
                            int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, void* hip_stream) {
   clear_error();
-  return lse_merge(num_parts, o_parts, lse_parts, n, heads_q, head_dim, o_out, lse_out, nullptr, 1,
+  return lse_merge(num_parts, o_parts, lse_parts, n, heads_q, head_dim, o_out, lse_out, nullptr, 0, 1,
                    (hipStream_t)hip_stream);
 }
 
@@ -375,8 +390,8 @@ hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const
 namespace hsap {
 
 hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const float* const* lse_parts, int64_t n,
-                      int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, const uint8_t* skip,
-                      int32_t block_m, hipStream_t s) {
+                      int32_t heads_q, int32_t head_dim, void* o_out, float* lse_out, const int32_t* tiles,
+                      int32_t num_tiles, int32_t block_m, hipStream_t s) {
   if (num_parts < 1 || num_parts > HSAP_MAX_MERGE_PARTS)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "num_parts %d outside 1..%d", num_parts, HSAP_MAX_MERGE_PARTS);
   if (!o_parts || !lse_parts || !o_out || !lse_out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
@@ -396,13 +411,16 @@ hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const floa
   a.n = n;
   a.o_out = (__bf16*)o_out;
   a.lse_out = lse_out;
-  if (skip && (block_m < 16 || block_m % 16)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "skip flags need BM a multiple of 16");
-  a.skip = skip;
-  a.bm = skip ? block_m : 1;
+  if (tiles && (block_m < 16 || block_m % 16 || num_tiles < 0 || (int64_t)num_tiles * block_m > n))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q-tile list needs BM a multiple of 16 and at most n / BM tiles");
+  a.tiles = tiles;
+  a.bm = tiles ? block_m : 1;
+  a.rows = tiles ? (int64_t)num_tiles * block_m : n;
+  if (a.rows == 0) return HSAP_OK;
   const dim3 block(256);
   if (num_parts <= 4) {
     // one wave per (head, 16 rows) group, four waves per block, grid-stride beyond 65536 blocks
-    const int64_t groups = ((n + 15) / 16) * heads_q;
+    const int64_t groups = ((a.rows + 15) / 16) * heads_q;
     const dim3 grid((unsigned)std::min<int64_t>((groups + 3) / 4, 65536));
     if (head_dim == 128) {
       if (num_parts <= 2) hipLaunchKernelGGL((lse_merge_few_kernel<128, 2>), grid, block, 0, s, a);
@@ -413,7 +431,7 @@ hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const floa
     }
   } else {
     constexpr int ITEMS = 4;
-    const int64_t threads = n * heads_q * (head_dim / 4);
+    const int64_t threads = a.rows * heads_q * (head_dim / 4);
     const int64_t blocks = (threads + 256 * ITEMS - 1) / (256 * ITEMS);
     if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "problem too large");
     const dim3 grid((unsigned)blocks);
