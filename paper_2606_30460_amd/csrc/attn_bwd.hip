@@ -225,6 +225,18 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
         sacc = mfma32(qa[kk], kf[kk], sacc);
         dpacc = mfma32(oa[kk], vf[kk], dpacc);
       }
+      // the transposed dO and Q reads of the dV / dK products depend on no score: issued here, they
+      // land while P and dS are computed (one wave per SIMD has nothing else to hide them)
+      bf16x8 bo[2][MB], bq[2][MB];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int rb = (32 * qb + 16 * half) * D;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          bo[half][mb] = cat4(ds_read_tr16(O + rb + troff[mb][0]), ds_read_tr16(O + rb + 8 * D + troff[mb][1]));
+          bq[half][mb] = cat4(ds_read_tr16(Q + rb + troff[mb][0]), ds_read_tr16(Q + rb + 8 * D + troff[mb][1]));
+        }
+      }
       // P for the block (register j = 4 grp + e holds query q4 + e, q4 = 32 qb + 8 grp + 4 hi),
       // masked in one uniform branch, then P and dS = P (dP - delta) as bf16
       float p[16];
@@ -256,20 +268,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
         }
       }
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int rb = (32 * qb + 16 * half) * D;
-        bf16x8 bo[MB], bq[MB];
+      for (int half = 0; half < 2; ++half)
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-          bo[mb] = cat4(ds_read_tr16(O + rb + troff[mb][0]), ds_read_tr16(O + rb + 8 * D + troff[mb][1]));
-          bq[mb] = cat4(ds_read_tr16(Q + rb + troff[mb][0]), ds_read_tr16(Q + rb + 8 * D + troff[mb][1]));
+          dv[mb] = mfma32(pb[half], bo[half][mb], dv[mb]);
+          dk[mb] = mfma32(sb[half], bq[half][mb], dk[mb]);
         }
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          dv[mb] = mfma32(pb[half], bo[mb], dv[mb]);
-          dk[mb] = mfma32(sb[half], bq[mb], dk[mb]);
-        }
-      }
     }
 
     if (it + 1 < total) store_sub(buf ^ 1);
