@@ -547,17 +547,13 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     const uint32_t lds = (uint32_t)(uintptr_t)(lds_void)dst + (uint32_t)(WCH * wu * 16);
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds + 64 * 16 * u), "v"(gsrc[u]),
-                   "s"(src)
-                   : "m0");
+      asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(gsrc[u]), "s"(src), "{m0}"(lds + 64 * 16 * u));
   };
   auto stage_k = [&](const KT* src, KT* dst) {
     const uint32_t lds = (uint32_t)(uintptr_t)(lds_void)dst + (uint32_t)(WCHK * wu * 16);
 #pragma unroll
     for (int u = 0; u < UK; ++u)
-      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds + 64 * 16 * u), "v"(gsrck[u]),
-                   "s"(src)
-                   : "m0");
+      asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(gsrck[u]), "s"(src), "{m0}"(lds + 64 * 16 * u));
   };
   const KT* kbase = (const KT*)a.k;
 
