@@ -369,6 +369,7 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
   if (major == HSAP_MAJOR_Q) {
     if (num_tiles > 0) std::memcpy(sorted_tiles, tiles, sizeof(hsap_tile) * num_tiles);
     const int64_t max_run = max_run_tiles > 0 ? max_run_tiles : INT64_MAX;
+    auto pieces_for = [&](int64_t cnt) { return cnt == 0 ? 0 : (cnt - 1) / max_run + 1; };  // no overflow
     int64_t i = 0;
     std::vector<int64_t> first(nq), count(nq);
     while (i < num_tiles) {
@@ -380,12 +381,12 @@ hsap_status hsap_plan_runs(const hsap_shard_desc* shard, const hsap_tile* tiles,
         while (j < num_tiles && tiles[j].chunk == c && tiles[j].q_tile == t) ++j;
         first[t] = i;
         count[t] = j - i;
-        pieces = std::max<int64_t>(pieces, (count[t] + max_run - 1) / max_run);
+        pieces = std::max<int64_t>(pieces, pieces_for(count[t]));
         i = j;
       }
       // every q-tile gets a run in every slot the chunk uses (count 0 where it has nothing there)
       for (int32_t t = 0; t < nq; ++t) {
-        const int64_t need = std::max<int64_t>(1, (count[t] + max_run - 1) / max_run);
+        const int64_t need = std::max<int64_t>(1, pieces_for(count[t]));
         int64_t at = first[t];
         for (int64_t piece = 0; piece < pieces; ++piece) {
           int64_t len = 0;
