@@ -423,6 +423,11 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
     stage(a.k + off, Ks[0]);
     stage(a.v + off, Vs[0]);
   }
+  // The compiler does not see the waits inside asm statements: without a use of Q and dO here it
+  // would wait for their loads at their first use inside the loop, in every step, and since the
+  // counter also counts the step's transfers, each step would wait for the next step's K and V.
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) asm volatile("" ::"v"(qf[kk]), "v"(of[kk]));
   asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
 
   // one 64-key step from slot PAR (= s % 2, a compile-time constant, so every slot address is an
