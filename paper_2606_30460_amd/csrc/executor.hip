@@ -58,6 +58,7 @@ struct hsap_executor {
   std::vector<int32_t> slot_map;
   std::vector<uint8_t> final_tile;  // per q-tile: 1 when its only part is written final by the partial forward
   std::vector<int32_t> merged_tiles;  // the other q-tiles, in order: the merge's rows
+  std::vector<int32_t> zero_ktiles;   // k-tiles (c * nk + k_tile) of chunks with tiles that no query reaches
 
   // pinned staging ring; upload u uses pinned[u % kStaging], and when u % kEventEvery is
   // kEventEvery - 1 an event recorded after its copy sits in uploaded[u % kStaging]
@@ -67,7 +68,7 @@ struct hsap_executor {
   int64_t uploads = 0;             // uploads issued so far
 
   // device side
-  DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu | merged_tiles]
+  DevBuf lists;  // [sorted_q | runs_q | sorted_k | runs_k | sorted_all | runs_all | cu | merged_tiles | zero_ktiles]
   int32_t* doc_start = nullptr;  // start(t) per position, for the backward only
   DevBuf o_part, lse_part;
   float* delta = nullptr;
@@ -82,6 +83,7 @@ struct hsap_executor {
   const hsap_tile* d_tiles_all = nullptr;
   const hsap_run* d_runs_all = nullptr;
   const int32_t* d_merged_tiles = nullptr;
+  const int32_t* d_zero_ktiles = nullptr;
   const int32_t* d_cu = nullptr;  // the plan's cu_seqlens (the forwards search it for document starts)
   int32_t num_docs = 0;
   std::vector<uint8_t> chunk_has_tiles;
@@ -308,6 +310,18 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   }
   ex->info.num_runs_k = RK;
   ex->info.num_runs_all = RA;
+  // dK/dV rows of a chunk with tiles are written by the k-major run of their k-tile; the k-tiles
+  // without one (no query of the shard reaches them) are zeroed by the backward instead
+  ex->zero_ktiles.clear();
+  if (RK) {
+    const int64_t nk = ex->geom.n / sd.block_n;
+    std::vector<uint8_t> reached((size_t)P * nk, 0);
+    for (int64_t i = 0; i < RK; ++i) reached[(size_t)(ex->runs_k[(size_t)i].slot * nk + ex->runs_k[(size_t)i].tile)] = 1;
+    for (int32_t c = 0; c < P; ++c)
+      if (ex->chunk_has_tiles[(size_t)c])
+        for (int64_t t = 0; t < nk; ++t)
+          if (!reached[(size_t)(c * nk + t)]) ex->zero_ktiles.push_back((int32_t)(c * nk + t));
+  }
 
   // 4. partial workspace for this plan's parts
   const size_t part_rows = (size_t)ex->geom.n * ex->desc.heads_q;
@@ -320,9 +334,9 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   const size_t w_tk = RK ? w_tq : 0, w_rk = words16((size_t)RK * 4);
   const size_t w_ta = RA ? w_tq : 0, w_ra = words16((size_t)RA * 4);
   const size_t w_cu = words16((size_t)num_docs + 1);
-  const size_t w_mt = words16(ex->merged_tiles.size());
+  const size_t w_mt = words16(ex->merged_tiles.size()), w_zt = words16(ex->zero_ktiles.size());
   const size_t o_rq = w_tq, o_tk = o_rq + w_rq, o_rk = o_tk + w_tk, o_ta = o_rk + w_rk, o_ra = o_ta + w_ta,
-               o_cu = o_ra + w_ra, o_mt = o_cu + w_cu, words = o_mt + w_mt;
+               o_cu = o_ra + w_ra, o_mt = o_cu + w_cu, o_zt = o_mt + w_mt, words = o_zt + w_zt;
   const int64_t u = ex->uploads;
   const int slot = (int)(u % kStaging);
   if (u >= kStaging) {  // the buffer last served upload u - kStaging
@@ -347,6 +361,7 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   }
   std::memcpy(h + o_cu, cu_seqlens, ((size_t)num_docs + 1) * sizeof(int32_t));
   std::memcpy(h + o_mt, ex->merged_tiles.data(), ex->merged_tiles.size() * sizeof(int32_t));
+  std::memcpy(h + o_zt, ex->zero_ktiles.data(), ex->zero_ktiles.size() * sizeof(int32_t));
   hipError_t e = hipMemcpyAsync(ex->lists.p, h, words * 4, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail("list upload", e);
   if (u % kEventEvery == kEventEvery - 1) {
@@ -364,6 +379,7 @@ hsap_status hsap_executor_plan(hsap_executor* ex, const int32_t* cu_seqlens, int
   ex->d_tiles_all = RA ? (const hsap_tile*)(d + o_ta) : nullptr;
   ex->d_runs_all = RA ? (const hsap_run*)(d + o_ra) : nullptr;
   ex->d_merged_tiles = d + o_mt;
+  ex->d_zero_ktiles = d + o_zt;
   ex->d_cu = d + o_cu;
   ex->num_docs = num_docs;
 
@@ -440,14 +456,10 @@ hsap_status hsap_executor_backward(hsap_executor* ex, const void* q, const void*
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   const hipStream_t stream = (hipStream_t)hip_stream;
   const int64_t n = ex->geom.n, hq = ex->desc.heads_q, d = ex->desc.head_dim;
-  // in a chunk with tiles, dK/dV rows of k-tiles that no query reaches have no owning run: zero first
-  const int64_t chunk_bytes = n * ex->desc.heads_kv * d * 2;
-  hsap_status st = HSAP_OK;
-  for (int32_t c = 0; st == HSAP_OK && c < ex->geom.P; ++c)
-    if (ex->chunk_has_tiles[(size_t)c]) {
-      st = zero_fill((char*)dk + c * chunk_bytes, chunk_bytes, stream);
-      if (st == HSAP_OK) st = zero_fill((char*)dv + c * chunk_bytes, chunk_bytes, stream);
-    }
+  // in a chunk with tiles, dK/dV rows of k-tiles that no query reaches have no owning run: zeroed
+  // here (the listed k-tiles only; the kernels write every other row of those chunks)
+  const int64_t ktile_bytes = (int64_t)ex->desc.shard.block_n * ex->desc.heads_kv * d * 2;
+  hsap_status st = zero_tiles(dk, dv, ex->d_zero_ktiles, (int32_t)ex->zero_ktiles.size(), ktile_bytes, stream);
   if (st == HSAP_OK) st = hsap_attn_bwd_preprocess(o, d_o, n, (int32_t)hq, (int32_t)d, ex->delta, hip_stream);
   if (st == HSAP_OK)
     st = hsap_attn_bwd_bf16(&ex->desc, q, k, v, d_o, lse, ex->delta, ex->doc_start, ex->d_tiles_k, ex->d_runs_k,

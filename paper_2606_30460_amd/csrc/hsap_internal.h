@@ -67,9 +67,11 @@ hsap_status check_shard(const hsap_shard_desc* d, Geom* g);
 hsap_status check_attn(const hsap_attn_desc* d, Geom* g);
 
 #if defined(__HIPCC__)
-// Writes `bytes` zero bytes at dst on `stream` with a kernel (bytes a multiple
-// of 4, dst 16-byte aligned).
-hsap_status zero_fill(void* dst, int64_t bytes, hipStream_t stream);
+// Zeroes tiles tiles[0 .. num_tiles-1] (device int32) of both a and b, tile t being the byte
+// range [t * tile_bytes, (t + 1) * tile_bytes); tile_bytes a multiple of 16, a and b 16-byte
+// aligned.  Nothing is launched for an empty list.
+hsap_status zero_tiles(void* a, void* b, const int32_t* tiles, int32_t num_tiles, int64_t tile_bytes,
+                       hipStream_t stream);
 
 // hsap_lse_merge over the rows of the BM-row q-tiles listed in tiles[0 .. num_tiles-1] (device
 // int32), or over every row when tiles is NULL; rows of other q-tiles are neither read nor written.

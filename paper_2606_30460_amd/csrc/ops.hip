@@ -262,10 +262,14 @@ __global__ __launch_bounds__(256) void gather_kernel(Geom g, const uint4* src, u
 // zero fill, 16 bytes per lane (a kernel rather than a memset node, so the
 // sequence stays valid inside captured graphs)
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void zero_kernel(uint4* dst, int64_t words16, uint32_t* tail, int32_t tail_words) {
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < words16; i += stride) dst[i] = uint4{0, 0, 0, 0};
-  if (blockIdx.x == 0 && (int)threadIdx.x < tail_words) tail[threadIdx.x] = 0;
+// Zeroes the listed tiles of two buffers: entry i names tile list[i], the byte range
+// [list[i] * tile_words * 16, +tile_words * 16) of both a and b.  blockIdx.x is the entry.
+__global__ __launch_bounds__(256) void zero_tiles_kernel(uint4* a, uint4* b, const int32_t* list, int64_t tile_words) {
+  const int64_t base = (int64_t)list[blockIdx.x] * tile_words;
+  for (int64_t i = (int64_t)blockIdx.y * 256 + threadIdx.x; i < tile_words; i += (int64_t)gridDim.y * 256) {
+    a[base + i] = uint4{0, 0, 0, 0};
+    b[base + i] = uint4{0, 0, 0, 0};
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -362,14 +366,16 @@ static unsigned grid_for(int64_t threads) {
   return (unsigned)(b < 1 ? 1 : (b > 65536 ? 65536 : b));
 }
 
-hsap_status zero_fill(void* dst, int64_t bytes, hipStream_t stream) {
-  if (bytes == 0) return HSAP_OK;
-  if (!dst || bytes < 0 || (bytes & 3) || ((uintptr_t)dst & 15))
-    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "zero_fill: bad buffer or size %lld", (long long)bytes);
-  const int64_t words16 = bytes / 16;
-  hipLaunchKernelGGL(zero_kernel, dim3(grid_for(words16)), dim3(256), 0, stream, (uint4*)dst, words16,
-                     (uint32_t*)((char*)dst + words16 * 16), (int32_t)((bytes - words16 * 16) / 4));
-  return check_launch("zero_fill");
+hsap_status zero_tiles(void* a, void* b, const int32_t* tiles, int32_t num_tiles, int64_t tile_bytes,
+                       hipStream_t stream) {
+  if (num_tiles == 0) return HSAP_OK;
+  if (!a || !b || !tiles || num_tiles < 0 || tile_bytes <= 0 || (tile_bytes & 15) || (((uintptr_t)a | (uintptr_t)b) & 15))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "zero_tiles: bad buffers, list or tile size %lld", (long long)tile_bytes);
+  const int64_t words = tile_bytes / 16;
+  const unsigned per_tile = (unsigned)std::min<int64_t>(64, (words + 1023) / 1024);  // about 4 stores per thread
+  hipLaunchKernelGGL(zero_tiles_kernel, dim3((unsigned)num_tiles, per_tile), dim3(256), 0, stream, (uint4*)a,
+                     (uint4*)b, tiles, words);
+  return check_launch("zero_tiles");
 }
 
 }  // namespace hsap
