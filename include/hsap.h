@@ -614,9 +614,11 @@ hsap_status hsap_executor_merge(hsap_executor* ex, void* o_out, float* lse_out, 
  * hsap_executor_backward -- gradients of the forward for the current plan
  * (needs HSAP_EXEC_BACKWARD): zeroes the dk and dv rows of the k-tiles that
  * no query of the shard reaches in the chunks with tiles (the plan lists
- * them), then hsap_attn_bwd_preprocess and hsap_attn_bwd_bf16 over the
- * k-major and MAJOR_Q_ALL runs, which write every other row of those
- * chunks.
+ * them), then the kernels of hsap_attn_bwd_bf16 over the k-major and
+ * MAJOR_Q_ALL runs, which write every other row of those chunks.  The dQ
+ * kernel runs first and computes the preprocess (delta of
+ * hsap_attn_bwd_preprocess) for its rows from o and d_o; the dK/dV kernel
+ * reads it.
  *   q, k, v  as for the forward;  d_o, o  device bf16 [n, Hq, d] (o: the
  *            forward's output);  lse  device fp32 [Hq, n] (the forward's).
  *   dq       device bf16 [n, Hq, d].

@@ -36,6 +36,8 @@ struct BwdArgs {
   const __bf16* d_o;
   const float* lse;
   const float* delta;
+  const __bf16* o;     // when set, the dQ kernel computes delta from O and dO itself, writing delta_out
+  float* delta_out;
   const int32_t* doc_start;
   const hsap_tile* tiles;
   const hsap_run* runs;
@@ -344,14 +346,36 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
   const uint32_t span = (uint32_t)(gq - qstart);
   const float lse_raw = a.lse[(int64_t)h * n + qrow];
   const float lse2 = lse_raw == NEG_INF ? __builtin_inff() : lse_raw * LOG2E;  // no key: P = 0
-  const float dlt = a.delta[(int64_t)h * n + qrow];
   bf16x8 qf[D / 16], of[D / 16];
+  float dlt;
   {
     const int64_t off = (qrow * a.hq + h) * D + 8 * hi;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       qf[kk] = *(const bf16x8*)(a.q + off + 16 * kk);
       of[kk] = *(const bf16x8*)(a.d_o + off + 16 * kk);
+    }
+    if (a.o) {
+      // the backward preprocess for this row, delta = sum_d dO O, summed in the order of
+      // hsap_attn_bwd_preprocess (so both give the same bits): a sum per 8-element chunk, then a
+      // tree over the chunk index from its highest bit down.  The lane holds chunks 2 kk + hi, so
+      // the tree runs over kk within the lane and ends with the lane l ^ 32 (chunk bit 0).
+      float p[D / 16];
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) {
+        const bf16x8 ov = *(const bf16x8*)(a.o + off + 16 * kk);
+        p[kk] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p[kk] = __builtin_fmaf((float)ov[e], (float)of[kk][e], p[kk]);
+      }
+#pragma unroll
+      for (int wdt = D / 32; wdt >= 1; wdt >>= 1)
+#pragma unroll
+        for (int kk = 0; kk < wdt; ++kk) p[kk] = p[kk] + p[kk + wdt];
+      dlt = p[0] + __shfl_xor(p[0], 32);
+      if (hi == 0) a.delta_out[(int64_t)h * n + qrow] = dlt;  // read by the dK/dV kernel, launched after
+    } else {
+      dlt = a.delta[(int64_t)h * n + qrow];
     }
   }
   const int tr_row = 4 * hi + ((lane & 15) >> 2);
@@ -538,11 +562,13 @@ static hsap_status launch_dq(const BwdArgs& a, int64_t num_runs, hipStream_t str
 
 // shared checks and dispatch of the fp32-accumulating and the bf16-storing backward
 template <bool BF16OUT>
+// o == NULL: delta is an input.  Otherwise the dQ kernel computes delta from o and d_o into
+// delta_out, and the dK/dV kernel (launched after it) reads it there.
 static hsap_status backward(const hsap_attn_desc* desc, const void* q, const void* k, const void* v, const void* d_o,
-                            const float* lse, const float* delta, const int32_t* doc_start, const hsap_tile* tiles_k,
-                            const hsap_run* runs_k, int64_t num_runs_k, const hsap_tile* tiles_q,
-                            const hsap_run* runs_q, int64_t num_runs_q, void* dq, void* dk, void* dv,
-                            hipStream_t s) {
+                            const void* o, const float* lse, const float* delta, float* delta_out,
+                            const int32_t* doc_start, const hsap_tile* tiles_k, const hsap_run* runs_k,
+                            int64_t num_runs_k, const hsap_tile* tiles_q, const hsap_run* runs_q,
+                            int64_t num_runs_q, void* dq, void* dk, void* dv, hipStream_t s) {
   Geom geom;
   hsap_status st = check_attn(desc, &geom);
   if (st != HSAP_OK) return st;
@@ -555,11 +581,13 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
     HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no backward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
   if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
   if (num_runs_k == 0 && num_runs_q == 0) return HSAP_OK;
-  if (!q || !k || !v || !d_o || !lse || !delta || !doc_start || !dq || !dk || !dv ||
+  if (!q || !k || !v || !d_o || !lse || !(o ? delta_out : delta) || !doc_start || !dq || !dk || !dv ||
       (num_runs_k > 0 && (!tiles_k || !runs_k)) || (num_runs_q > 0 && (!tiles_q || !runs_q)))
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
-  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)d_o) & 15)
-    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k, v and d_o must be 16-byte aligned");
+  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)d_o | (uintptr_t)o) & 15)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k, v, d_o and o must be 16-byte aligned");
+  if (o && num_runs_k > 0 && num_runs_q == 0)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "delta from o needs the q-major runs (the dQ kernel computes it)");
   if ((uintptr_t)dq & (BF16OUT ? 7 : 15))
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "dq must be %d-byte aligned", BF16OUT ? 8 : 16);
   BwdArgs a = {};
@@ -568,7 +596,9 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
   a.v = (const __bf16*)v;
   a.d_o = (const __bf16*)d_o;
   a.lse = lse;
-  a.delta = delta;
+  a.delta = o ? delta_out : delta;
+  a.o = (const __bf16*)o;
+  a.delta_out = delta_out;
   a.doc_start = doc_start;
   if (BF16OUT) {
     a.dq16 = (__bf16*)dq;
@@ -587,6 +617,23 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
   a.bm = bm;
   a.scale = desc->softmax_scale;
   a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
+  if (num_runs_q > 0) {
+    a.tiles = tiles_q;
+    a.runs = runs_q;
+#define HSAP_DQ_CASE(D_, BN_, W_) \
+  if (d == D_ && bn == BN_ && bm == 32 * W_) st = launch_dq<D_, BN_, W_, BF16OUT>(a, num_runs_q, s);
+    HSAP_DQ_CASE(128, 128, 4)
+    else HSAP_DQ_CASE(128, 64, 4)
+    else HSAP_DQ_CASE(128, 128, 2)
+    else HSAP_DQ_CASE(128, 64, 2)
+    else HSAP_DQ_CASE(64, 128, 4)
+    else HSAP_DQ_CASE(64, 64, 4)
+    else HSAP_DQ_CASE(64, 128, 2)
+    else HSAP_DQ_CASE(64, 64, 2)
+#undef HSAP_DQ_CASE
+    if (st != HSAP_OK) return st;
+    a.o = nullptr;  // the dK/dV kernel reads delta
+  }
   if (num_runs_k > 0) {
     a.tiles = tiles_k;
     a.runs = runs_k;
@@ -594,21 +641,6 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
     else if (d == 128) st = launch_dkdv<128, 2, BF16OUT>(a, num_runs_k, s);
     else st = launch_dkdv<64, 2, BF16OUT>(a, num_runs_k, s);
     if (st != HSAP_OK) return st;
-  }
-  if (num_runs_q > 0) {
-    a.tiles = tiles_q;
-    a.runs = runs_q;
-#define HSAP_DQ_CASE(D_, BN_, W_) \
-  if (d == D_ && bn == BN_ && bm == 32 * W_) return launch_dq<D_, BN_, W_, BF16OUT>(a, num_runs_q, s);
-    HSAP_DQ_CASE(128, 128, 4)
-    HSAP_DQ_CASE(128, 64, 4)
-    HSAP_DQ_CASE(128, 128, 2)
-    HSAP_DQ_CASE(128, 64, 2)
-    HSAP_DQ_CASE(64, 128, 4)
-    HSAP_DQ_CASE(64, 64, 4)
-    HSAP_DQ_CASE(64, 128, 2)
-    HSAP_DQ_CASE(64, 64, 2)
-#undef HSAP_DQ_CASE
   }
   return HSAP_OK;
 }
@@ -624,8 +656,8 @@ extern "C" hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const v
                                              const hsap_run* runs_q, int64_t num_runs_q, float* dq_acc,
                                              float* dk_acc, float* dv_acc, void* hip_stream) {
   clear_error();
-  return backward<false>(desc, q, k, v, d_o, lse, delta, doc_start, tiles_k, runs_k, num_runs_k, tiles_q, runs_q,
-                         num_runs_q, dq_acc, dk_acc, dv_acc, (hipStream_t)hip_stream);
+  return backward<false>(desc, q, k, v, d_o, nullptr, lse, delta, nullptr, doc_start, tiles_k, runs_k, num_runs_k,
+                         tiles_q, runs_q, num_runs_q, dq_acc, dk_acc, dv_acc, (hipStream_t)hip_stream);
 }
 
 extern "C" hsap_status hsap_attn_bwd_bf16(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
@@ -634,6 +666,18 @@ extern "C" hsap_status hsap_attn_bwd_bf16(const hsap_attn_desc* desc, const void
                                           int64_t num_runs_k, const hsap_tile* tiles_q, const hsap_run* runs_q,
                                           int64_t num_runs_q, void* dq, void* dk, void* dv, void* hip_stream) {
   clear_error();
-  return backward<true>(desc, q, k, v, d_o, lse, delta, doc_start, tiles_k, runs_k, num_runs_k, tiles_q, runs_q,
-                        num_runs_q, dq, dk, dv, (hipStream_t)hip_stream);
+  return backward<true>(desc, q, k, v, d_o, nullptr, lse, delta, nullptr, doc_start, tiles_k, runs_k, num_runs_k,
+                        tiles_q, runs_q, num_runs_q, dq, dk, dv, (hipStream_t)hip_stream);
 }
+
+namespace hsap {
+hsap_status attn_bwd_bf16_delta(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                const void* d_o, const void* o, const float* lse, float* delta,
+                                const int32_t* doc_start, const hsap_tile* tiles_k, const hsap_run* runs_k,
+                                int64_t num_runs_k, const hsap_tile* tiles_q, const hsap_run* runs_q,
+                                int64_t num_runs_q, void* dq, void* dk, void* dv, hipStream_t stream) {
+  if (!o) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL o");
+  return backward<true>(desc, q, k, v, d_o, o, lse, nullptr, delta, doc_start, tiles_k, runs_k, num_runs_k, tiles_q,
+                        runs_q, num_runs_q, dq, dk, dv, stream);
+}
+}  // namespace hsap

@@ -455,16 +455,16 @@ hsap_status hsap_executor_backward(hsap_executor* ex, const void* q, const void*
   if (!q || !k || !v || !d_o || !o || !lse || !dq || !dk || !dv)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   const hipStream_t stream = (hipStream_t)hip_stream;
-  const int64_t n = ex->geom.n, hq = ex->desc.heads_q, d = ex->desc.head_dim;
+  const int64_t d = ex->desc.head_dim;
   // in a chunk with tiles, dK/dV rows of k-tiles that no query reaches have no owning run: zeroed
   // here (the listed k-tiles only; the kernels write every other row of those chunks)
   const int64_t ktile_bytes = (int64_t)ex->desc.shard.block_n * ex->desc.heads_kv * d * 2;
   hsap_status st = zero_tiles(dk, dv, ex->d_zero_ktiles, (int32_t)ex->zero_ktiles.size(), ktile_bytes, stream);
-  if (st == HSAP_OK) st = hsap_attn_bwd_preprocess(o, d_o, n, (int32_t)hq, (int32_t)d, ex->delta, hip_stream);
+  // the preprocess (delta = rowsum(dO o O)) runs inside the dQ kernel, which reads dO anyway
   if (st == HSAP_OK)
-    st = hsap_attn_bwd_bf16(&ex->desc, q, k, v, d_o, lse, ex->delta, ex->doc_start, ex->d_tiles_k, ex->d_runs_k,
-                            ex->info.num_runs_k, ex->d_tiles_all, ex->d_runs_all, ex->info.num_runs_all, dq, dk, dv,
-                            hip_stream);
+    st = attn_bwd_bf16_delta(&ex->desc, q, k, v, d_o, o, lse, ex->delta, ex->doc_start, ex->d_tiles_k, ex->d_runs_k,
+                             ex->info.num_runs_k, ex->d_tiles_all, ex->d_runs_all, ex->info.num_runs_all, dq, dk, dv,
+                             stream);
   return st;
 }
 

@@ -85,6 +85,14 @@ hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const floa
 // kFinalSlot write the final bf16 O and LSE of their q-tile to o_out / lse_out (the q-tile's
 // only part: nothing to merge).
 constexpr int32_t kFinalSlot = -2;
+
+// hsap_attn_bwd_bf16 with the backward preprocess folded into the dQ kernel: delta (device fp32
+// [Hq, n], written) is computed there from o and d_o, and read by the dK/dV kernel launched after.
+hsap_status attn_bwd_bf16_delta(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                const void* d_o, const void* o, const float* lse, float* delta,
+                                const int32_t* doc_start, const hsap_tile* tiles_k, const hsap_run* runs_k,
+                                int64_t num_runs_k, const hsap_tile* tiles_q, const hsap_run* runs_q,
+                                int64_t num_runs_q, void* dq, void* dk, void* dv, hipStream_t stream);
 hsap_status executor_forward(const hsap_attn_desc* desc, bool fused, const void* q, const void* k, const void* v,
                              const int32_t* cu_seqlens, int32_t num_docs, const hsap_tile* tiles,
                              const hsap_run* runs, int64_t num_runs, float* o_part, float* lse_part,

@@ -198,7 +198,7 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(const __bf16* o, co
     const bf16x8 x = *(const bf16x8*)(o + rh * D + 8 * part);
     const bf16x8 y = *(const bf16x8*)(d_o + rh * D + 8 * part);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc += (float)x[e] * (float)y[e];
+    for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)x[e], (float)y[e], acc);
   }
 #pragma unroll
   for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
