@@ -109,75 +109,86 @@ __global__ __launch_bounds__(256) void lse_merge_few_kernel(MergeArgs a) {
   }
 }
 
-// Any number of parts: D/4 consecutive lanes own one (row, head) item, 4
-// consecutive d each; each thread carries ITEMS items spaced a grid apart and
-// issues the LSE loads of all of them, then the O loads of all of them, before
-// using any.  (For many parts this measured faster than the 16-row groups.)
-template <int D, int ITEMS>
-__global__ __launch_bounds__(256) void lse_merge_kernel(MergeArgs a) {
-  constexpr int TPR = D / 4;
+// Many parts (up to HSAP_MAX_MERGE_PARTS): one wave per (head, 16-row group) as in the
+// few-parts kernel, with lane = row + 16 g reading the LSEs of parts g, g + 4, g + 8, ... of its
+// row, so each lane holds at most a quarter of them.  Max and sum are combined over the four
+// lanes of a row with lane permutes (max and result in natural-log units, differences scaled to
+// log2 units, as in the few-parts kernel: a single finite part passes through exactly); the
+// weights go to LDS, and the O pass then walks the parts with no LSE load in front of any O load
+// (issuing the next part's loads before accumulating the current one measured slower: more
+// registers, fewer resident waves).
+template <int D>
+__global__ __launch_bounds__(256) void lse_merge_many_kernel(MergeArgs a) {
+  constexpr int RPI = 256 / D;                       // rows per wave instruction
+  constexpr int STEPS = 16 / RPI;                    // instructions per 16-row group
+  constexpr int LPER = HSAP_MAX_MERGE_PARTS / 4;     // parts per lane
   constexpr float NEG_INF = -__builtin_inff();
   constexpr float LOG2E = 1.44269504088896340736f;
   constexpr float LN2 = 0.69314718055994530942f;
-  const int64_t items = a.rows * a.hq;
-  const int part = (int)(threadIdx.x % TPR);
-  const int64_t stride = (int64_t)gridDim.x * (256 / TPR);
-  const int64_t base = ((int64_t)blockIdx.x * 256 + threadIdx.x) / TPR;
-  int64_t li[ITEMS], rh[ITEMS];
-  bool live[ITEMS];
+  __shared__ float w_s[4][HSAP_MAX_MERGE_PARTS][16];  // per wave: weight of (part, row of the group)
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int r16 = lane & 15, pg = lane >> 4;
+  const int sub = lane / (D / 4);                    // row of an instruction this lane serves
+  const int d0 = 4 * (lane % (D / 4));
+  const int np = a.num_parts;
+  const int64_t groups_per_head = (a.rows + 15) / 16;
+  const int64_t groups = groups_per_head * a.hq;
+  const int64_t waves = (int64_t)gridDim.x * 4;
+  for (int64_t grp = (int64_t)blockIdx.x * 4 + wv; grp < groups; grp += waves) {
+    const int64_t h = grp / groups_per_head;
+    const int64_t v0 = (grp - h * groups_per_head) * 16;
+    const int64_t r0 = merge_row(a, v0);  // the group's shard rows are r0 + 0..15 (BM % 16 == 0)
+    const bool row_ok = v0 + r16 < a.rows;
+    float l[LPER];
+    float mx = NEG_INF;
 #pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    const int64_t vh = base + it * stride;  // merge row * hq + head
-    live[it] = vh < items;
-    const int64_t v = live[it] ? vh / a.hq : 0;
-    const int64_t row = merge_row(a, v);
-    rh[it] = row * a.hq + (vh - v * a.hq);  // shard row * hq + head
-    li[it] = (int64_t)(vh - v * a.hq) * a.n + row;  // index into [Hq, n]
-  }
-  // pass 1: running max (natural-log units) and sum of exp(LSE - max) over the parts
-  float mx[ITEMS], sum[ITEMS];
-#pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    mx[it] = NEG_INF;
-    sum[it] = 0.f;
-  }
-  for (int p = 0; p < a.num_parts; ++p) {
-    float l[ITEMS];
-#pragma unroll
-    for (int it = 0; it < ITEMS; ++it) l[it] = live[it] ? a.lse[p][li[it]] : NEG_INF;
-#pragma unroll
-    for (int it = 0; it < ITEMS; ++it) {
-      const float m_new = fmaxf(mx[it], l[it]);
-      if (m_new != NEG_INF)
-        sum[it] = sum[it] * fast_exp2((mx[it] - m_new) * LOG2E) + fast_exp2((l[it] - m_new) * LOG2E);
-      mx[it] = m_new;
+    for (int j = 0; j < LPER; ++j) {
+      const int p = pg + 4 * j;
+      l[j] = (p < np && row_ok) ? a.lse[p][h * a.n + r0 + r16] : NEG_INF;
+      mx = fmaxf(mx, l[j]);
     }
-  }
-  float Lm[ITEMS];  // merged LSE
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    float sum = 0.f;
 #pragma unroll
-  for (int it = 0; it < ITEMS; ++it) Lm[it] = mx[it] == NEG_INF ? NEG_INF : mx[it] + __log2f(sum[it]) * LN2;
-  // pass 2: weighted sum of the finite parts
-  f32x4 acc[ITEMS];
+    for (int j = 0; j < LPER; ++j) sum += l[j] == NEG_INF ? 0.f : fast_exp2((l[j] - mx) * LOG2E);
+    sum += __shfl_xor(sum, 16);
+    sum += __shfl_xor(sum, 32);
+    const float Lm = mx == NEG_INF ? NEG_INF : mx + __log2f(sum) * LN2;
 #pragma unroll
-  for (int it = 0; it < ITEMS; ++it) acc[it] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int p = 0; p < a.num_parts; ++p) {
-    float wgt[ITEMS];
-    f32x4 x[ITEMS];
+    for (int j = 0; j < LPER; ++j) {
+      const int p = pg + 4 * j;
+      if (p < np) w_s[wv][p][r16] = l[j] == NEG_INF ? 0.f : fast_exp2((l[j] - Lm) * LOG2E);
+    }
+    __builtin_amdgcn_wave_barrier();  // a wave's LDS accesses complete in order: the weights are there
+    // O pass: instruction k covers rows RPI k + sub of the group
+    f32x4 acc[STEPS], x[STEPS];
+    float wk[STEPS];
+    auto load = [&](int p, f32x4 (&xs)[STEPS], float (&ws)[STEPS]) {
 #pragma unroll
-    for (int it = 0; it < ITEMS; ++it) {
-      const float l = live[it] ? a.lse[p][li[it]] : NEG_INF;
-      wgt[it] = l == NEG_INF ? 0.f : fast_exp2((l - Lm[it]) * LOG2E);
-      x[it] = wgt[it] > 0.f ? *(const f32x4*)(a.o[p] + rh[it] * D + 4 * part) : f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < STEPS; ++k) {
+        const int j = RPI * k + sub;
+        ws[k] = w_s[wv][p][j];
+        xs[k] = (ws[k] > 0.f && v0 + j < a.rows) ? *(const f32x4*)(a.o[p] + ((r0 + j) * a.hq + h) * D + d0)
+                                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    };
+#pragma unroll
+    for (int k = 0; k < STEPS; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int p = 0; p < np; ++p) {
+      load(p, x, wk);
+#pragma unroll
+      for (int k = 0; k < STEPS; ++k) acc[k] += wk[k] * x[k];
     }
 #pragma unroll
-    for (int it = 0; it < ITEMS; ++it) acc[it] += wgt[it] * x[it];
-  }
-#pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    if (!live[it]) continue;
-    const bf16x4 out{(__bf16)acc[it][0], (__bf16)acc[it][1], (__bf16)acc[it][2], (__bf16)acc[it][3]};
-    *(bf16x4*)(a.o_out + rh[it] * D + 4 * part) = out;
-    if (part == 0) a.lse_out[li[it]] = Lm[it];
+    for (int k = 0; k < STEPS; ++k) {
+      const int j = RPI * k + sub;
+      if (v0 + j >= a.rows) continue;
+      const bf16x4 out{(__bf16)acc[k][0], (__bf16)acc[k][1], (__bf16)acc[k][2], (__bf16)acc[k][3]};
+      *(bf16x4*)(a.o_out + ((r0 + j) * a.hq + h) * D + d0) = out;
+    }
+    if (pg == 0 && row_ok) a.lse_out[h * a.n + r0 + r16] = Lm;
+    __builtin_amdgcn_wave_barrier();  // the next group's weights overwrite w_s only after every read
   }
 }
 
@@ -436,13 +447,10 @@ hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const floa
       else hipLaunchKernelGGL((lse_merge_few_kernel<64, 4>), grid, block, 0, s, a);
     }
   } else {
-    constexpr int ITEMS = 4;
-    const int64_t threads = a.rows * heads_q * (head_dim / 4);
-    const int64_t blocks = (threads + 256 * ITEMS - 1) / (256 * ITEMS);
-    if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "problem too large");
-    const dim3 grid((unsigned)blocks);
-    if (head_dim == 128) hipLaunchKernelGGL((lse_merge_kernel<128, ITEMS>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((lse_merge_kernel<64, ITEMS>), grid, block, 0, s, a);
+    const int64_t groups = ((a.rows + 15) / 16) * heads_q;
+    const dim3 grid((unsigned)std::min<int64_t>((groups + 3) / 4, 65536));
+    if (head_dim == 128) hipLaunchKernelGGL((lse_merge_many_kernel<128>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((lse_merge_many_kernel<64>), grid, block, 0, s, a);
   }
   return check_launch("lse_merge");
 }
