@@ -14,11 +14,15 @@ sustained load), then the warm-up steps, then the timed steps with nothing
 between the launches; a second pass of the same steps with events around
 each stage gives the per-kernel breakdown.
 
-Default workload: 32768-token packed sequence, log-normal documents, 32
-heads of 128, sequence-parallel degree 8 (contiguous), shard 3, forward.
+Default workload: the largest single-GPU configuration, a 262144-token packed
+sequence with Pareto document lengths, head-parallel degree 4 x ring degree 8
+(contiguous): the shard holds 8 of 32 heads of 128 and 1/8 of the tokens, shard
+4 (the one with the most allowed pairs), forward.  The other workloads are
+reported under "extra", each with its own roofline figures; a name with "+bwd"
+runs that workload forward + backward.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
-  python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload c2]
+  python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload c4]
 """
 from __future__ import annotations
 
@@ -93,12 +97,15 @@ def _merged_rows(L, cu, sd, split: int):
 
 
 def measure(name: str, steps: int, warmup: int, backward=None):
-    """Time `steps` steps of one workload through the step executor; returns a result dict (GPU side only)."""
+    """Time `steps` steps of one workload through the step executor; returns a result dict (GPU side only).
+    A name ending in "+bwd" runs the workload forward + backward."""
     import torch
     from paper_2606_30460_amd import _lib as L
     from paper_2606_30460_amd.shard_attention import to_sharded
     from workloads import make_workload
 
+    if name.endswith("+bwd"):
+        name, backward = name[:-4], True
     w = make_workload(name)
     bwd = w.backward if backward is None else backward
     shard = w.shard if w.shard is not None else _critical_shard(L, w)
@@ -200,7 +207,7 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     bwd_flops = 10.0 * w.head_dim * w.heads_q * pairs if bwd else 0.0
     ms_step = wall / steps * 1e3
     res = {
-        "workload": w.name, "shard": shard, "tokens": w.total_tokens, "batch": w.batch, "sp_degree": w.sp_degree,
+        "workload": w.name, "workload_key": name, "shard": shard, "tokens": w.total_tokens, "batch": w.batch, "sp_degree": w.sp_degree,
         "layout": w.layout, "heads_q": w.heads_q, "heads_kv": w.heads_kv, "head_dim": w.head_dim,
         "block_m": w.block_m, "block_n": w.block_n, "backward": bool(bwd), "docs": w.num_docs,
         "useful_pairs": pairs, "tiles": tiles, "full_tiles": info["num_full_tiles"],
@@ -224,6 +231,15 @@ def measure(name: str, steps: int, warmup: int, backward=None):
     if bwd:
         res.update({"bwd_ms_mean": float(bwd_ms.mean()), "bwd_ms_median": float(np.median(bwd_ms)),
                     "bwd_tflops": bwd_flops / (bwd_ms.mean() * 1e-3) / 1e12})
+    # the dominant kernel's roofline figures: useful flops of one launch over its mean duration
+    fwd_achieved = fwd_flops / (fwd_ms.mean() * 1e-3) / 1e12
+    res["roofline"] = {"bound": "mfma", "kernel": fwd_kernel_name(res), "achieved": round(fwd_achieved, 3),
+                       "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(fwd_achieved / PEAK_BF16_TFLOPS, 5)}
+    if bwd:
+        bwd_achieved = bwd_flops / (bwd_ms.mean() * 1e-3) / 1e12
+        res["roofline_bwd"] = {"bound": "mfma", "kernels": bwd_kernel_names(res), "achieved": round(bwd_achieved, 3),
+                               "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                               "frac": round(bwd_achieved / PEAK_BF16_TFLOPS, 5)}
     res["_fwd_flops"] = fwd_flops
     log("[bench] %s: %.3f ms/step, %.1f TFLOP/s useful (fwd kernel %.3f ms = %.1f TFLOP/s)" % (
         w.name, ms_step, res["tflops"], res["fwd_kernel_ms_mean"], res["fwd_kernel_tflops"]))
@@ -412,7 +428,7 @@ def fp8_analysis(name: str, reps: int = 50) -> dict:
 
 FWD_SOURCES = ("paper_2606_30460_amd/csrc/attn_fwd.hip", "paper_2606_30460_amd/csrc/mfma.h",
                "paper_2606_30460_amd/csrc/hsap_internal.h")
-TRAFFIC_SUMMARY = "profiles/attn_fwd_hbm_traffic.md"
+TRAFFIC_GLOB = "profiles/attn_fwd_hbm_traffic*.md"
 
 
 def fwd_source_hash() -> str:
@@ -433,28 +449,37 @@ def fwd_kernel_name(res) -> str:
     return "attn_fwd_kernel<%d, %d, %d, false, false>" % (d, bn, bm // 32)
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per forward launch from the committed counter summary, or None.
+def bwd_kernel_names(res) -> list:
+    """The two backward kernels the library dispatches for a workload's shapes (bf16 gradients)."""
+    d, bm, bn = res["head_dim"], res["block_m"], res["block_n"]
+    return ["attn_bwd_dkdv_kernel<%d, %d, true>" % (d, bn // 32),
+            "attn_bwd_dq_kernel<%d, %d, %d, true>" % (d, bn, bm // 32)]
 
-    The summary records the bytes measured with rocprofv3 (FETCH_SIZE +
-    WRITE_SIZE, scaled by a plain copy of known size) together with the hash of
-    the forward kernel's sources at the time; a changed kernel reports None.
+
+def measured_traffic(workload: str):
+    """HBM bytes per forward launch from the committed counter summary of this workload, or None.
+
+    Each summary (profiles/attn_fwd_hbm_traffic*.md) records the bytes measured with rocprofv3
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size) together with the workload and
+    the hash of the forward kernel's sources at the time; a changed kernel reports None.
     """
-    path = os.path.join(ROOT, TRAFFIC_SUMMARY)
-    if not os.path.exists(path):
-        return None
-    fields = {}
-    with open(path) as f:
-        for line in f:
-            if line.startswith("- ") and ":" in line:
-                k, v = line[2:].split(":", 1)
-                fields[k.strip()] = v.strip().strip("`")
-    if fields.get("kernel_source_sha256_16") != fwd_source_hash() or fields.get("workload") != workload:
-        return None
-    try:
-        return int(fields["hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+    import glob
+    for path in sorted(glob.glob(os.path.join(ROOT, TRAFFIC_GLOB))):
+        fields = {}
+        with open(path) as f:
+            for line in f:
+                if line.startswith("- ") and ":" in line:
+                    k, v = line[2:].split(":", 1)
+                    fields[k.strip()] = v.strip().strip("`")
+        if fields.get("workload") != workload:
+            continue
+        if fields.get("kernel_source_sha256_16") != fwd_source_hash():
+            return None
+        try:
+            return int(fields["hbm_bytes_per_launch"])
+        except (KeyError, ValueError):
+            return None
+    return None
 
 
 def calibrate_copy(nbytes: int) -> None:
@@ -474,8 +499,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2")
-    ap.add_argument("--extra", default="c3,c4,c5,c6", help="other workloads reported under 'extra' ('' for none)")
+    ap.add_argument("--workload", default="c4")
+    ap.add_argument("--extra", default="c2,c3,c5,c5m,c6,c3+bwd,c4+bwd",
+                    help="other workloads reported under 'extra' ('' for none); 'name+bwd' runs forward + backward")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle budget for the CPU baseline (0: skip)")
     ap.add_argument("--no-all-shards", action="store_true",
                     help="skip the all-shard load analysis of the main workload (e.g. under a kernel trace)")
@@ -511,7 +537,7 @@ def main():
     if not args.no_all_shards:       # analyses beside the timed step, skipped under kernel traces
         for name, res in [(args.workload, main_res)] + list(extra.items()):
             if not res["backward"]:
-                res["fp8_scores"] = fp8_analysis(name)
+                res["fp8_scores"] = fp8_analysis(res["workload_key"])
     if not args.no_all_shards:
         main_res["all_shards"] = all_shards_analysis(args.workload)
     cpu = None
@@ -519,8 +545,9 @@ def main():
         log("[bench] CPU baseline (oracle) on %s, ~%.0f s" % (args.workload, args.cpu_seconds))
         cpu = cpu_baseline(args.workload, args.cpu_seconds)
 
-    fwd_flops = main_res.pop("_fwd_flops")
-    achieved = fwd_flops / (main_res["fwd_kernel_ms_mean"] * 1e-3) / 1e12
+    main_res.pop("_fwd_flops")
+    roof = dict(main_res["roofline"])
+    roof.update({"traffic": measured_traffic(main_res["workload_key"]), "kernel_source_sha256_16": fwd_source_hash()})
     line = {
         "metric": METRIC,
         "value": round(main_res["tflops"], 3),
@@ -540,9 +567,7 @@ def main():
                    "block_m": main_res["block_m"], "block_n": main_res["block_n"], "pass": "forward"
                    if not main_res["backward"] else "forward+backward"},
         "pct_of_bf16_peak": round(100.0 * main_res["tflops"] / PEAK_BF16_TFLOPS, 3),
-        "roofline": {"bound": "mfma", "kernel": fwd_kernel_name(main_res), "achieved": round(achieved, 3),
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
-                     "traffic": measured_traffic(args.workload), "kernel_source_sha256_16": fwd_source_hash()},
+        "roofline": roof,
         "cpu_baseline": cpu,
         "detail": main_res,
         "extra": extra,

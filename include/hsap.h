@@ -198,6 +198,19 @@ int32_t hsap_split_length(const hsap_shard_desc* shard, int64_t num_tiles, int32
                           int32_t resident_workgroups);
 
 /*
+ * hsap_fwd_resident_workgroups -- workgroups of the bf16 partial forward that
+ * fit on the current device at once for the shapes in `desc`: the HIP
+ * runtime's occupancy of the kernel hsap_partial_attn_fwd dispatches for
+ * (head_dim, BM, BN) (its registers, LDS and workgroup size), times the
+ * device's compute units -- the resident_workgroups of hsap_split_length.
+ * Not in the paper (scheduling of this library's kernels).
+ *   out  host int32, written (0 on failure).
+ * Returns HSAP_ERR_UNSUPPORTED for shapes without a forward kernel and
+ * HSAP_ERR_HIP when the device cannot be queried.
+ */
+hsap_status hsap_fwd_resident_workgroups(const hsap_attn_desc* desc, int32_t* out);
+
+/*
  * hsap_load_matrix -- the size of every rank block of the packed sequence
  * (host): for each shard r (query rows) and chunk c (key rows), the number of
  * non-empty tiles and of allowed (query, key) pairs per head that hsap_plan
@@ -321,7 +334,10 @@ hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, voi
  *              softmax scale.  Supported: d in {64, 128}; BM in {64, 128},
  *              or 256 with d = 128; BN in {64, 128}; Hq % Hkv == 0.
  *   q          device bf16 [n, Hq, d]: shard r's queries, local row order.
- *   k, v       device bf16 [P, n, Hkv, d]: every chunk, sharded order.
+ *   k, v       device bf16 [P, n, Hkv, d]: every chunk, sharded order.  Only
+ *              the rows of the chunks that the passed runs' tiles name are
+ *              read, so a caller holding one received chunk c alone may pass
+ *              the address that chunk 0 would have (k_c - c * n * Hkv * d).
  *   doc_start  device int32 [N] from hsap_doc_start.
  *   tiles      device hsap_tile [..]: sorted_tiles of hsap_plan_runs(MAJOR_Q).
  *   runs       device hsap_run [num_runs] from hsap_plan_runs(MAJOR_Q); any
@@ -425,8 +441,17 @@ hsap_status hsap_lse_merge(int32_t num_parts, const float* const* o_parts, const
 
 /*
  * hsap_attn_bwd_preprocess -- delta[h, i] = sum_d dO[i, h, d] * O[i, h, d]
- * (fp32 accumulation), the per-row term of the softmax backward.
- *   o, d_o  device bf16 [n, Hq, d];  delta device fp32 [Hq, n].
+ * (fp32 accumulation), the per-row term of the softmax backward.  The
+ * backward half of each rank's per-step code receives the output gradient of
+ * its query shard (the `do` message of the instruction table of the SAP
+ * section) next to its own O; this is the first thing computed from them,
+ * before the dq / dkv messages go back (differentiating the attention
+ * equation of the inter-group SP section gives dS = P o (dP - delta)).
+ *   o, d_o  device bf16 [n, Hq, d]: shard r's final output and its gradient,
+ *           local row order, 16-byte aligned.
+ *   delta   device fp32 [Hq, n], written (every row).
+ *   n >= 0, heads_q >= 1, head_dim in {64, 128} (else HSAP_ERR_UNSUPPORTED);
+ *   one launch on `stream`, nothing launched for n = 0.
  */
 hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, int32_t heads_q,
                                      int32_t head_dim, float* delta, void* hip_stream);
@@ -440,8 +465,12 @@ hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, 
  * on the stream: one over the k-major runs (dK, dV) and one over the q-major
  * runs (dQ); either list may be empty (count 0) to skip its kernel.
  *
- *   desc, q, k, v, doc_start  as for the forward.  Supported: BM in
- *              {64, 128}; d = 128 with BN in {64, 128}, or d = 64 with BN = 64.
+ *   desc, q, k, v, doc_start  as for the forward.  Supported: d = 128 with
+ *              BM in {64, 128, 256} and BN in {64, 128}; d = 64 with BM in
+ *              {64, 128} and BN = 64.  The q-major runs (dQ kernel) further
+ *              need sp_degree <= 256 and fewer than 2^23 k-tiles per chunk
+ *              (packed tile descriptors); HSAP_ERR_UNSUPPORTED otherwise,
+ *              before anything is launched.
  *   d_o        device bf16 [n, Hq, d] (shard r, local rows).
  *   lse        device fp32 [Hq, n]: the merged forward LSE.
  *   delta      device fp32 [Hq, n] from hsap_attn_bwd_preprocess.
@@ -548,11 +577,12 @@ typedef struct {
 /*
  * hsap_executor_create -- an executor for the shard and heads in `desc`
  * (same supported shapes as hsap_partial_attn_fwd; with HSAP_EXEC_BACKWARD
- * those of hsap_partial_attn_bwd).
+ * also those of hsap_partial_attn_bwd, checked here: HSAP_ERR_UNSUPPORTED
+ * before anything is allocated).
  *   options        HSAP_EXEC_* bits.
  *   max_run_tiles  q-major split: -1 picks hsap_split_length per plan from
- *                  the device's compute-unit count, 0 never splits, > 0 is
- *                  used as given.  A plan whose split would need more than
+ *                  hsap_fwd_resident_workgroups of the device current at
+ *                  creation, 0 never splits, > 0 is used as given.  A plan whose split would need more than
  *                  HSAP_MAX_MERGE_PARTS partials is planned without split.
  *   out            receives the executor; NULL on failure.
  * Returns HSAP_ERR_HIP when device or pinned memory cannot be allocated.

@@ -34,7 +34,8 @@ MAX_MERGE_PARTS = 64
 
 # Every symbol include/hsap.h declares.
 EXPORTED = (
-    "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length", "hsap_load_matrix",
+    "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length",
+    "hsap_fwd_resident_workgroups", "hsap_load_matrix",
     "hsap_balance", "hsap_emit_forward", "hsap_doc_start",
     "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_quantize_fp8",
     "hsap_partial_attn_fwd_fp8", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
@@ -96,6 +97,7 @@ _SIG = {
     "hsap_plan": (ctypes.c_int, [_P, _I32, _P, _P, _I64, _P, _P, _P]),
     "hsap_plan_runs": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P, _I64, _P, _P]),
     "hsap_split_length": (ctypes.c_int32, [_P, _I64, _I32, _I32]),
+    "hsap_fwd_resident_workgroups": (ctypes.c_int, [_P, _P]),
     "hsap_load_matrix": (ctypes.c_int, [_P, _I32, _P, _P, _P]),
     "hsap_balance": (ctypes.c_int, [_I32, _P, _P, _P]),
     "hsap_emit_forward": (ctypes.c_int, [_I32, _P, _P, _P, _I64, _P, _P]),
@@ -253,6 +255,13 @@ def split_length(shard: ShardDesc, num_tiles: int, heads_q: int, resident_workgr
     return v
 
 
+def fwd_resident_workgroups(desc: AttnDesc) -> int:
+    """hsap_fwd_resident_workgroups: partial-forward workgroups resident on the current device."""
+    out = ctypes.c_int32(0)
+    _check(lib().hsap_fwd_resident_workgroups(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
 def plan_into(cu_seqlens: np.ndarray, shard: ShardDesc, tiles_out: np.ndarray, step_offsets_out: np.ndarray,
               useful_pairs_out: np.ndarray) -> int:
     """hsap_plan into caller-provided host buffers (e.g. views of pinned memory).
@@ -341,13 +350,22 @@ def shard_gather(shard: ShardDesc, src, dst, stream=None) -> None:
 
 
 def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev, o_part, lse_part,
-                     stream=None) -> None:
+                     stream=None, kv_chunk: Optional[int] = None) -> None:
+    """hsap_partial_attn_fwd.  k / v are [P, n, Hkv, d] (every chunk, sharded order), or, with
+    ``kv_chunk`` = c, [n, Hkv, d] holding chunk c alone (every run passed must be of chunk c):
+    the library then gets the address chunk 0 would have, and reads only chunk c's rows."""
     s = desc.shard
     n = s.rows
     hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
     _dev(q, "bfloat16", "q", n * hq * d)
-    _dev(k, "bfloat16", "k", P * n * hkv * d)
-    _dev(v, "bfloat16", "v", P * n * hkv * d)
+    kv_rows = P if kv_chunk is None else 1
+    _dev(k, "bfloat16", "k", kv_rows * n * hkv * d)
+    _dev(v, "bfloat16", "v", kv_rows * n * hkv * d)
+    kv_shift = 0
+    if kv_chunk is not None:
+        if not 0 <= int(kv_chunk) < P:
+            raise ValueError("kv_chunk %d outside [0, %d)" % (kv_chunk, P))
+        kv_shift = int(kv_chunk) * n * hkv * d * 2
     _dev(doc_start_dev, "int32", "doc_start", s.positions)
     _dev(tiles_dev, "int32", "tiles")
     _dev(runs_dev, "int32", "runs")
@@ -356,7 +374,8 @@ def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev
     slots = o_part.numel() // (n * hq * d)
     if o_part.numel() != slots * n * hq * d or lse_part.numel() != slots * hq * n or slots < 1:
         raise ValueError("o_part / lse_part must hold a whole number of [n, Hq, d] / [Hq, n] slots")
-    _check(lib().hsap_partial_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(doc_start_dev),
+    _check(lib().hsap_partial_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k) - kv_shift, _ptr(v) - kv_shift,
+                                       _ptr(doc_start_dev),
                                        _ptr(tiles_dev), _ptr(runs_dev), runs_dev.numel() // 4, _ptr(o_part),
                                        _ptr(lse_part), int(slots), _stream(stream)))
 

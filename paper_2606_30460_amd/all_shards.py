@@ -69,7 +69,7 @@ class AllShards:
         self.cu_dev = torch.from_numpy(self.cu_host).to(dev)
         self.doc_start = torch.empty(self.N, dtype=torch.int32, device=dev)
         L.doc_start(self.cu_dev, self.N, self.doc_start)
-        resident = _resident_workgroups(dev, self.bm, self.d)
+        resident = _resident_workgroups(dev, L.attn_desc(base, self.hq, self.hkv, self.d, self.scale))
         self.descs, self.tiles_dev, self.parts = [], [], []
         # runs[e][r]: device run list of shard r's blocks that rank e computes (None if none)
         self.runs: List[List[Optional[torch.Tensor]]] = [[None] * P for _ in range(P)]

@@ -560,6 +560,23 @@ static hsap_status launch_dq(const BwdArgs& a, int64_t num_runs, hipStream_t str
 }
 
 
+// Packed tile descriptors of the dQ kernel: chunks below 256, k-tiles below 2^23.
+constexpr int kMaxDqChunks = 256;
+constexpr int64_t kMaxDqKTiles = int64_t(1) << 23;
+
+}  // namespace hsap
+
+// (head_dim, BM, BN) combinations with both backward kernels: the dK/dV kernel takes any BM that
+// is a multiple of 64 (64-row sub-tiles) and BN = 32 x waves; the dQ kernel BM = 32 x waves.
+bool hsap::backward_supported(const hsap_attn_desc* desc) {
+  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
+  const bool dkdv_ok = bm % 64 == 0 && ((d == 128 && (bn == 128 || bn == 64)) || (d == 64 && bn == 64));
+  const bool dq_ok = (bm == 128 || bm == 64 || (bm == 256 && d == 128)) && (bn == 128 || bn == 64);
+  return dkdv_ok && dq_ok;
+}
+
+namespace hsap {
+
 // shared checks and dispatch of the fp32-accumulating and the bf16-storing backward
 template <bool BF16OUT>
 // o == NULL: delta is an input.  Otherwise the dQ kernel computes delta from o and d_o into
@@ -574,12 +591,13 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
   if (st != HSAP_OK) return st;
   if (num_runs_k < 0 || num_runs_q < 0) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "negative run count");
   const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
-  if (bm % 64) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "backward needs BM a multiple of 64 (BM=%d)", bm);
-  const bool dkdv_ok = (d == 128 && (bn == 128 || bn == 64)) || (d == 64 && bn == 64);
-  const bool dq_ok = (bm == 128 || bm == 64) && (bn == 128 || bn == 64);
-  if (!dkdv_ok || !dq_ok)
+  if (!backward_supported(desc))
     HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no backward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
   if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
+  // the dQ kernel packs a tile descriptor as k_tile | chunk << 23 | kind << 31
+  if (num_runs_q > 0 && (geom.P > kMaxDqChunks || geom.n / bn >= kMaxDqKTiles))
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "the dQ kernel needs sp_degree <= %d and fewer than 2^23 k-tiles per chunk "
+              "(sp_degree %d)", kMaxDqChunks, geom.P);
   if (num_runs_k == 0 && num_runs_q == 0) return HSAP_OK;
   if (!q || !k || !v || !d_o || !lse || !(o ? delta_out : delta) || !doc_start || !dq || !dk || !dv ||
       (num_runs_k > 0 && (!tiles_k || !runs_k)) || (num_runs_q > 0 && (!tiles_q || !runs_q)))
@@ -622,7 +640,9 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
     a.runs = runs_q;
 #define HSAP_DQ_CASE(D_, BN_, W_) \
   if (d == D_ && bn == BN_ && bm == 32 * W_) st = launch_dq<D_, BN_, W_, BF16OUT>(a, num_runs_q, s);
-    HSAP_DQ_CASE(128, 128, 4)
+    HSAP_DQ_CASE(128, 128, 8)
+    else HSAP_DQ_CASE(128, 64, 8)
+    else HSAP_DQ_CASE(128, 128, 4)
     else HSAP_DQ_CASE(128, 64, 4)
     else HSAP_DQ_CASE(128, 128, 2)
     else HSAP_DQ_CASE(128, 64, 2)

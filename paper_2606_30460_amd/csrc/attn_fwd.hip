@@ -120,6 +120,12 @@ __device__ __forceinline__ int32_t doc_window_start(const FwdArgs& a, const DocW
   return start;
 }
 
+// fp8 scores: the exp2 scale of a step, q_scale[h] * k_scale[chunk, g] * scale * log2(e), kept at
+// or above the smallest normal float.  A scale is 0 only when its slice is all zeros, so every
+// code and every finite score of the step is 0 and stays 0 after the multiply, while a masked
+// score (-inf) must stay -inf: times 0 it would turn into NaN and poison the row.
+__device__ __forceinline__ float fp8_step_scale(float sl) { return fmaxf(sl, 1.17549435e-38f); }
+
 // FP8: Q and K are e4m3 codes (scores S = (Q8 K8^T) * q_scale[h] * k_scale[chunk, g]
 // from the 32x32x64 fp8 MFMA, a K row held as 128 bytes), V and the rest as in bf16.
 template <int D, int BN, int WAVES, bool FUSED, bool FP8 = false>
@@ -303,7 +309,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   auto step = [&](int s, auto par, f32x16 (&sc)[KB / 32], f32x16 (&sn)[KB / 32]) __attribute__((always_inline)) {
     constexpr int PAR = decltype(par)::value;
     const hsap_tile tile = tile_at(s);
-    const float sl = FP8 ? head_scale * a.k_scale[tile.chunk * a.hkv + g] : head_scale;
+    const float sl = FP8 ? fp8_step_scale(head_scale * a.k_scale[tile.chunk * a.hkv + g]) : head_scale;
     if (s + 2 < total) load_k(step_off(tile_at(s + 2), s + 2));
     if (s + 1 < total) load_v(step_off(tile_at(s + 1), s + 1));
     // scores of the next step: independent of this step's softmax
@@ -628,7 +634,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     // the window of tile (s + NSLOT) / SUBS is needed now (rare vector load: every 64 tiles)
     if (s + NSLOT < total && ((s + NSLOT) / SUBS) >> 6 > win_hi) load_window(win_hi + 1);
     const uint32_t tile = tile_at(s);
-    const float sl = FP8 ? head_scale * kscale_s[chunk_of(tile)] : head_scale;
+    const float sl = FP8 ? fp8_step_scale(head_scale * kscale_s[chunk_of(tile)]) : head_scale;
     // s % NSLOT, (s + 1) % NSLOT and (s + NSLOT - 1) % NSLOT: this step's slot, the slot of the
     // next scores and of V's refill
     const int s0 = NSLOT == 2 ? PAR : sk;
@@ -843,9 +849,61 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
   HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no forward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
 }
 
+// Workgroups of the bf16 partial forward resident on one compute unit, from the runtime's
+// occupancy calculation for the kernel forward() dispatches for this shape (its registers, LDS
+// and workgroup size); 0 when the shape has no kernel or the query fails.
+template <typename Kernel>
+static int blocks_per_cu(Kernel kernel, int threads) {
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, threads, 0) != hipSuccess) return 0;
+  return blocks;
+}
+
+int fwd_resident_per_cu(const hsap_attn_desc* desc) {
+  Geom geom;
+  if (check_attn(desc, &geom) != HSAP_OK) return 0;
+  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
+  if (bn != 64 && bn != 128) return 0;
+  const bool dl = d == 128 && (bm == 128 || bm == 256) && geom.P <= kMaxDlChunks && geom.n / bn < kMaxDlKTiles;
+  if (dl && bm == 256)
+    return bn == 128 ? blocks_per_cu(attn_fwd_dl_kernel<128, 8, false>, 512) : blocks_per_cu(attn_fwd_dl_kernel<64, 8, false>, 512);
+  if (dl) return bn == 128 ? blocks_per_cu(attn_fwd_dl_kernel<128, 4, false>, 256) : blocks_per_cu(attn_fwd_dl_kernel<64, 4, false>, 256);
+#define HSAP_OCC_CASE(D_, BN_, W_) \
+  if (d == D_ && bn == BN_ && bm == 32 * W_) return blocks_per_cu(attn_fwd_kernel<D_, BN_, W_, false>, 64 * W_);
+  HSAP_OCC_CASE(128, 128, 4)
+  HSAP_OCC_CASE(128, 64, 4)
+  HSAP_OCC_CASE(128, 128, 2)
+  HSAP_OCC_CASE(128, 64, 2)
+  HSAP_OCC_CASE(64, 128, 4)
+  HSAP_OCC_CASE(64, 64, 4)
+  HSAP_OCC_CASE(64, 128, 2)
+  HSAP_OCC_CASE(64, 64, 2)
+#undef HSAP_OCC_CASE
+  return 0;
+}
+
 }  // namespace hsap
 
 using namespace hsap;
+
+extern "C" hsap_status hsap_fwd_resident_workgroups(const hsap_attn_desc* desc, int32_t* out) {
+  clear_error();
+  if (!out) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "out is NULL");
+  *out = 0;
+  Geom geom;
+  const hsap_status st = check_attn(desc, &geom);
+  if (st != HSAP_OK) return st;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "device query: %s", hipGetErrorString(e));
+  const int per_cu = fwd_resident_per_cu(desc);
+  if (per_cu <= 0)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no forward kernel occupancy for head_dim=%d BM=%d BN=%d", desc->head_dim,
+              desc->shard.block_m, desc->shard.block_n);
+  *out = per_cu * cus;
+  return HSAP_OK;
+}
 
 extern "C" hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
                                              const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,

@@ -12,15 +12,6 @@ using namespace hsap;
 
 namespace {
 
-// Forward workgroups resident per compute unit: the kernel runs two waves per SIMD (eight
-// per CU, BM / 32 per workgroup) and double-buffers 64-key K and V steps in LDS (rows padded
-// by 8 and 32 elements) out of 160 KiB.
-int fwd_resident_per_cu(int bm, int d) {
-  const int by_waves = std::max(1, 8 / std::max(1, bm / 32));
-  const int lds = 2 * 64 * (d + 8) * 2 + 2 * 64 * (d + 32) * 2;
-  return std::min(by_waves, std::max(1, 160 * 1024 / lds));
-}
-
 // Pinned staging buffers for the list uploads, used in a ring.  The host may rewrite a buffer only
 // once the copy out of it has run; an event tells it so, but an event marker costs the stream a
 // gap of several microseconds, so one is recorded only after every kEventEvery-th upload: before
@@ -173,6 +164,9 @@ hsap_status hsap_executor_create(const hsap_attn_desc* desc, int32_t options, in
   if (desc->shard.sp_degree > HSAP_MAX_MERGE_PARTS)
     HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "sp_degree %d above the merge limit %d", desc->shard.sp_degree,
               HSAP_MAX_MERGE_PARTS);
+  if ((options & HSAP_EXEC_BACKWARD) && !backward_supported(desc))
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no backward kernel for head_dim=%d BM=%d BN=%d", desc->head_dim,
+              desc->shard.block_m, desc->shard.block_n);
 
   hsap_executor* ex = new hsap_executor();
   ex->desc = *desc;
@@ -198,7 +192,7 @@ hsap_status hsap_executor_create(const hsap_attn_desc* desc, int32_t options, in
     release(ex);
     return hip_fail("create", e);
   }
-  ex->resident_workgroups = fwd_resident_per_cu(desc->shard.block_m, desc->head_dim) * std::max(cus, 1);
+  ex->resident_workgroups = std::max(1, fwd_resident_per_cu(desc)) * std::max(cus, 1);
   *out = ex;
   return HSAP_OK;
 }

@@ -66,6 +66,16 @@ hsap_status check_shard(const hsap_shard_desc* d, Geom* g);
 // Validates an attention descriptor (shard part plus heads, head_dim, scale).
 hsap_status check_attn(const hsap_attn_desc* d, Geom* g);
 
+// Whether the backward kernels exist for the descriptor's (head_dim, BM, BN); the descriptor
+// must already pass check_attn.
+bool backward_supported(const hsap_attn_desc* d);
+
+#if defined(__HIPCC__)
+// Workgroups of the bf16 partial forward resident on one compute unit for the descriptor's shape
+// (the runtime's occupancy of the kernel that runs); 0 when there is none.
+int fwd_resident_per_cu(const hsap_attn_desc* d);
+#endif
+
 #if defined(__HIPCC__)
 // Zeroes tiles tiles[0 .. num_tiles-1] (device int32) of both a and b, tile t being the byte
 // range [t * tile_bytes, (t + 1) * tile_bytes); tile_bytes a multiple of 16, a and b 16-byte

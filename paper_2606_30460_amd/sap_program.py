@@ -2,8 +2,10 @@
 executed on one GPU with one HIP stream standing in for each rank.
 
 Every rank gets the buffers the lists name: its own Q shard and K/V chunk (views of the
-sharded inputs), two receive slots for Q and for K/V, two result slots for partials it
-computes for other shards, and one part slot per chunk with tiles of its own shard.  A
+sharded inputs), two receive slots for Q and for K/V (one shard or one chunk each: the
+partial forward is given the address chunk 0 would have, so that it reads the received
+chunk's rows from the slot), two result slots for partials it computes for other shards,
+and one part slot per chunk with tiles of its own shard.  A
 stage runs on every rank's stream after all ranks finished the previous stage (the batched
 point-to-point group of a stage); within it a rank's receives are device copies from the
 peer's buffer, its computation is hsap_partial_attn_fwd over that block's q-major runs, and
@@ -79,9 +81,9 @@ class SapProgram:
         bf, f32 = torch.bfloat16, torch.float32
         return {
             "q_recv": [torch.empty(2, n, self.hq, self.d, dtype=bf, device=dev) for _ in range(P)],
-            # receive slots hold one chunk each, in the [P, n, Hkv, d] layout the kernel indexes by chunk
-            "k_recv": [torch.empty(2, P, n, self.hkv, self.d, dtype=bf, device=dev) for _ in range(P)],
-            "v_recv": [torch.empty(2, P, n, self.hkv, self.d, dtype=bf, device=dev) for _ in range(P)],
+            # receive slots hold one chunk each
+            "k_recv": [torch.empty(2, n, self.hkv, self.d, dtype=bf, device=dev) for _ in range(P)],
+            "v_recv": [torch.empty(2, n, self.hkv, self.d, dtype=bf, device=dev) for _ in range(P)],
             "o_res": [torch.empty(2, n, self.hq, self.d, dtype=f32, device=dev) for _ in range(P)],
             "lse_res": [torch.empty(2, self.hq, n, dtype=f32, device=dev) for _ in range(P)],
             "o_part": [torch.empty(max(p, 1), n, self.hq, self.d, dtype=f32, device=dev) for p in self.parts],
@@ -118,21 +120,24 @@ class SapProgram:
                             if tensor == L.T_Q:
                                 bufs["q_recv"][e][out_slot].copy_(q[peer])
                             elif tensor == L.T_KV:
-                                bufs["k_recv"][e][out_slot][peer].copy_(k[peer])
-                                bufs["v_recv"][e][out_slot][peer].copy_(v[peer])
+                                bufs["k_recv"][e][out_slot].copy_(k[peer])
+                                bufs["v_recv"][e][out_slot].copy_(v[peer])
                             else:
                                 src = self._send_slot(peer, e, t, shard, chunk)
                                 bufs["o_part"][e][out_slot].copy_(bufs["o_res"][peer][src])
                                 bufs["lse_part"][e][out_slot].copy_(bufs["lse_res"][peer][src])
                         elif op == L.OP_COMPUTE:
                             qq = q[e] if shard == e else bufs["q_recv"][e][in_slot]
-                            kk, vv = (k, v) if chunk == e else (bufs["k_recv"][e][in_slot], bufs["v_recv"][e][in_slot])
+                            # the own chunk, or the receive slot holding chunk `chunk` alone
+                            kk, vv = k[chunk], v[chunk]
+                            if chunk != e:
+                                kk, vv = bufs["k_recv"][e][in_slot], bufs["v_recv"][e][in_slot]
                             if shard == e:
                                 ob, lb = bufs["o_part"][e], bufs["lse_part"][e]
                             else:
                                 ob, lb = bufs["o_res"][e], bufs["lse_res"][e]
                             L.partial_attn_fwd(self.descs[shard], qq, kk, vv, self.doc_start, self.tiles_dev[shard],
-                                               self._runs(shard, chunk, out_slot), ob, lb, stream=s)
+                                               self._runs(shard, chunk, out_slot), ob, lb, stream=s, kv_chunk=chunk)
                         elif op == L.OP_MERGE:
                             parts = out_slot
                             L.lse_merge([bufs["o_part"][e][i] for i in range(parts)],

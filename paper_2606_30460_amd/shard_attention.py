@@ -29,13 +29,12 @@ import torch
 
 from . import _lib as L
 
-def _resident_workgroups(device, block_m: int, head_dim: int) -> int:
-    """Forward workgroups resident on the device: two waves per SIMD (eight per CU, BM / 32
-    per workgroup), bounded by the double-buffered K/V staging in 160 KiB of LDS."""
-    by_waves = max(1, 8 // max(1, block_m // 32))
-    lds = 2 * 64 * (head_dim + 8) * 2 + 2 * 64 * (head_dim + 32) * 2
-    per_cu = min(by_waves, max(1, 160 * 1024 // lds))
-    return per_cu * torch.cuda.get_device_properties(device).multi_processor_count
+def _resident_workgroups(device, desc) -> int:
+    """Forward workgroups resident on ``device`` for the shapes in ``desc``: the HIP runtime's
+    occupancy of the partial-forward kernel the library dispatches, times the compute units
+    (hsap_fwd_resident_workgroups)."""
+    with torch.cuda.device(device):
+        return L.fwd_resident_workgroups(desc)
 
 
 class ShardAttention:
@@ -64,8 +63,7 @@ class ShardAttention:
     def _split(self, num_tiles: int) -> int:
         if self.max_run_tiles is not None:
             return int(self.max_run_tiles)
-        return L.split_length(self.shard, num_tiles, self.hq,
-                              _resident_workgroups(self.device, self.shard.block_m, self.d))
+        return L.split_length(self.shard, num_tiles, self.hq, _resident_workgroups(self.device, self.desc))
 
     # ------------------------------------------------------------------ plan
     def plan(self, backward: bool = False) -> Dict:

@@ -2,10 +2,13 @@
 and the same shard through the fp64 oracle, on the same seeded inputs."""
 from __future__ import annotations
 
+import concurrent.futures
+import os
 from typing import Dict, Optional
 
 import numpy as np
 import torch
+from threadpoolctl import threadpool_limits
 
 import oracle
 from paper_2606_30460_amd import _lib as L
@@ -123,12 +126,61 @@ class Case:
             ex.close()
 
     # --------------------------------------------------------------- oracle
-    def run_oracle(self, rows=None) -> Dict:
+    def run_oracle(self, rows=None, kv_heads=None, backward=None) -> Dict:
+        """The fp64 oracle on this case (backward when the case has one, unless ``backward`` says
+        otherwise).  Heads are independent problems, so the work is split by K/V head over host
+        threads (each oracle call sees a plain head subset) and the results are put back together
+        along the head axes; ``kv_heads`` restricts it to those K/V heads and their query heads."""
+        bwd = self.backward if backward is None else backward
+        kv = list(range(self.hkv)) if kv_heads is None else [int(g) for g in kv_heads]
         q, k, v = self.q.float().numpy(), self.k.float().numpy(), self.v.float().numpy()
-        if self.backward:
-            return oracle.shard_backward(q, k, v, self.do.float().numpy(), self.cu, self.N, self.P, self.layout,
-                                         self.shard)
-        return oracle.shard_forward(q, k, v, self.cu, self.N, self.P, self.layout, self.shard, rows=rows)
+        do = self.do.float().numpy() if bwd else None
+        return oracle_by_kv_heads(q, k, v, do, self.cu, self.N, self.P, self.layout, self.shard, kv, rows=rows)
+
+    def q_heads(self, kv_heads) -> np.ndarray:
+        """Query heads that read the given K/V heads, in order."""
+        group = self.hq // self.hkv
+        return np.concatenate([np.arange(g * group, (g + 1) * group) for g in kv_heads])
+
+
+def _oracle_workers() -> int:
+    return max(1, len(os.sched_getaffinity(0)) // 2)
+
+
+def oracle_by_kv_heads(q, k, v, do, cu, N, P, layout, shard, kv_heads, rows=None) -> Dict:
+    """oracle.shard_forward (do is None) or oracle.shard_backward for the given K/V heads and the
+    query heads that read them, one K/V head per task on a pool of host threads with two BLAS
+    threads each; results are concatenated along the head axes in the order of ``kv_heads``."""
+    hq, hkv = q.shape[1], k.shape[1]
+    group = hq // hkv
+
+    def one(g):
+        hs = slice(g * group, (g + 1) * group)
+        if do is None:
+            return oracle.shard_forward(q[:, hs], k[:, g:g + 1], v[:, g:g + 1], cu, N, P, layout, shard, rows=rows)
+        if rows is not None:
+            raise ValueError("the backward is computed over every row")
+        return oracle.shard_backward(q[:, hs], k[:, g:g + 1], v[:, g:g + 1], do[:, hs], cu, N, P, layout, shard)
+
+    with threadpool_limits(limits=2):
+        with concurrent.futures.ThreadPoolExecutor(min(_oracle_workers(), len(kv_heads))) as pool:
+            parts = list(pool.map(one, kv_heads))
+
+    def fwd_cat(fs):
+        return {"chunks": fs[0]["chunks"], "q_pos": fs[0]["q_pos"],
+                "o_parts": [np.concatenate([f["o_parts"][i] for f in fs], axis=1) for i in range(len(fs[0]["chunks"]))],
+                "lse_parts": [np.concatenate([f["lse_parts"][i] for f in fs], axis=0)
+                              for i in range(len(fs[0]["chunks"]))],
+                "o": np.concatenate([f["o"] for f in fs], axis=1), "lse": np.concatenate([f["lse"] for f in fs], axis=0)}
+
+    if do is None:
+        return fwd_cat(parts)
+    out = fwd_cat([p["fwd"] for p in parts])
+    return {"dq": np.concatenate([p["dq"] for p in parts], axis=1),
+            "dk": np.concatenate([p["dk"] for p in parts], axis=2),
+            "dv": np.concatenate([p["dv"] for p in parts], axis=2),
+            "o": out["o"], "lse": out["lse"], "delta": np.concatenate([p["delta"] for p in parts], axis=0),
+            "fwd": out}
 
 
 def max_abs(a, b) -> float:

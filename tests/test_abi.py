@@ -200,6 +200,29 @@ def test_backward_validates_before_launch():
     assert st == L.HSAP_ERR_INVALID_ARG
 
 
+def test_backward_rejects_dq_beyond_packed_descriptors():
+    # the dQ kernel packs a tile's chunk into 8 bits: more than 256 chunks are rejected before any
+    # launch when q-major runs are passed (the dK/dV kernel alone has no such limit)
+    lib = L.lib()
+    fake = ctypes.c_void_p(4096)
+    d = _attn_desc(sp_degree=260, total_tokens=260 * 128)
+    for fn in (lib.hsap_partial_attn_bwd, lib.hsap_attn_bwd_bf16):
+        st = fn(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 0, fake, fake, 1, fake, fake,
+                fake, None)
+        assert st == L.HSAP_ERR_UNSUPPORTED, lib.hsap_last_error().decode()
+        assert "256" in lib.hsap_last_error().decode()
+
+
+def test_backward_shapes_of_256_row_tiles():
+    # 256-row q-tiles have a backward for head_dim 128 only; a rejected shape launches nothing
+    lib = L.lib()
+    fake = ctypes.c_void_p(4096)
+    d = _attn_desc(block_m=256, head_dim=64, block_n=64, total_tokens=2048)
+    st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
+                                   fake, 1, fake, fake, fake, None)
+    assert st == L.HSAP_ERR_UNSUPPORTED
+
+
 def test_bf16_backward_validates_before_launch():
     lib = L.lib()
     fake = ctypes.c_void_p(4096)
@@ -270,6 +293,15 @@ def test_executor_validates_before_touching_the_device():
     bad_d = L.attn_desc(L.shard_desc(2048, 2, "contiguous", 0, 128, 128), 4, 4, 96, 0.1)
     assert lib.hsap_executor_create(ctypes.byref(bad_d), 0, -1, ctypes.byref(h)) == L.HSAP_ERR_UNSUPPORTED
     assert lib.hsap_executor_create(ctypes.byref(good), 4, -1, ctypes.byref(h)) == L.HSAP_ERR_INVALID_ARG
+    # the backward option needs backward kernels for the shape: refused at creation, before any allocation
+    no_bwd = L.attn_desc(L.shard_desc(2048, 2, "contiguous", 0, 128, 128), 4, 4, 64, 0.1)
+    assert lib.hsap_executor_create(ctypes.byref(no_bwd), L.EXEC_BACKWARD, -1, ctypes.byref(h)) == \
+        L.HSAP_ERR_UNSUPPORTED
+    assert "backward" in lib.hsap_last_error().decode()
+    assert lib.hsap_fwd_resident_workgroups(ctypes.byref(good), None) == L.HSAP_ERR_INVALID_ARG
+    out = ctypes.c_int32(7)
+    assert lib.hsap_fwd_resident_workgroups(ctypes.byref(bad_d), ctypes.byref(out)) == L.HSAP_ERR_UNSUPPORTED
+    assert out.value == 0
     assert lib.hsap_executor_create(ctypes.byref(good), 0, -2, ctypes.byref(h)) == L.HSAP_ERR_INVALID_ARG
     # calls on a NULL executor
     cu = np.asarray([0, 2048], dtype=np.int32)

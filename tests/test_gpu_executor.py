@@ -56,11 +56,9 @@ def test_executor_matches_oracle_and_entry_points(case):
     N, P, layout, hq, hkv, d, bm, bn, mean = case
     cu = _cu(np.random.default_rng(N + P), N, mean)
     r = P - 1
-    bwd = bm <= 128  # the backward has no 256-row q-tile kernel
+    bwd = True
     c = Case(cu, N, P, layout, r, hq, hkv, d, bm, bn, seed=20 + r, backward=bwd)
     ref = c.run_oracle()
-    if not bwd:
-        ref = {"fwd": ref}
     for split in (-1, 0, 1):
         _say("executor", case, "shard", r, "split", split)
         ex = c.run_executor(max_run_tiles=split)

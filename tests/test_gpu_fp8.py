@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from _harness import LSE_ATOL, O_ATOL, max_abs
+from _harness import LSE_ATOL, O_ATOL, max_abs, oracle_by_kv_heads
 from paper_2606_30460_amd import _lib as L
 from paper_2606_30460_amd.shard_attention import ShardAttention, to_sharded
 from workloads import make_workload, random_bf16
@@ -50,7 +50,9 @@ def test_quantize_bit_exact(shape):
 
 def _fp8_forward(cu, N, P, layout, r, hq, hkv, d, bm, bn, q, k, v, split=None):
     """Plan shard r, quantise its Q and every chunk's K on the GPU, run the fp8 partial forward and
-    the merge.  Returns GPU outputs and the dequantised Q / K in global order for the oracle."""
+    the merge.  Returns GPU outputs and the oracle's dequantised Q / K in global order: the
+    oracle quantises the same bf16 inputs itself (its codes and scales must equal the GPU's bit
+    for bit), so no oracle input comes from the GPU."""
     sa = ShardAttention(cu, N, P, layout, r, hq, hkv, d, bm, bn, max_run_tiles=split)
     sa.plan()
     dev = torch.device("cuda")
@@ -66,11 +68,19 @@ def _fp8_forward(cu, N, P, layout, r, hq, hkv, d, bm, bn, q, k, v, split=None):
     L.lse_merge([bufs["o_part"][x] for x in sa.present], [bufs["lse_part"][x] for x in sa.present], sa.n, hq, d,
                 bufs["o"], bufs["lse"])
     torch.cuda.synchronize()
-    # dequantised values in global order (only shard r's query rows are read by the oracle)
+    # the oracle's own quantisation of shard r's Q and of every chunk's K (sharded order, as
+    # the codes are laid out), dequantised back into global order
+    qf, kf = q.float().numpy(), k.float().numpy()
+    q_pos = oracle.shard_positions(N, P, layout, r)
+    k_sh = np.stack([kf[oracle.shard_positions(N, P, layout, c)] for c in range(P)])
+    rq8, rqs = oracle.quantize_fp8(qf[q_pos][None])
+    rk8, rks = oracle.quantize_fp8(k_sh)
+    assert np.array_equal(q8.cpu().numpy(), rq8) and np.array_equal(qs.cpu().numpy(), rqs)
+    assert np.array_equal(k8.cpu().numpy(), rk8) and np.array_equal(ks.cpu().numpy(), rks)
     q_deq = np.zeros((N, hq, d))
     k_deq = np.zeros((N, hkv, d))
-    q_deq[oracle.shard_positions(N, P, layout, r)] = oracle.dequantize_fp8(q8.cpu().numpy(), qs.cpu().numpy())[0]
-    kd = oracle.dequantize_fp8(k8.cpu().numpy(), ks.cpu().numpy())
+    q_deq[q_pos] = oracle.dequantize_fp8(rq8, rqs)[0]
+    kd = oracle.dequantize_fp8(rk8, rks)
     for c in range(P):
         k_deq[oracle.shard_positions(N, P, layout, c)] = kd[c]
     return sa, bufs, q_deq, k_deq
@@ -114,17 +124,37 @@ def test_fp8_forward_matches_oracle(case):
         assert rep["o"] <= O_ATOL and rep["lse"] <= LSE_ATOL, rep
 
 
-def test_fp8_forward_workload_sampled():
-    """The 32768-token log-normal workload's shard with fp8 scores: sampled rows against the oracle."""
+def test_fp8_forward_workload_every_row():
+    """The 32768-token log-normal workload's shard with fp8 scores: every row against the oracle."""
     w = make_workload("c2")
     t = w.tensors(backward=False)
     sa, bufs, q_deq, k_deq = _fp8_forward(w.cu_seqlens, w.total_tokens, w.sp_degree, w.layout, w.shard, w.heads_q,
                                           w.heads_kv, w.head_dim, w.block_m, w.block_n, t["q"], t["k"], t["v"])
-    n = w.total_tokens // w.sp_degree
-    rows = np.sort(np.random.default_rng(8).choice(n, size=256, replace=False))
-    ref = oracle.shard_forward(q_deq, k_deq, t["v"].float().numpy(), w.cu_seqlens, w.total_tokens, w.sp_degree,
-                               w.layout, w.shard, rows=rows)
-    o, lse = bufs["o"].float().cpu().numpy()[rows], bufs["lse"].cpu().numpy()[:, rows]
+    ref = oracle_by_kv_heads(q_deq, k_deq, t["v"].float().numpy(), None, w.cu_seqlens, w.total_tokens, w.sp_degree,
+                             w.layout, w.shard, list(range(w.heads_kv)))
+    o, lse = bufs["o"].float().cpu().numpy(), bufs["lse"].cpu().numpy()
+    assert not np.isnan(o).any() and not np.isnan(lse).any()
     rep = {"o": max_abs(o, ref["o"]), "lse": max_abs(lse, ref["lse"])}
     _say(rep)
     assert rep["o"] <= O_ATOL and rep["lse"] <= LSE_ATOL, rep
+
+
+@pytest.mark.parametrize("bm", [128, 64])
+def test_fp8_forward_zero_slices(bm):
+    """A K chunk that is all zeros and a query head that is all zeros quantise with scale 0: their
+    scores are all 0, so those rows attend uniformly over their allowed keys (the oracle's
+    result), never NaN from a masked score times a zero scale (direct-to-LDS kernel at 128-row
+    q-tiles, register-staged kernel at 64)."""
+    N, P, layout, hq, hkv, d, bn = 2048, 4, "contiguous", 4, 2, 128, 64
+    cu = np.array([0, 300, 301, 900, 1500, 2048], dtype=np.int32)
+    q, k, v = random_bf16((N, hq, d), 41), random_bf16((N, hkv, d), 42), random_bf16((N, hkv, d), 43)
+    q[:, 1] = 0                                                   # query head 1: amax 0 on every shard
+    k[oracle.shard_positions(N, P, layout, 1)] = 0                # chunk 1: amax 0 for both K/V heads
+    for r in (1, 2, 3):
+        sa, bufs, q_deq, k_deq = _fp8_forward(cu, N, P, layout, r, hq, hkv, d, bm, bn, q, k, v)
+        ref = oracle.shard_forward(q_deq, k_deq, v.float().numpy(), cu, N, P, layout, r)
+        o, lse = bufs["o"].float().cpu().numpy(), bufs["lse"].cpu().numpy()
+        assert not np.isnan(o).any() and not np.isnan(lse).any(), r
+        rep = {"o": max_abs(o, ref["o"]), "lse": max_abs(lse, ref["lse"])}
+        _say("zero slices, shard", r, rep)
+        assert rep["o"] <= O_ATOL and rep["lse"] <= LSE_ATOL, (r, rep)
