@@ -402,6 +402,26 @@ hsap_status hsap_quantize_fp8(const void* x, int32_t groups, int64_t rows, int32
                               uint8_t* codes, float* scale, float* workspace, void* hip_stream);
 
 /*
+ * hsap_quantize_fp8_noalloc -- hsap_quantize_fp8 with no workspace argument,
+ * for callers that cannot allocate device memory around the call (code under
+ * HIP graph capture, serving loops that forbid allocation): the per-range
+ * maxima go to a scratch array of fixed size inside the library (512 KiB of
+ * device memory per GPU the library runs on, held until the process ends).
+ * Allocates nothing.  Same arguments, results and launches as
+ * hsap_quantize_fp8 otherwise.
+ *   groups * heads  at most HSAP_QUANT_NOALLOC_MAX_SLICES, else
+ *                   HSAP_ERR_UNSUPPORTED before anything is launched.
+ * Every call on one GPU shares that GPU's scratch array: calls that overlap
+ * on one GPU (e.g. on two streams without ordering between them) race and may
+ * produce wrong scales and codes; calls ordered on one stream are safe.  The
+ * first call on a device looks up that device's copy of the array (with that
+ * device current) and returns HSAP_ERR_HIP if the runtime cannot.
+ */
+#define HSAP_QUANT_NOALLOC_MAX_SLICES 4096
+hsap_status hsap_quantize_fp8_noalloc(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
+                                      uint8_t* codes, float* scale, void* hip_stream);
+
+/*
  * hsap_partial_attn_fwd_fp8 -- hsap_partial_attn_fwd with the scores taken
  * from e4m3 operands: S = (Q8 K8^T) * q_scale[h] * k_scale[c, g] /
  * sqrt-scale as in desc, i.e. the attention of the dequantised Q and K

@@ -37,7 +37,7 @@ EXPORTED = (
     "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length",
     "hsap_fwd_resident_workgroups", "hsap_load_matrix",
     "hsap_balance", "hsap_emit_forward", "hsap_doc_start",
-    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_quantize_fp8",
+    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_quantize_fp8", "hsap_quantize_fp8_noalloc",
     "hsap_partial_attn_fwd_fp8", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
     "hsap_partial_attn_bwd", "hsap_attn_bwd_bf16", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
     "hsap_executor_plan", "hsap_executor_info", "hsap_executor_forward", "hsap_executor_partial_forward",
@@ -106,6 +106,7 @@ _SIG = {
     "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_attn_fwd_fused": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
     "hsap_quantize_fp8": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _P, _P, _P, _P]),
+    "hsap_quantize_fp8_noalloc": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_partial_attn_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_lse_merge": (ctypes.c_int, [_I32, _P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
@@ -395,6 +396,22 @@ def quantize_fp8(x, codes, scale, workspace, stream=None) -> None:
     _dev(workspace, "float32", "workspace", G * H * QUANT_SPLIT)
     _check(lib().hsap_quantize_fp8(_ptr(x), int(G), int(rows), int(H), int(d), _ptr(codes), _ptr(scale),
                                    _ptr(workspace), _stream(stream)))
+
+
+QUANT_NOALLOC_MAX_SLICES = 4096
+
+
+def quantize_fp8_noalloc(x, codes, scale, stream=None) -> None:
+    """hsap_quantize_fp8_noalloc: hsap_quantize_fp8 with the per-range maxima in the library's own
+    fixed scratch array (no workspace; at most QUANT_NOALLOC_MAX_SLICES groups x heads)."""
+    if x.dim() != 4:
+        raise ValueError("x must be [groups, rows, heads, head_dim]")
+    G, rows, H, d = x.shape
+    _dev(x, "bfloat16", "x")
+    _dev(codes, "uint8", "codes", x.numel())
+    _dev(scale, "float32", "scale", G * H)
+    _check(lib().hsap_quantize_fp8_noalloc(_ptr(x), int(G), int(rows), int(H), int(d), _ptr(codes), _ptr(scale),
+                                           _stream(stream)))
 
 
 def partial_attn_fwd_fp8(desc: AttnDesc, q8, k8, v, q_scale, k_scale, doc_start_dev, tiles_dev, runs_dev, o_part,

@@ -3,6 +3,7 @@
 // per-position document start, the gather into sharded order, and the e4m3
 // quantisation of Q and K for the fp8 score variant.
 #include <algorithm>
+#include <mutex>
 
 #include "hsap_internal.h"
 #include "mfma.h"
@@ -491,23 +492,90 @@ hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, vo
   return check_launch("convert");
 }
 
-hsap_status hsap_quantize_fp8(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
-                              uint8_t* codes, float* scale, float* workspace, void* hip_stream) {
-  clear_error();
+}  // extern "C"
+
+namespace hsap {
+
+// Shape and pointer checks of both quantisation entry points (the workspace is checked apart).
+static hsap_status check_quantize(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
+                                  const uint8_t* codes, const float* scale) {
   if (groups < 1 || rows < 1 || heads < 1 || head_dim < 8 || head_dim % 8)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "bad shape: groups %d, rows %lld, heads %d, head_dim %d (a multiple of 8)", groups,
               (long long)rows, heads, head_dim);
   if ((int64_t)groups * heads * QSPLIT > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many groups x heads");
-  if (!x || !codes || !scale || !workspace) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (!x || !codes || !scale) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if (((uintptr_t)x & 15) || ((uintptr_t)codes & 7))
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "x must be 16-byte and codes 8-byte aligned");
+  return HSAP_OK;
+}
+
+// The two launches of the quantisation: per-range maxima into `workspace` (every entry written),
+// then the slice maxima, scales and codes.
+static hsap_status quantize(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
+                            uint8_t* codes, float* scale, float* workspace, hipStream_t stream) {
   const QuantArgs a{(const __bf16*)x, rows, heads, head_dim, codes, scale, workspace};
   const dim3 grid((unsigned)(groups * heads * QSPLIT));
-  hipLaunchKernelGGL(quantize_amax_kernel, grid, dim3(256), 0, (hipStream_t)hip_stream, a);
+  hipLaunchKernelGGL(quantize_amax_kernel, grid, dim3(256), 0, stream, a);
   hsap_status st = check_launch("quantize_fp8 amax");
   if (st != HSAP_OK) return st;
-  hipLaunchKernelGGL(quantize_convert_kernel, grid, dim3(256), 0, (hipStream_t)hip_stream, a);
+  hipLaunchKernelGGL(quantize_convert_kernel, grid, dim3(256), 0, stream, a);
   return check_launch("quantize_fp8 convert");
+}
+
+// Scratch of hsap_quantize_fp8_noalloc: the per-range maxima of up to
+// HSAP_QUANT_NOALLOC_MAX_SLICES (group, head) slices.  Every device the library runs on holds its
+// own copy (512 KiB) until the process ends.  Host code never uses this name as an address: each
+// device's copy is reached through the address hipGetSymbolAddress returns for it.
+static __device__ __align__(256) float scratch[HSAP_QUANT_NOALLOC_MAX_SLICES * QSPLIT];
+
+constexpr int kMaxScratchDevices = 64;
+static std::mutex scratch_mutex;
+static float* scratch_addr[kMaxScratchDevices];  // per device, resolved on the first call there
+
+// The device address of the current device's `scratch`, looked up once per device with that
+// device current.
+static hsap_status scratch_for_current_device(float** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxScratchDevices) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      HSAP_FAIL(HSAP_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    scratch_addr[dev] = (float*)p;
+  }
+  *out = scratch_addr[dev];
+  return HSAP_OK;
+}
+
+}  // namespace hsap
+
+extern "C" {
+
+hsap_status hsap_quantize_fp8(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
+                              uint8_t* codes, float* scale, float* workspace, void* hip_stream) {
+  clear_error();
+  const hsap_status st = check_quantize(x, groups, rows, heads, head_dim, codes, scale);
+  if (st != HSAP_OK) return st;
+  if (!workspace) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL workspace");
+  return quantize(x, groups, rows, heads, head_dim, codes, scale, workspace, (hipStream_t)hip_stream);
+}
+
+hsap_status hsap_quantize_fp8_noalloc(const void* x, int32_t groups, int64_t rows, int32_t heads, int32_t head_dim,
+                                      uint8_t* codes, float* scale, void* hip_stream) {
+  clear_error();
+  hsap_status st = check_quantize(x, groups, rows, heads, head_dim, codes, scale);
+  if (st != HSAP_OK) return st;
+  if ((int64_t)groups * heads > HSAP_QUANT_NOALLOC_MAX_SLICES)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "groups x heads = %lld above the scratch limit of %d slices",
+              (long long)groups * heads, HSAP_QUANT_NOALLOC_MAX_SLICES);
+  float* work = nullptr;
+  st = scratch_for_current_device(&work);
+  if (st != HSAP_OK) return st;
+  return quantize(x, groups, rows, heads, head_dim, codes, scale, work, (hipStream_t)hip_stream);
 }
 
 hsap_status hsap_doc_start(const int32_t* cu_seqlens, int32_t num_docs, int64_t total_tokens, int32_t* doc_start,
