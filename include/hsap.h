@@ -250,10 +250,22 @@ hsap_status hsap_balance(int32_t sp_degree, const int64_t* cost, int32_t* exec_r
 
 /* Instruction set of the per-rank programs (instruction table of the SAP
  * section): send / receive of a tensor to / from a peer, computing one rank
- * block, and the copy-and-rescale of partial outputs (one merge of all of a
- * shard's parts). */
+ * block, and the local combination of results -- the copy-and-rescale of
+ * partial outputs (one merge of all of a shard's parts) in the forward, the
+ * accumulation of gradient parts (one sum per gradient) in the backward.
+ * Tensors: q (a shard's Q), kv (a chunk's K and V), o (a block's partial O
+ * and LSE), dq (a block's dQ part), dkv (a block's dK and dV parts), do (a
+ * shard's dO with its final LSE and delta = rowsum(dO o O)). */
 typedef enum { HSAP_OP_SEND = 0, HSAP_OP_RECV = 1, HSAP_OP_COMPUTE = 2, HSAP_OP_MERGE = 3 } hsap_op_kind;
-typedef enum { HSAP_T_NONE = -1, HSAP_T_Q = 0, HSAP_T_KV = 1, HSAP_T_O = 2 } hsap_tensor_kind;
+typedef enum {
+  HSAP_T_NONE = -1,
+  HSAP_T_Q = 0,
+  HSAP_T_KV = 1,
+  HSAP_T_O = 2,
+  HSAP_T_DQ = 3,
+  HSAP_T_DKV = 4,
+  HSAP_T_DO = 5
+} hsap_tensor_kind;
 
 /* One instruction, 32-byte POD.  Buffers of a rank: its own Q shard and K/V
  * chunk; two receive slots each for Q and K/V; two result slots for the
@@ -303,6 +315,37 @@ typedef struct {
  */
 hsap_status hsap_emit_forward(int32_t sp_degree, const int64_t* block_tiles, const int32_t* exec_rank, hsap_op* ops,
                               int64_t capacity, int64_t* rank_offsets, int32_t* num_stages);
+
+/*
+ * hsap_emit_backward -- the per-rank instruction lists of the backward pass
+ * (host), the jitted code generation of the SAP section for the gradient
+ * messages of its instruction table (dq, dkv, do): every non-empty block is
+ * computed on the rank that computed its forward (exec_rank), at the same
+ * stage as in hsap_emit_forward.
+ *   Ring block (r, c), c != r, on rank r: K/V of chunk c arrive from rank c
+ *     one stage ahead (receive slot stage % 2); the block's dQ part stays on
+ *     r; its dK/dV part goes to result slot stage % 2 and is sent to rank c
+ *     one stage later (SEND/RECV of tensor DKV, shard r, chunk c).
+ *   Transferred block (r, c), r != c, on rank c: Q and dO (with the final
+ *     LSE and delta of shard r) arrive from rank r one stage ahead (two
+ *     receives into slot stage % 2); the dK/dV part stays on c; the dQ part
+ *     goes to result slot stage % 2 and is sent to rank r one stage later
+ *     (tensor DQ).
+ *   Diagonal block (e, e): local data only; both parts stay on e.
+ * COMPUTE: in_slot = the receive slot of the block's inputs and out_slot =
+ * the result slot of the part that leaves the rank (both -1 for a diagonal
+ * block).  Parts that stay, and every received part, are indexed as
+ * RECV.out_slot is: dQ part part(r, c) = rank of chunk c among the chunks
+ * with a non-empty block of shard r; dK/dV part kpart(c, r) = rank of shard r
+ * among the shards with a non-empty block in chunk c.  In the last stage a
+ * rank with dQ parts lists MERGE (tensor DQ, shard e, out_slot = the number
+ * of parts): the sum of its dQ parts in part order; and one with dK/dV parts
+ * MERGE (tensor DKV, chunk e, out_slot = the number of parts) likewise.  The
+ * order inside a stage and the matching of sends and receives are those of
+ * hsap_emit_forward; arguments, output layout and errors as there.
+ */
+hsap_status hsap_emit_backward(int32_t sp_degree, const int64_t* block_tiles, const int32_t* exec_rank, hsap_op* ops,
+                               int64_t capacity, int64_t* rank_offsets, int32_t* num_stages);
 
 /*
  * hsap_doc_start -- device int32 [total_tokens]: start(t) for every position
@@ -495,6 +538,10 @@ hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, 
  *   lse        device fp32 [Hq, n]: the merged forward LSE.
  *   delta      device fp32 [Hq, n] from hsap_attn_bwd_preprocess.
  *   tiles_k, runs_k, num_runs_k  device lists from hsap_plan_runs(MAJOR_K).
+ *              k, v, dk_acc and dv_acc are read and written only in the
+ *              rows of the chunks that the passed runs' tiles name, so a
+ *              caller holding one chunk c alone may pass the addresses that
+ *              chunk 0 would have (as for hsap_partial_attn_fwd).
  *   tiles_q, runs_q, num_runs_q  device q-tile runs in which no q_tile
  *              appears twice: hsap_plan_runs(MAJOR_Q_ALL) (every chunk in
  *              one pass), or the runs of one chunk from
@@ -539,6 +586,23 @@ hsap_status hsap_attn_bwd_bf16(const hsap_attn_desc* desc, const void* q, const 
                                const hsap_tile* tiles_k, const hsap_run* runs_k, int64_t num_runs_k,
                                const hsap_tile* tiles_q, const hsap_run* runs_q, int64_t num_runs_q, void* dq,
                                void* dk, void* dv, void* hip_stream);
+
+/*
+ * hsap_sum_parts -- out[i] = parts[0][i] + parts[1][i] + ... (fp32, added in
+ * part order), stored as fp32 or as bf16 (round to nearest even).  The
+ * accumulation of gradient parts in the backward's per-rank programs: a rank
+ * sums the dQ parts of its shard and the dK/dV parts of its chunk that it
+ * computed or received (the dq / dkv messages of the instruction table of
+ * the SAP section; see hsap_emit_backward).
+ *   num_parts  1 .. HSAP_MAX_MERGE_PARTS.
+ *   parts      HOST array of num_parts device pointers, each fp32 [count],
+ *              16-byte aligned.
+ *   out        device fp32 [count] (16-byte aligned) or, with out_bf16 != 0,
+ *              bf16 [count] (8-byte aligned); may not overlap a part.
+ * One launch on `stream`; nothing launched for count = 0.
+ */
+hsap_status hsap_sum_parts(int32_t num_parts, const float* const* parts, int64_t count, void* out, int32_t out_bf16,
+                           void* hip_stream);
 
 /*
  * hsap_convert_f32_bf16 -- dst[i] = bf16(src[i]), round to nearest even

@@ -37,9 +37,10 @@ What it computes, with the passages it follows (HSAP paper, arxiv 2606.30460):
 * ``fp8`` -- the e4m3 quantisation of Q and K for the fp8 score variant (an
   extension beyond the paper's bf16 attention; its attention is the oracle's
   attention on the dequantised values).
-* ``schedule`` -- the per-rank instruction lists of the forward pass (the
-  jitted code generation of the SAP section, with the paper's instruction
-  set), arranged in stages with matched sends and receives.
+* ``schedule`` -- the per-rank instruction lists of the forward and backward
+  passes (the jitted code generation of the SAP section, with the paper's
+  instruction set: q, kv, o, dq, dkv, do messages), arranged in stages with
+  matched sends and receives.
 
 Parity status: every function above is pinned by ``tests/test_oracle_pins.py``
 against brute force, closed forms, library routines or invariants; none is
@@ -62,6 +63,6 @@ from .plan import (  # noqa: F401
     useful_pairs_all_shards,
 )
 from .balance import load_matrix, q_transfer_balance  # noqa: F401
-from .schedule import forward_program  # noqa: F401
+from .schedule import backward_program, forward_program  # noqa: F401
 from .batch import batch_plan_shard, batch_shard_backward, batch_shard_forward, split_batch  # noqa: F401
 from .fp8 import decode_fp8, dequantize_fp8, quantize_fp8  # noqa: F401

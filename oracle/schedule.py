@@ -1,4 +1,4 @@
-"""Per-rank instruction lists of the forward pass (the jitted code of the SAP section).
+"""Per-rank instruction lists of the forward and backward passes (the jitted code of the SAP section).
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
@@ -34,6 +34,32 @@ below):
   (peer, kind with send before receive, tensor, shard, chunk), then its
   computation, then the merge.
 
+The backward program (``backward_program``) moves the gradient messages of
+the same instruction table (dq, dkv, do).  Reading:
+
+* Every block is differentiated on the rank that computed its forward, at the
+  same stage as there (the forward's block order and first stages).
+* A ring block (r, c), c != r, on rank r: chunk c's K/V come from rank c one
+  stage ahead into receive slot t % 2 (as in the forward).  Its dQ part stays
+  on r; its dK/dV part is written to result slot t % 2 and sent to rank c at
+  stage t+1 as tensor dkv.
+* A transferred block (r, c) on rank c: shard r's Q and its dO (with the
+  shard's final LSE and delta) come from rank r at stage t-1 into receive slot
+  t % 2, as two messages (q, then do).  Its dK/dV part stays on c; its dQ
+  part goes to result slot t % 2 and is sent to rank r at stage t+1 as tensor
+  dq.
+* A diagonal block keeps both parts.
+* COMPUTE carries in_slot = receive slot and out_slot = result slot (both -1
+  for a diagonal block).  Parts that stay and parts received are indexed by
+  kind: dQ parts of shard r by chunk (index of c among the chunks with a
+  block of shard r), dK/dV parts of chunk c by shard (index of r among the
+  shards with a block in chunk c); a receive names that index in out_slot.
+* In the last stage each rank sums its dQ parts in index order (MERGE of
+  tensor dq, shard e, out_slot = count) and then its dK/dV parts (MERGE of
+  tensor dkv, chunk e, out_slot = count) -- the accumulation the paper does
+  with local copies into its gradient buffers.
+* Order within a stage: as in the forward.
+
 Op tuples: (op, tensor, peer, stage, shard, chunk, in_slot, out_slot), the
 fields of the library's op record.  Pins: ``tests/test_schedule.py`` checks
 matched sends and receives, that every block is computed once on its rank
@@ -48,7 +74,7 @@ from typing import List, Tuple
 import numpy as np
 
 OP_SEND, OP_RECV, OP_COMPUTE, OP_MERGE = 0, 1, 2, 3
-T_NONE, T_Q, T_KV, T_O = -1, 0, 1, 2
+T_NONE, T_Q, T_KV, T_O, T_DQ, T_DKV, T_DO = -1, 0, 1, 2, 3, 4, 5
 
 Op = Tuple[int, int, int, int, int, int, int, int]
 
@@ -100,3 +126,57 @@ def forward_program(block_tiles, exec_rank) -> Tuple[List[List[Op]], int]:
                 ops.append((OP_MERGE, T_NONE, -1, S, e, -1, -1, len(parts[e])))
         program.append(ops)
     return program, S + 1
+
+
+def backward_program(block_tiles, exec_rank) -> Tuple[List[List[Op]], int]:
+    """(ops per rank, number of stages) of the backward pass for block sizes [P, P] and ranks [P, P]."""
+    tiles = np.asarray(block_tiles, dtype=np.int64)
+    ex = np.asarray(exec_rank, dtype=np.int64)
+    P = tiles.shape[0]
+    # the forward's stage of every block
+    on_rank = [[] for _ in range(P)]
+    for r in range(P):
+        for c in range(P):
+            if tiles[r, c] > 0:
+                on_rank[int(ex[r, c])].append((r, c))
+    for e in range(P):
+        on_rank[e].sort(key=lambda b: (b[0] != b[1], (b[0] - b[1]) % P, b[0], b[1]))
+    start = [0 if on_rank[e] and on_rank[e][0][0] == on_rank[e][0][1] else 1 for e in range(P)]
+    last = max(start[e] + len(on_rank[e]) for e in range(P))
+    dq_parts = [[c for c in range(P) if tiles[r, c] > 0] for r in range(P)]      # of shard r, by chunk
+    dkv_parts = [[r for r in range(P) if tiles[r, c] > 0] for c in range(P)]     # of chunk c, by shard
+
+    transfers = [[[] for _ in range(last + 1)] for _ in range(P)]
+    work = [[[] for _ in range(last + 1)] for _ in range(P)]
+    for e in range(P):
+        for k, (r, c) in enumerate(on_rank[e]):
+            t = start[e] + k
+            slot = t % 2
+            if r == c:
+                work[e][t].append((OP_COMPUTE, T_NONE, -1, t, r, c, -1, -1))
+                continue
+            if r == e:       # ring block: K/V in; dK/dV out to the chunk's owner
+                transfers[c][t - 1].append((OP_SEND, T_KV, e, t - 1, -1, c, -1, -1))
+                transfers[e][t - 1].append((OP_RECV, T_KV, c, t - 1, -1, c, -1, slot))
+                transfers[e][t + 1].append((OP_SEND, T_DKV, c, t + 1, r, c, slot, -1))
+                transfers[c][t + 1].append((OP_RECV, T_DKV, e, t + 1, r, c, -1, dkv_parts[c].index(r)))
+            else:            # transferred block: Q and dO in; dQ out to the shard's owner
+                for tensor in (T_Q, T_DO):
+                    transfers[r][t - 1].append((OP_SEND, tensor, e, t - 1, r, -1, -1, -1))
+                    transfers[e][t - 1].append((OP_RECV, tensor, r, t - 1, r, -1, -1, slot))
+                transfers[e][t + 1].append((OP_SEND, T_DQ, r, t + 1, r, c, slot, -1))
+                transfers[r][t + 1].append((OP_RECV, T_DQ, e, t + 1, r, c, -1, dq_parts[r].index(c)))
+            work[e][t].append((OP_COMPUTE, T_NONE, -1, t, r, c, slot, slot))
+    program = []
+    for e in range(P):
+        ops = []
+        for t in range(last + 1):
+            ops += sorted(transfers[e][t], key=lambda o: (o[2], o[0], o[1], o[4], o[5]))
+            ops += work[e][t]
+            if t == last:
+                if dq_parts[e]:
+                    ops.append((OP_MERGE, T_DQ, -1, last, e, -1, -1, len(dq_parts[e])))
+                if dkv_parts[e]:
+                    ops.append((OP_MERGE, T_DKV, -1, last, -1, e, -1, len(dkv_parts[e])))
+        program.append(ops)
+    return program, last + 1

@@ -36,10 +36,10 @@ MAX_MERGE_PARTS = 64
 EXPORTED = (
     "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length",
     "hsap_fwd_resident_workgroups", "hsap_load_matrix",
-    "hsap_balance", "hsap_emit_forward", "hsap_doc_start",
+    "hsap_balance", "hsap_emit_forward", "hsap_emit_backward", "hsap_doc_start",
     "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_quantize_fp8", "hsap_quantize_fp8_noalloc",
     "hsap_partial_attn_fwd_fp8", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
-    "hsap_partial_attn_bwd", "hsap_attn_bwd_bf16", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
+    "hsap_partial_attn_bwd", "hsap_attn_bwd_bf16", "hsap_sum_parts", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
     "hsap_executor_plan", "hsap_executor_info", "hsap_executor_forward", "hsap_executor_partial_forward",
     "hsap_executor_merge", "hsap_executor_backward",
 )
@@ -101,6 +101,7 @@ _SIG = {
     "hsap_load_matrix": (ctypes.c_int, [_P, _I32, _P, _P, _P]),
     "hsap_balance": (ctypes.c_int, [_I32, _P, _P, _P]),
     "hsap_emit_forward": (ctypes.c_int, [_I32, _P, _P, _P, _I64, _P, _P]),
+    "hsap_emit_backward": (ctypes.c_int, [_I32, _P, _P, _P, _I64, _P, _P]),
     "hsap_doc_start": (ctypes.c_int, [_P, _I32, _I64, _P, _P]),
     "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
     "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
@@ -114,6 +115,7 @@ _SIG = {
                                              _P]),
     "hsap_attn_bwd_bf16": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P, _P]),
     "hsap_convert_f32_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
+    "hsap_sum_parts": (ctypes.c_int, [_I32, _P, _I64, _P, _I32, _P]),
     "hsap_executor_create": (ctypes.c_int, [_P, _I32, _I32, _P]),
     "hsap_executor_destroy": (None, [_P]),
     "hsap_executor_plan": (ctypes.c_int, [_P, _P, _I32, _P]),
@@ -297,24 +299,32 @@ def balance(cost):
 
 
 OP_SEND, OP_RECV, OP_COMPUTE, OP_MERGE = 0, 1, 2, 3
-T_NONE, T_Q, T_KV, T_O = -1, 0, 1, 2
+T_NONE, T_Q, T_KV, T_O, T_DQ, T_DKV, T_DO = -1, 0, 1, 2, 3, 4, 5
 
 
-def emit_forward(block_tiles, exec_rank):
-    """hsap_emit_forward with the two-call pattern: (list of int32 [ops_e, 8] arrays per rank --
-    fields op, tensor, peer, stage, shard, chunk, in_slot, out_slot -- and the number of stages)."""
+def _emit(fn, block_tiles, exec_rank):
     tiles = np.ascontiguousarray(block_tiles, dtype=np.int64)
     ex = np.ascontiguousarray(exec_rank, dtype=np.int32)
     P = tiles.shape[0]
     offs = np.zeros(P + 1, dtype=np.int64)
     stages = ctypes.c_int32(0)
-    st = lib().hsap_emit_forward(int(P), _ptr(tiles), _ptr(ex), None, 0, _ptr(offs), ctypes.byref(stages))
+    st = fn(int(P), _ptr(tiles), _ptr(ex), None, 0, _ptr(offs), ctypes.byref(stages))
     if st != HSAP_ERR_CAPACITY:
         _check(st)
     ops = np.zeros((max(int(offs[P]), 1), 8), dtype=np.int32)
-    _check(lib().hsap_emit_forward(int(P), _ptr(tiles), _ptr(ex), _ptr(ops), int(offs[P]), _ptr(offs),
-                                   ctypes.byref(stages)))
+    _check(fn(int(P), _ptr(tiles), _ptr(ex), _ptr(ops), int(offs[P]), _ptr(offs), ctypes.byref(stages)))
     return [ops[offs[e]:offs[e + 1]] for e in range(P)], int(stages.value)
+
+
+def emit_forward(block_tiles, exec_rank):
+    """hsap_emit_forward with the two-call pattern: (list of int32 [ops_e, 8] arrays per rank --
+    fields op, tensor, peer, stage, shard, chunk, in_slot, out_slot -- and the number of stages)."""
+    return _emit(lib().hsap_emit_forward, block_tiles, exec_rank)
+
+
+def emit_backward(block_tiles, exec_rank):
+    """hsap_emit_backward with the two-call pattern, as emit_forward."""
+    return _emit(lib().hsap_emit_backward, block_tiles, exec_rank)
 
 
 def plan_runs_into(shard: ShardDesc, tiles: np.ndarray, num_tiles: int, major: int, max_run_tiles: int,
@@ -483,14 +493,22 @@ def attn_bwd_preprocess(o, d_o, n: int, heads_q: int, head_dim: int, delta, stre
 
 
 def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_k_dev, runs_k_dev, tiles_q_dev,
-                     runs_q_dev, dq_acc, dk_acc, dv_acc, stream=None) -> None:
-    """hsap_partial_attn_bwd.  Either run list may be None to skip its kernel."""
+                     runs_q_dev, dq_acc, dk_acc, dv_acc, stream=None, kv_chunk: Optional[int] = None) -> None:
+    """hsap_partial_attn_bwd.  Either run list may be None to skip its kernel.  With ``kv_chunk`` = c,
+    k, v, dk_acc and dv_acc are [n, Hkv, d] tensors of chunk c alone (every run passed must be of
+    chunk c), passed as the addresses chunk 0 would have."""
     s = desc.shard
     n = s.rows
     hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
+    kv_rows = P if kv_chunk is None else 1
+    kv_shift = 0
+    if kv_chunk is not None:
+        if not 0 <= int(kv_chunk) < P:
+            raise ValueError("kv_chunk %d outside [0, %d)" % (kv_chunk, P))
+        kv_shift = int(kv_chunk) * n * hkv * d
     _dev(q, "bfloat16", "q", n * hq * d)
-    _dev(k, "bfloat16", "k", P * n * hkv * d)
-    _dev(v, "bfloat16", "v", P * n * hkv * d)
+    _dev(k, "bfloat16", "k", kv_rows * n * hkv * d)
+    _dev(v, "bfloat16", "v", kv_rows * n * hkv * d)
     _dev(d_o, "bfloat16", "d_o", n * hq * d)
     _dev(lse, "float32", "lse", hq * n)
     _dev(delta, "float32", "delta", hq * n)
@@ -499,14 +517,27 @@ def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, ti
         if t is not None:
             _dev(t, "int32", name)
     _dev(dq_acc, "float32", "dq_acc", n * hq * d)
-    _dev(dk_acc, "float32", "dk_acc", P * n * hkv * d)
-    _dev(dv_acc, "float32", "dv_acc", P * n * hkv * d)
+    _dev(dk_acc, "float32", "dk_acc", kv_rows * n * hkv * d)
+    _dev(dv_acc, "float32", "dv_acc", kv_rows * n * hkv * d)
     nk = runs_k_dev.numel() // 4 if runs_k_dev is not None else 0
     nq = runs_q_dev.numel() // 4 if runs_q_dev is not None else 0
-    _check(lib().hsap_partial_attn_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(d_o), _ptr(lse),
-                                       _ptr(delta), _ptr(doc_start_dev), _ptr(tiles_k_dev), _ptr(runs_k_dev), nk,
-                                       _ptr(tiles_q_dev), _ptr(runs_q_dev), nq, _ptr(dq_acc), _ptr(dk_acc),
-                                       _ptr(dv_acc), _stream(stream)))
+    _check(lib().hsap_partial_attn_bwd(ctypes.byref(desc), _ptr(q), _ptr(k) - 2 * kv_shift, _ptr(v) - 2 * kv_shift,
+                                       _ptr(d_o), _ptr(lse), _ptr(delta), _ptr(doc_start_dev), _ptr(tiles_k_dev),
+                                       _ptr(runs_k_dev), nk, _ptr(tiles_q_dev), _ptr(runs_q_dev), nq, _ptr(dq_acc),
+                                       _ptr(dk_acc) - 4 * kv_shift, _ptr(dv_acc) - 4 * kv_shift, _stream(stream)))
+
+
+def sum_parts(parts, out, stream=None) -> None:
+    """hsap_sum_parts: out = parts[0] + parts[1] + ... (fp32, in order), out fp32 or bf16 of the parts' size."""
+    count = parts[0].numel()
+    for i, p in enumerate(parts):
+        _dev(p, "float32", "parts[%d]" % i, count)
+    if str(out.dtype) not in ("torch.float32", "torch.bfloat16"):
+        raise TypeError("out must be float32 or bfloat16")
+    _dev(out, str(out.dtype)[6:], "out", count)
+    arr = (ctypes.c_void_p * len(parts))(*[_ptr(p) for p in parts])
+    _check(lib().hsap_sum_parts(len(parts), arr, count, _ptr(out), int(str(out.dtype) == "torch.bfloat16"),
+                                _stream(stream)))
 
 
 def attn_bwd_bf16(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_k_dev, runs_k_dev, tiles_all_dev,

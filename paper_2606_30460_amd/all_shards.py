@@ -57,7 +57,7 @@ class AllShards:
         self.planned = False
 
     # ------------------------------------------------------------------ plan
-    def plan(self) -> None:
+    def plan(self, backward: bool = False) -> None:
         P, dev = self.P, self.device
         base = L.shard_desc(self.N, P, self.layout, 0, self.bm, self.bn)
         self.block_tiles, self.block_pairs = L.load_matrix(self.cu_host, base)
@@ -93,7 +93,30 @@ class AllShards:
                 sel = runs[self.exec_rank[r, chunk_of_run] == e]
                 if len(sel):
                     self.runs[e][r] = torch.from_numpy(np.ascontiguousarray(sel).reshape(-1)).to(dev)
+        self.backward_planned = False
+        if backward:
+            self._plan_backward()
         self.planned = True
+
+    def _plan_backward(self) -> None:
+        """Per block (r, c): shard r's unsplit q-major runs of chunk c (dQ kernel) and its k-major runs
+        of chunk c (dK/dV kernel); the part indices of every shard's dQ and every chunk's dK/dV."""
+        P, dev = self.P, self.device
+        self.dq_parts = [[c for c in range(P) if self.block_tiles[r, c] > 0] for r in range(P)]
+        self.dkv_parts = [[r for r in range(P) if self.block_tiles[r, c] > 0] for c in range(P)]
+        self.bwd_tiles_q, self.bwd_tiles_k = [], []
+        self.bwd_runs: Dict[tuple, tuple] = {}
+        for r in range(P):
+            shard = self.descs[r].shard
+            tiles = L.plan(self.cu_host, shard)["tiles"]
+            sq, rq, _ = L.plan_runs(shard, tiles, L.MAJOR_Q, 0)     # unsplit: slot = chunk
+            sk, rk, _ = L.plan_runs(shard, tiles, L.MAJOR_K, 0)     # slot = chunk
+            self.bwd_tiles_q.append(torch.from_numpy(np.ascontiguousarray(sq).reshape(-1)).to(dev))
+            self.bwd_tiles_k.append(torch.from_numpy(np.ascontiguousarray(sk).reshape(-1)).to(dev))
+            for c in self.dq_parts[r]:
+                self.bwd_runs[(r, c)] = tuple(torch.from_numpy(np.ascontiguousarray(x[x[:, 0] == c]).reshape(-1)).to(dev)
+                                              for x in (rq, rk))
+        self.backward_planned = True
 
     # ------------------------------------------------------------ schedule
     def schedule(self) -> Dict:
@@ -164,3 +187,65 @@ class AllShards:
         torch.cuda.synchronize()
         return {"blocks_ms": [ev[e][0].elapsed_time(ev[e][1]) for e in range(P)],
                 "merge_ms": [ev[r][2].elapsed_time(ev[r][3]) for r in range(P)]}
+
+    # ------------------------------------------------------------ backward
+    def alloc_backward(self) -> Dict[str, object]:
+        dev, n, f32 = self.device, self.n, torch.float32
+        return {
+            "delta": torch.empty(self.P, self.hq, n, dtype=f32, device=dev),
+            "dq_part": [torch.empty(max(len(x), 1), n, self.hq, self.d, dtype=f32, device=dev) for x in self.dq_parts],
+            "dk_part": [torch.empty(max(len(x), 1), n, self.hkv, self.d, dtype=f32, device=dev) for x in self.dkv_parts],
+            "dv_part": [torch.empty(max(len(x), 1), n, self.hkv, self.d, dtype=f32, device=dev) for x in self.dkv_parts],
+            "dq": torch.empty(self.P, n, self.hq, self.d, dtype=torch.bfloat16, device=dev),
+            "dk": torch.empty(self.P, n, self.hkv, self.d, dtype=torch.bfloat16, device=dev),
+            "dv": torch.empty(self.P, n, self.hkv, self.d, dtype=torch.bfloat16, device=dev),
+        }
+
+    def backward(self, q, k, v, d_o, o, lse, bufs: Dict[str, object],
+                 timed: bool = False) -> Optional[Dict[str, List[float]]]:
+        """Gradients of every shard's attention: q, d_o, o [P, n, Hq, d], lse [P, Hq, n] (the forward's
+        outputs), k / v [P, n, Hkv, d] -> bufs["dq"] [P, n, Hq, d], bufs["dk"] / bufs["dv"] [P, n, Hkv, d]
+        (bf16; chunks without any block are left as they are).  Rank e differentiates the blocks
+        its schedule gives it, each into its own zeroed fp32 parts (hsap_partial_attn_bwd); then
+        every shard's dQ parts and every chunk's dK/dV parts are summed in part order
+        (hsap_sum_parts), so any schedule gives the same bits.  With ``timed`` the milliseconds of
+        each rank's blocks and of its sums are returned."""
+        if not (self.planned and self.backward_planned):
+            raise RuntimeError("call plan(backward=True) first")
+        P = self.P
+        for r in range(P):
+            L.attn_bwd_preprocess(o[r], d_o[r], self.n, self.hq, self.d, bufs["delta"][r])
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(P)] if timed else None
+        for e in range(P):
+            if timed:
+                ev[e][0].record()
+            for r in range(P):
+                for c in self.dq_parts[r]:
+                    if self.exec_rank[r, c] != e:
+                        continue
+                    dq_t = bufs["dq_part"][r][self.dq_parts[r].index(c)]
+                    i = self.dkv_parts[c].index(r)
+                    dk_t, dv_t = bufs["dk_part"][c][i], bufs["dv_part"][c][i]
+                    for t_ in (dq_t, dk_t, dv_t):
+                        t_.zero_()
+                    runs_q, runs_k = self.bwd_runs[(r, c)]
+                    L.partial_attn_bwd(self.descs[r], q[r], k[c], v[c], d_o[r], lse[r], bufs["delta"][r],
+                                       self.doc_start, self.bwd_tiles_k[r], runs_k, self.bwd_tiles_q[r], runs_q,
+                                       dq_t, dk_t, dv_t, kv_chunk=c)
+            if timed:
+                ev[e][1].record()
+        for x in range(P):
+            if timed:
+                ev[x][2].record()
+            if self.dq_parts[x]:
+                L.sum_parts([bufs["dq_part"][x][i] for i in range(len(self.dq_parts[x]))], bufs["dq"][x])
+            if self.dkv_parts[x]:
+                L.sum_parts([bufs["dk_part"][x][i] for i in range(len(self.dkv_parts[x]))], bufs["dk"][x])
+                L.sum_parts([bufs["dv_part"][x][i] for i in range(len(self.dkv_parts[x]))], bufs["dv"][x])
+            if timed:
+                ev[x][3].record()
+        if not timed:
+            return None
+        torch.cuda.synchronize()
+        return {"blocks_ms": [ev[e][0].elapsed_time(ev[e][1]) for e in range(P)],
+                "sum_ms": [ev[x][2].elapsed_time(ev[x][3]) for x in range(P)]}
