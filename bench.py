@@ -412,7 +412,7 @@ def fp8_analysis(name: str, reps: int = 50) -> dict:
     quant_ms = timed(lambda: (L.quantize_fp8(q.unsqueeze(0), q8.unsqueeze(0), qs, wq), L.quantize_fp8(k, k8, ks, wk)))
     fp8_ms = timed(lambda: L.partial_attn_fwd_fp8(sa.desc, q8, k8, v, qs, ks, sa.doc_start, sa.tiles_q, sa.runs_q,
                                                   bufs["o_part"], bufs["lse_part"]))
-    bf16_ms = timed(lambda: L.partial_attn_fwd(sa.desc, q, k, v, sa.doc_start, sa.tiles_q, sa.runs_q, bufs["o_part"],
+    bf16_ms = timed(lambda: L.partial_attn_fwd_runs(sa.desc, q, k, v, sa.doc_start, sa.tiles_q, sa.runs_q, bufs["o_part"],
                                                bufs["lse_part"]))
     flops = 4.0 * w.head_dim * w.heads_q * sa.total_useful_pairs
     log("[bench] fp8 scores %s: partial forward %.3f ms (%.1f TFLOP/s) vs bf16 %.3f ms; quantisation %.3f ms" % (

@@ -113,6 +113,9 @@ typedef struct {
 
 typedef struct {
   hsap_shard_desc shard;
+  int32_t chunk_id;      /* K/V chunk of hsap_partial_attn_fwd / _bwd; the
+                            run-based entry points read the chunk of each tile
+                            and ignore this field                            */
   int32_t heads_q;       /* Hq                                              */
   int32_t heads_kv;      /* Hkv, divides Hq                                 */
   int32_t head_dim;      /* d: 64 or 128                                    */
@@ -200,7 +203,7 @@ int32_t hsap_split_length(const hsap_shard_desc* shard, int64_t num_tiles, int32
 /*
  * hsap_fwd_resident_workgroups -- workgroups of the bf16 partial forward that
  * fit on the current device at once for the shapes in `desc`: the HIP
- * runtime's occupancy of the kernel hsap_partial_attn_fwd dispatches for
+ * runtime's occupancy of the kernel hsap_partial_attn_fwd_runs dispatches for
  * (head_dim, BM, BN) (its registers, LDS and workgroup size), times the
  * device's compute units -- the resident_workgroups of hsap_split_length.
  * Not in the paper (scheduling of this library's kernels).
@@ -368,7 +371,74 @@ hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, voi
                               int64_t row_bytes, void* hip_stream);
 
 /*
- * hsap_partial_attn_fwd -- "computing" for the forward: for every run (slot,
+ * hsap_partial_attn_fwd -- "computing" of the SAP instruction table for the
+ * forward: shard r's queries against K/V chunk c = desc->chunk_id, one
+ * partial output and log-sum-exp (the attention equation of the inter-group
+ * SP section restricted to the packing mask and to chunk c's keys), for the
+ * non-empty tiles that hsap_plan listed for that chunk.
+ *
+ *   desc       shard (N, P, layout, r, BM, BN), chunk_id c in [0, P), heads,
+ *              head_dim, softmax scale.  Shapes as hsap_partial_attn_fwd_runs.
+ *   q          device bf16 [n, Hq, d]: shard r's queries, local row order.
+ *   k, v       device bf16 [P, n, Hkv, d] sharded order; only chunk c's rows
+ *              are read (a caller holding chunk c alone may pass the address
+ *              chunk 0 would have, k_c - c * n * Hkv * d).
+ *   doc_start  device int32 [N] from hsap_doc_start.
+ *   tiles      device hsap_tile [num_tiles]: chunk c's tiles in hsap_plan's
+ *              order (the ring step's range tiles[step_offsets[s] ..
+ *              step_offsets[s+1]-1] with c = (r - s) mod P): q_tile ascending,
+ *              then k_tile, every tile's chunk equal to c.  The kernels trust
+ *              the list (they index with its q_tile / k_tile values) and find
+ *              each q-tile's tiles in it by search; NULL when num_tiles = 0.
+ *   num_tiles  0 .. 2^31 - 1.
+ *   o_part     device fp32 [n, Hq, d], 16-byte aligned: rows with an allowed
+ *              key in chunk c receive the normalised partial output; rows
+ *              without one are undefined and must not be read.
+ *   lse_part   device fp32 [Hq, n]: every row written; -inf where the row has
+ *              no allowed key in chunk c (always for q-tiles without a tile).
+ * One launch of (n / BM) x Hq workgroups on `stream`; HSAP_ERR_INVALID_ARG
+ * for a bad chunk_id, count or pointer, HSAP_ERR_UNSUPPORTED for shapes
+ * without a kernel, both before anything is launched.  Same bits as
+ * hsap_partial_attn_fwd_runs over the unsplit q-major runs of chunk c.
+ */
+hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                  const int32_t* doc_start, const hsap_tile* tiles, int64_t num_tiles,
+                                  float* o_part, float* lse_part, void* hip_stream);
+
+/*
+ * hsap_partial_attn_bwd -- "computing" for the backward, on the same tile
+ * list: the gradients of hsap_partial_attn_fwd's partial with P = exp(s - LSE)
+ * recomputed from the shard's final LSE (the backward of the attention
+ * equation; its dq and dkv results are the dq / dkv messages of the SAP
+ * instruction table):
+ *   dV_c += P^T dO,  dS = P o (dO V_c^T - delta),
+ *   dQ   += scale dS K_c,  dK_c += scale dS^T Q,
+ * dK/dV summed over the query heads of each K/V head.
+ *
+ *   desc, q, k, v, doc_start, tiles, num_tiles  as for hsap_partial_attn_fwd
+ *              (chunk c = desc->chunk_id).  Shapes as
+ *              hsap_partial_attn_bwd_runs; additionally n / BM <= 2048
+ *              (the dK/dV kernel gathers each k-tile's q-tiles in LDS).
+ *   d_o        device bf16 [n, Hq, d] (shard r, local rows).
+ *   lse        device fp32 [Hq, n]: the shard's final (merged) forward LSE.
+ *   delta      device fp32 [Hq, n] from hsap_attn_bwd_preprocess.
+ *   dq_acc     device fp32 [n, Hq, d] (+=): every q-tile with a tile.
+ *   dk_acc, dv_acc  device fp32 [P, n, Hkv, d] sharded order (+=): the rows
+ *              of chunk c's k-tiles that have a tile (a caller holding chunk c
+ *              alone may pass the address chunk 0 would have).
+ * Two launches on `stream` (dQ: (n / BM) x Hq workgroups; dK/dV: (n / BN) x
+ * Hkv workgroups, each scanning the list for its k-tile).  The caller zeroes
+ * the accumulators once; one call per chunk of a ring accumulates dQ over the
+ * ring.  Errors as for hsap_partial_attn_fwd.  For the gradients of every
+ * chunk at once, the run-based entry points below avoid the per-k-tile scans.
+ */
+hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                  const void* d_o, const float* lse, const float* delta, const int32_t* doc_start,
+                                  const hsap_tile* tiles, int64_t num_tiles, float* dq_acc, float* dk_acc,
+                                  float* dv_acc, void* hip_stream);
+
+/*
+ * hsap_partial_attn_fwd_runs -- "computing" for the forward: for every run (slot,
  * q_tile t), the queries of q-tile t of shard r against the run's k-tiles of
  * one chunk, producing that slot's partial output and log-sum-exp (attention
  * equation of the inter-group SP section restricted to the packing mask).
@@ -399,7 +469,7 @@ hsap_status hsap_shard_gather(const hsap_shard_desc* shard, const void* src, voi
  *   run are untouched.  tiles and runs must be the lists hsap_plan_runs made
  *   for this shard: the kernel trusts their tile indices.
  */
-hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, const void* k,
+hsap_status hsap_partial_attn_fwd_runs(const hsap_attn_desc* desc, const void* q, const void* k,
                                   const void* v, const int32_t* doc_start, const hsap_tile* tiles,
                                   const hsap_run* runs, int64_t num_runs, float* o_part,
                                   float* lse_part, int32_t num_slots, void* hip_stream);
@@ -412,7 +482,7 @@ hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, con
  * fusion of the copy and rescale operations into the attention computation
  * that the paper's Limitations section proposes as future work.
  *
- *   desc, q, k, v, doc_start  as for hsap_partial_attn_fwd (same supported
+ *   desc, q, k, v, doc_start  as for hsap_partial_attn_fwd_runs (same supported
  *              shapes).
  *   tiles, runs, num_runs  device lists from hsap_plan_runs(MAJOR_Q_ALL).
  *   o_out      device bf16 [n, Hq, d] (round to nearest even).
@@ -465,7 +535,7 @@ hsap_status hsap_quantize_fp8_noalloc(const void* x, int32_t groups, int64_t row
                                       uint8_t* codes, float* scale, void* hip_stream);
 
 /*
- * hsap_partial_attn_fwd_fp8 -- hsap_partial_attn_fwd with the scores taken
+ * hsap_partial_attn_fwd_fp8 -- hsap_partial_attn_fwd_runs with the scores taken
  * from e4m3 operands: S = (Q8 K8^T) * q_scale[h] * k_scale[c, g] /
  * sqrt-scale as in desc, i.e. the attention of the dequantised Q and K
  * (codes times scales); softmax, P V (bf16 V) and the outputs as in the bf16
@@ -475,7 +545,7 @@ hsap_status hsap_quantize_fp8_noalloc(const void* x, int32_t groups, int64_t row
  *   k8        device uint8 [P, n, Hkv, d], k_scale device fp32 [P, Hkv]
  *             (G = P), 16-byte aligned.
  *   v, doc_start, tiles, runs, o_part, lse_part, num_slots  as for
- *             hsap_partial_attn_fwd.
+ *             hsap_partial_attn_fwd_runs.
  * Supported: head_dim 128; BM 64, 128 or 256; BN 64 or 128.
  */
 hsap_status hsap_partial_attn_fwd_fp8(const hsap_attn_desc* desc, const uint8_t* q8, const uint8_t* k8,
@@ -520,7 +590,7 @@ hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, 
                                      int32_t head_dim, float* delta, void* hip_stream);
 
 /*
- * hsap_partial_attn_bwd -- "computing" for the backward: the gradients of the
+ * hsap_partial_attn_bwd_runs -- "computing" for the backward: the gradients of the
  * forward above with P = exp(s - LSE) recomputed from the final LSE:
  *   dV_c += P^T dO,  dS = P o (dO V_c^T - delta),
  *   dQ   += scale dS K_c,  dK_c += scale dS^T Q,
@@ -541,7 +611,7 @@ hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, 
  *              k, v, dk_acc and dv_acc are read and written only in the
  *              rows of the chunks that the passed runs' tiles name, so a
  *              caller holding one chunk c alone may pass the addresses that
- *              chunk 0 would have (as for hsap_partial_attn_fwd).
+ *              chunk 0 would have (as for hsap_partial_attn_fwd_runs).
  *   tiles_q, runs_q, num_runs_q  device q-tile runs in which no q_tile
  *              appears twice: hsap_plan_runs(MAJOR_Q_ALL) (every chunk in
  *              one pass), or the runs of one chunk from
@@ -557,7 +627,7 @@ hsap_status hsap_attn_bwd_preprocess(const void* o, const void* d_o, int64_t n, 
  *   The caller zeroes the accumulators once; concurrent calls on the same
  *   accumulators race.
  */
-hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, const void* k,
+hsap_status hsap_partial_attn_bwd_runs(const hsap_attn_desc* desc, const void* q, const void* k,
                                   const void* v, const void* d_o, const float* lse,
                                   const float* delta, const int32_t* doc_start,
                                   const hsap_tile* tiles_k, const hsap_run* runs_k, int64_t num_runs_k,
@@ -565,13 +635,13 @@ hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, con
                                   float* dq_acc, float* dk_acc, float* dv_acc, void* hip_stream);
 
 /*
- * hsap_attn_bwd_bf16 -- hsap_partial_attn_bwd over every chunk in one pass
+ * hsap_attn_bwd_bf16 -- hsap_partial_attn_bwd_runs over every chunk in one pass
  * with the finalisation fused: each q-tile and each (chunk, k_tile, K/V
  * head) block has exactly one owning run, so its gradient is complete in
  * registers and stored once, as bf16 (round to nearest even), instead of
  * being added to fp32 accumulators and converted afterwards.
  *
- *   desc, q, k, v, d_o, lse, delta, doc_start  as for hsap_partial_attn_bwd
+ *   desc, q, k, v, d_o, lse, delta, doc_start  as for hsap_partial_attn_bwd_runs
  *              (same supported shapes).
  *   tiles_k, runs_k, num_runs_k  hsap_plan_runs(MAJOR_K) lists.
  *   tiles_q, runs_q, num_runs_q  hsap_plan_runs(MAJOR_Q_ALL) lists.
@@ -632,7 +702,7 @@ hsap_status hsap_convert_f32_bf16(const float* src, void* dst, int64_t count, vo
  * on one device (the device current at creation), and all its calls should
  * pass the same stream: the single device list buffer is reused in stream
  * order.  Inputs and outputs are caller-owned device tensors in the layouts
- * of hsap_partial_attn_fwd / hsap_partial_attn_bwd.
+ * of hsap_partial_attn_fwd_runs / hsap_partial_attn_bwd_runs.
  * --------------------------------------------------------------------- */
 typedef struct hsap_executor hsap_executor;
 
@@ -660,8 +730,8 @@ typedef struct {
 
 /*
  * hsap_executor_create -- an executor for the shard and heads in `desc`
- * (same supported shapes as hsap_partial_attn_fwd; with HSAP_EXEC_BACKWARD
- * also those of hsap_partial_attn_bwd, checked here: HSAP_ERR_UNSUPPORTED
+ * (same supported shapes as hsap_partial_attn_fwd_runs; with HSAP_EXEC_BACKWARD
+ * also those of hsap_partial_attn_bwd_runs, checked here: HSAP_ERR_UNSUPPORTED
  * before anything is allocated).
  *   options        HSAP_EXEC_* bits.
  *   max_run_tiles  q-major split: -1 picks hsap_split_length per plan from
@@ -698,7 +768,7 @@ hsap_status hsap_executor_info(const hsap_executor* ex, hsap_exec_info* info);
 
 /*
  * hsap_executor_forward -- the shard's attention against every chunk for the
- * current plan.  fused = 0: hsap_partial_attn_fwd over all q-major runs into
+ * current plan.  fused = 0: hsap_partial_attn_fwd_runs over all q-major runs into
  * the executor's partials, then hsap_lse_merge of the num_parts partials --
  * except that a q-tile whose tiles all lie in one chunk, in one unsplit run,
  * has a single part: that run writes its final O (bf16) and LSE to o_out /

@@ -26,7 +26,9 @@ from ._lib import (  # noqa: F401
     lib,
     lse_merge,
     partial_attn_bwd,
+    partial_attn_bwd_runs,
     partial_attn_fwd,
+    partial_attn_fwd_runs,
     plan,
     plan_runs,
     shard_desc,

@@ -37,9 +37,9 @@ EXPORTED = (
     "hsap_status_string", "hsap_last_error", "hsap_plan", "hsap_plan_runs", "hsap_split_length",
     "hsap_fwd_resident_workgroups", "hsap_load_matrix",
     "hsap_balance", "hsap_emit_forward", "hsap_emit_backward", "hsap_doc_start",
-    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_attn_fwd_fused", "hsap_quantize_fp8", "hsap_quantize_fp8_noalloc",
+    "hsap_shard_gather", "hsap_partial_attn_fwd", "hsap_partial_attn_bwd", "hsap_partial_attn_fwd_runs", "hsap_attn_fwd_fused", "hsap_quantize_fp8", "hsap_quantize_fp8_noalloc",
     "hsap_partial_attn_fwd_fp8", "hsap_lse_merge", "hsap_attn_bwd_preprocess",
-    "hsap_partial_attn_bwd", "hsap_attn_bwd_bf16", "hsap_sum_parts", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
+    "hsap_partial_attn_bwd_runs", "hsap_attn_bwd_bf16", "hsap_sum_parts", "hsap_convert_f32_bf16", "hsap_executor_create", "hsap_executor_destroy",
     "hsap_executor_plan", "hsap_executor_info", "hsap_executor_forward", "hsap_executor_partial_forward",
     "hsap_executor_merge", "hsap_executor_backward",
 )
@@ -75,8 +75,8 @@ class ShardDesc(ctypes.Structure):
 
 
 class AttnDesc(ctypes.Structure):
-    _fields_ = [("shard", ShardDesc), ("heads_q", ctypes.c_int32), ("heads_kv", ctypes.c_int32),
-                ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
+    _fields_ = [("shard", ShardDesc), ("chunk_id", ctypes.c_int32), ("heads_q", ctypes.c_int32),
+                ("heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
 
 
 class ExecInfo(ctypes.Structure):
@@ -104,14 +104,16 @@ _SIG = {
     "hsap_emit_backward": (ctypes.c_int, [_I32, _P, _P, _P, _I64, _P, _P]),
     "hsap_doc_start": (ctypes.c_int, [_P, _I32, _I64, _P, _P]),
     "hsap_shard_gather": (ctypes.c_int, [_P, _P, _P, _I64, _P]),
-    "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
+    "hsap_partial_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
+    "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P, _P]),
+    "hsap_partial_attn_fwd_runs": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_attn_fwd_fused": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]),
     "hsap_quantize_fp8": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _P, _P, _P, _P]),
     "hsap_quantize_fp8_noalloc": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_partial_attn_fwd_fp8": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P]),
     "hsap_lse_merge": (ctypes.c_int, [_I32, _P, _P, _I64, _I32, _I32, _P, _P, _P]),
     "hsap_attn_bwd_preprocess": (ctypes.c_int, [_P, _P, _I64, _I32, _I32, _P, _P]),
-    "hsap_partial_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P,
+    "hsap_partial_attn_bwd_runs": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P,
                                              _P]),
     "hsap_attn_bwd_bf16": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P, _P]),
     "hsap_convert_f32_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
@@ -175,8 +177,10 @@ def shard_desc(total_tokens: int, sp_degree: int, layout, shard_id: int, block_m
                      int(batch))
 
 
-def attn_desc(shard: ShardDesc, heads_q: int, heads_kv: int, head_dim: int, softmax_scale: float) -> AttnDesc:
-    return AttnDesc(shard, int(heads_q), int(heads_kv), int(head_dim), float(softmax_scale))
+def attn_desc(shard: ShardDesc, heads_q: int, heads_kv: int, head_dim: int, softmax_scale: float,
+              chunk_id: int = 0) -> AttnDesc:
+    return AttnDesc(shard=shard, chunk_id=int(chunk_id), heads_q=int(heads_q), heads_kv=int(heads_kv),
+                    head_dim=int(head_dim), softmax_scale=float(softmax_scale))
 
 
 def _ptr(a) -> int:
@@ -360,9 +364,66 @@ def shard_gather(shard: ShardDesc, src, dst, stream=None) -> None:
     _check(lib().hsap_shard_gather(ctypes.byref(shard), _ptr(src), _ptr(dst), int(row_bytes), _stream(stream)))
 
 
-def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev, o_part, lse_part,
+def _kv_base(t, chunk: int, n: int, hkv: int, d: int, elem: int, what: str) -> int:
+    """Address of chunk 0 for k / v / dk / dv given either every chunk [P, n, Hkv, d] or chunk c alone."""
+    if t.numel() == n * hkv * d:
+        return _ptr(t) - int(chunk) * n * hkv * d * elem
+    return _ptr(t)
+
+
+def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, o_part, lse_part, stream=None) -> None:
+    """hsap_partial_attn_fwd: shard r's queries against chunk desc.chunk_id over that chunk's tiles (int32
+    [T, 4], hsap_plan's order) -> o_part fp32 [n, Hq, d], lse_part fp32 [Hq, n].  k / v are every chunk
+    [P, n, Hkv, d] or chunk chunk_id alone [n, Hkv, d]."""
+    s = desc.shard
+    n = s.rows
+    hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
+    _dev(q, "bfloat16", "q", n * hq * d)
+    for t, name in ((k, "k"), (v, "v")):
+        _dev(t, "bfloat16", name)
+        if t.numel() not in (n * hkv * d, P * n * hkv * d):
+            raise ValueError("%s must hold one chunk or every chunk" % name)
+    _dev(doc_start_dev, "int32", "doc_start", s.positions)
+    _dev(tiles_dev, "int32", "tiles")
+    _dev(o_part, "float32", "o_part", n * hq * d)
+    _dev(lse_part, "float32", "lse_part", hq * n)
+    c = desc.chunk_id
+    _check(lib().hsap_partial_attn_fwd(ctypes.byref(desc), _ptr(q), _kv_base(k, c, n, hkv, d, 2, "k"),
+                                       _kv_base(v, c, n, hkv, d, 2, "v"), _ptr(doc_start_dev), _ptr(tiles_dev),
+                                       tiles_dev.numel() // 4, _ptr(o_part), _ptr(lse_part), _stream(stream)))
+
+
+def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_dev, dq_acc, dk_acc, dv_acc,
+                     stream=None) -> None:
+    """hsap_partial_attn_bwd: the gradients of partial_attn_fwd's partial (chunk desc.chunk_id, its tiles),
+    accumulated (+=) into dq_acc fp32 [n, Hq, d] and dk_acc / dv_acc fp32 (every chunk [P, n, Hkv, d] or
+    chunk chunk_id alone [n, Hkv, d], like k / v)."""
+    s = desc.shard
+    n = s.rows
+    hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
+    _dev(q, "bfloat16", "q", n * hq * d)
+    _dev(d_o, "bfloat16", "d_o", n * hq * d)
+    _dev(lse, "float32", "lse", hq * n)
+    _dev(delta, "float32", "delta", hq * n)
+    for t, name, dt in ((k, "k", "bfloat16"), (v, "v", "bfloat16"), (dk_acc, "dk_acc", "float32"),
+                        (dv_acc, "dv_acc", "float32")):
+        _dev(t, dt, name)
+        if t.numel() not in (n * hkv * d, P * n * hkv * d):
+            raise ValueError("%s must hold one chunk or every chunk" % name)
+    _dev(doc_start_dev, "int32", "doc_start", s.positions)
+    _dev(tiles_dev, "int32", "tiles")
+    _dev(dq_acc, "float32", "dq_acc", n * hq * d)
+    c = desc.chunk_id
+    _check(lib().hsap_partial_attn_bwd(ctypes.byref(desc), _ptr(q), _kv_base(k, c, n, hkv, d, 2, "k"),
+                                       _kv_base(v, c, n, hkv, d, 2, "v"), _ptr(d_o), _ptr(lse), _ptr(delta),
+                                       _ptr(doc_start_dev), _ptr(tiles_dev), tiles_dev.numel() // 4, _ptr(dq_acc),
+                                       _kv_base(dk_acc, c, n, hkv, d, 4, "dk"), _kv_base(dv_acc, c, n, hkv, d, 4, "dv"),
+                                       _stream(stream)))
+
+
+def partial_attn_fwd_runs(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev, o_part, lse_part,
                      stream=None, kv_chunk: Optional[int] = None) -> None:
-    """hsap_partial_attn_fwd.  k / v are [P, n, Hkv, d] (every chunk, sharded order), or, with
+    """hsap_partial_attn_fwd_runs.  k / v are [P, n, Hkv, d] (every chunk, sharded order), or, with
     ``kv_chunk`` = c, [n, Hkv, d] holding chunk c alone (every run passed must be of chunk c):
     the library then gets the address chunk 0 would have, and reads only chunk c's rows."""
     s = desc.shard
@@ -385,7 +446,7 @@ def partial_attn_fwd(desc: AttnDesc, q, k, v, doc_start_dev, tiles_dev, runs_dev
     slots = o_part.numel() // (n * hq * d)
     if o_part.numel() != slots * n * hq * d or lse_part.numel() != slots * hq * n or slots < 1:
         raise ValueError("o_part / lse_part must hold a whole number of [n, Hq, d] / [Hq, n] slots")
-    _check(lib().hsap_partial_attn_fwd(ctypes.byref(desc), _ptr(q), _ptr(k) - kv_shift, _ptr(v) - kv_shift,
+    _check(lib().hsap_partial_attn_fwd_runs(ctypes.byref(desc), _ptr(q), _ptr(k) - kv_shift, _ptr(v) - kv_shift,
                                        _ptr(doc_start_dev),
                                        _ptr(tiles_dev), _ptr(runs_dev), runs_dev.numel() // 4, _ptr(o_part),
                                        _ptr(lse_part), int(slots), _stream(stream)))
@@ -427,7 +488,7 @@ def quantize_fp8_noalloc(x, codes, scale, stream=None) -> None:
 def partial_attn_fwd_fp8(desc: AttnDesc, q8, k8, v, q_scale, k_scale, doc_start_dev, tiles_dev, runs_dev, o_part,
                          lse_part, stream=None) -> None:
     """hsap_partial_attn_fwd_fp8: the partial forward with e4m3 Q [n, Hq, d] and K [P, n, Hkv, d] and their
-    scales [Hq] and [P, Hkv] (hsap_quantize_fp8); V, outputs and lists as for partial_attn_fwd."""
+    scales [Hq] and [P, Hkv] (hsap_quantize_fp8); V, outputs and lists as for partial_attn_fwd_runs."""
     s = desc.shard
     n = s.rows
     hq, hkv, d, P = desc.heads_q, desc.heads_kv, desc.head_dim, s.sp_degree
@@ -492,9 +553,9 @@ def attn_bwd_preprocess(o, d_o, n: int, heads_q: int, head_dim: int, delta, stre
                                           _stream(stream)))
 
 
-def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_k_dev, runs_k_dev, tiles_q_dev,
+def partial_attn_bwd_runs(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, tiles_k_dev, runs_k_dev, tiles_q_dev,
                      runs_q_dev, dq_acc, dk_acc, dv_acc, stream=None, kv_chunk: Optional[int] = None) -> None:
-    """hsap_partial_attn_bwd.  Either run list may be None to skip its kernel.  With ``kv_chunk`` = c,
+    """hsap_partial_attn_bwd_runs.  Either run list may be None to skip its kernel.  With ``kv_chunk`` = c,
     k, v, dk_acc and dv_acc are [n, Hkv, d] tensors of chunk c alone (every run passed must be of
     chunk c), passed as the addresses chunk 0 would have."""
     s = desc.shard
@@ -521,7 +582,7 @@ def partial_attn_bwd(desc: AttnDesc, q, k, v, d_o, lse, delta, doc_start_dev, ti
     _dev(dv_acc, "float32", "dv_acc", kv_rows * n * hkv * d)
     nk = runs_k_dev.numel() // 4 if runs_k_dev is not None else 0
     nq = runs_q_dev.numel() // 4 if runs_q_dev is not None else 0
-    _check(lib().hsap_partial_attn_bwd(ctypes.byref(desc), _ptr(q), _ptr(k) - 2 * kv_shift, _ptr(v) - 2 * kv_shift,
+    _check(lib().hsap_partial_attn_bwd_runs(ctypes.byref(desc), _ptr(q), _ptr(k) - 2 * kv_shift, _ptr(v) - 2 * kv_shift,
                                        _ptr(d_o), _ptr(lse), _ptr(delta), _ptr(doc_start_dev), _ptr(tiles_k_dev),
                                        _ptr(runs_k_dev), nk, _ptr(tiles_q_dev), _ptr(runs_q_dev), nq, _ptr(dq_acc),
                                        _ptr(dk_acc) - 4 * kv_shift, _ptr(dv_acc) - 4 * kv_shift, _stream(stream)))

@@ -169,7 +169,7 @@ class AllShards:
             for r in range(P):
                 runs = self.runs[e][r]
                 if runs is not None:
-                    L.partial_attn_fwd(self.descs[r], q[r], k, v, self.doc_start, self.tiles_dev[r], runs,
+                    L.partial_attn_fwd_runs(self.descs[r], q[r], k, v, self.doc_start, self.tiles_dev[r], runs,
                                        bufs["o_part"][r], bufs["lse_part"][r])
             if timed:
                 ev[e][1].record()
@@ -229,7 +229,7 @@ class AllShards:
                     for t_ in (dq_t, dk_t, dv_t):
                         t_.zero_()
                     runs_q, runs_k = self.bwd_runs[(r, c)]
-                    L.partial_attn_bwd(self.descs[r], q[r], k[c], v[c], d_o[r], lse[r], bufs["delta"][r],
+                    L.partial_attn_bwd_runs(self.descs[r], q[r], k[c], v[c], d_o[r], lse[r], bufs["delta"][r],
                                        self.doc_start, self.bwd_tiles_k[r], runs_k, self.bwd_tiles_q[r], runs_q,
                                        dq_t, dk_t, dv_t, kv_chunk=c)
             if timed:

@@ -55,10 +55,16 @@ struct BwdArgs {
   int32_t bm;
   float scale;
   float scale_log2;
+  int32_t num_tiles;     // tile-list mode: entries of tiles (one chunk's, sorted by q_tile)
+  int32_t chunk;         // tile-list mode: the chunk of every tile
 };
 
-template <int D, int WAVES, bool BF16OUT>
+// Tile-list mode of the dK/dV kernel: at most this many q-tiles (n / BM) per k-tile.
+constexpr int kMaxListQTiles = 2048;
+
+template <int D, int WAVES, bool BF16OUT, bool LIST = false>
 __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a) {
+  static_assert(!LIST || !BF16OUT, "the tile-list mode accumulates fp32");
   constexpr int BN = 32 * WAVES;
   constexpr int NT = 64 * WAVES;
   constexpr int SUB = 64;                 // query rows per sub-tile
@@ -73,13 +79,47 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   __shared__ __attribute__((aligned(16))) float lse_s[2][SUB];
   __shared__ __attribute__((aligned(16))) float delta_s[2][SUB];
   __shared__ __attribute__((aligned(16))) int32_t start_s[2][SUB];
+  __shared__ uint32_t qlist[LIST ? kMaxListQTiles : 1];  // tile-list mode: this k-tile's q-tiles (q_tile | kind << 31)
+  __shared__ int32_t wave_hits[WAVES];
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int run_idx = blockIdx.x / a.hkv;
   const int g = blockIdx.x - run_idx * a.hkv;
-  const hsap_run run = a.runs[run_idx];
-  const int c = a.tiles[run.first].chunk;  // k-major runs are never empty
+  // Run mode: a k-major run from hsap_plan_runs (never empty).  Tile-list mode: k-tile run_idx of
+  // chunk a.chunk; the workgroup gathers the tiles with that k_tile from the list (sorted by
+  // q_tile) into LDS, in list order, 64 per wave per pass.
+  constexpr bool list_mode = LIST;
+  const hsap_run run = list_mode ? hsap_run{a.chunk, run_idx, 0, 0} : a.runs[run_idx];
+  const int c = list_mode ? a.chunk : a.tiles[run.first].chunk;
+  int count = run.count;
+  if (list_mode) {
+    int total = 0;
+    for (int base = 0; base < a.num_tiles; base += 64 * WAVES) {
+      const int i = base + 64 * w + lane;
+      bool hit = false;
+      uint32_t packed = 0u;
+      if (i < a.num_tiles) {
+        const hsap_tile t = a.tiles[i];
+        hit = t.k_tile == run.tile;
+        packed = (uint32_t)t.q_tile | ((uint32_t)t.kind << 31);
+      }
+      const uint64_t m = __builtin_amdgcn_ballot_w64(hit);
+      const int rank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (lane == 0) wave_hits[w] = __popcll(m);
+      __syncthreads();
+      int off = total, all = 0;
+      for (int x = 0; x < WAVES; ++x) {
+        off += x < w ? wave_hits[x] : 0;
+        all += wave_hits[x];
+      }
+      if (hit && off + rank < kMaxListQTiles) qlist[off + rank] = packed;
+      total += all;
+      __syncthreads();  // wave_hits is rewritten by the next pass; qlist is complete after the last
+    }
+    count = min(total, kMaxListQTiles);
+    if (count == 0) return;  // no query of the shard reaches this k-tile in the chunk: nothing to add
+  }
   const int64_t n = a.geom.n;
   const int64_t krow0 = (int64_t)run.tile * BN;
   const int32_t gk = (int32_t)global_pos(a.geom, c, krow0 + 32 * w + l32);  // this lane's key position
@@ -119,7 +159,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   }
 
   const int nsub = a.bm / SUB;
-  const int per_head = run.count * nsub;
+  const int per_head = count * nsub;
   const int total = a.group * per_head;
   // The run's q-tiles, packed one per lane (q_tile | kind << 31) in windows of 64 tiles, read
   // with v_readlane: the next sub-tile's address never waits on a memory load.  Window v lives
@@ -130,9 +170,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
   auto load_window = [&](int v) {
     const int i = 64 * v + lane;
     uint32_t p = 0;
-    if (i < run.count) {
-      const hsap_tile t = a.tiles[run.first + i];
-      p = (uint32_t)t.q_tile | ((uint32_t)t.kind << 31);
+    if (i < count) {
+      if (!list_mode) {
+        const hsap_tile t = a.tiles[run.first + i];
+        p = (uint32_t)t.q_tile | ((uint32_t)t.kind << 31);
+      } else {
+        p = qlist[i];
+      }
     }
     if (v & 1) win1 = p;
     else win0 = p;
@@ -311,8 +355,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
 // the end, by the q-tile's only run: a plain read-add-write of the fp32
 // accumulator, or a store of the final bf16 value.
 // ---------------------------------------------------------------------------
-template <int D, int BN, int WAVES, bool BF16OUT>
+template <int D, int BN, int WAVES, bool BF16OUT, bool LIST = false>
 __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
+  static_assert(!LIST || !BF16OUT, "the tile-list mode accumulates fp32");
   constexpr int KB = 64;                     // keys per step
   constexpr int SUBS = BN / KB;
   constexpr int NT = 64 * WAVES;
@@ -329,7 +374,8 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int run_idx = blockIdx.x / a.hq;
   const int h = blockIdx.x - run_idx * a.hq;
-  const hsap_run run = a.runs[run_idx];
+  // LIST: the tile-list mode, this workgroup's q-tile found in one chunk's list
+  const hsap_run run = LIST ? q_tile_run(a.tiles, a.num_tiles, run_idx, lane) : a.runs[run_idx];
   const int g = h / a.group;
   const int64_t n = a.geom.n;
   const int64_t qrow = (int64_t)run.tile * (32 * WAVES) + 32 * w + l32;
@@ -537,23 +583,23 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
     }
 }
 
-template <int D, int WAVES, bool BF16OUT>
+template <int D, int WAVES, bool BF16OUT, bool LIST = false>
 static hsap_status launch_dkdv(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hkv;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, WAVES, BF16OUT>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream,
-                     a);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, WAVES, BF16OUT, LIST>), dim3((unsigned)blocks), dim3(64 * WAVES), 0,
+                     stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_bwd_dkdv launch: %s", hipGetErrorString(e));
   return HSAP_OK;
 }
 
-template <int D, int BN, int WAVES, bool BF16OUT>
+template <int D, int BN, int WAVES, bool BF16OUT, bool LIST = false>
 static hsap_status launch_dq(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, BN, WAVES, BF16OUT>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream,
-                     a);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, BN, WAVES, BF16OUT, LIST>), dim3((unsigned)blocks), dim3(64 * WAVES), 0,
+                     stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_bwd_dq launch: %s", hipGetErrorString(e));
   return HSAP_OK;
@@ -665,11 +711,88 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
   return HSAP_OK;
 }
 
+// hsap_partial_attn_bwd: both kernels in tile-list mode over one chunk's tiles (fp32 accumulators).
+static hsap_status backward_tile_list(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                      const void* d_o, const float* lse, const float* delta,
+                                      const int32_t* doc_start, const hsap_tile* tiles, int64_t num_tiles,
+                                      float* dq, float* dk, float* dv, hipStream_t s) {
+  Geom geom;
+  hsap_status st = check_attn(desc, &geom);
+  if (st != HSAP_OK) return st;
+  const int bm = desc->shard.block_m, bn = desc->shard.block_n, d = desc->head_dim;
+  if (!backward_supported(desc))
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "no backward kernel for head_dim=%d BM=%d BN=%d", d, bm, bn);
+  if ((int64_t)desc->heads_kv * d * 64 > INT32_MAX) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "heads_kv too large");
+  if (desc->chunk_id < 0 || desc->chunk_id >= geom.P)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "chunk_id %d outside [0, %d)", desc->chunk_id, geom.P);
+  if (num_tiles < 0 || num_tiles > (int64_t(1) << 30))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "bad num_tiles %lld", (long long)num_tiles);
+  if (geom.n / bm > kMaxListQTiles)
+    HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "the tile-list backward needs n / BM <= %d (%lld)", kMaxListQTiles,
+              (long long)(geom.n / bm));
+  if (geom.n / bn >= kMaxDqKTiles) HSAP_FAIL(HSAP_ERR_UNSUPPORTED, "too many k-tiles per chunk");
+  if (!q || !k || !v || !d_o || !lse || !delta || !doc_start || !dq || !dk || !dv || (num_tiles > 0 && !tiles))
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)d_o | (uintptr_t)dq) & 15)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k, v, d_o and dq_acc must be 16-byte aligned");
+  if (num_tiles == 0) return HSAP_OK;  // no pair of this shard and chunk: every gradient term is 0
+  BwdArgs a = {};
+  a.q = (const __bf16*)q;
+  a.k = (const __bf16*)k;
+  a.v = (const __bf16*)v;
+  a.d_o = (const __bf16*)d_o;
+  a.lse = lse;
+  a.delta = delta;
+  a.doc_start = doc_start;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.geom = geom;
+  a.shard = desc->shard.shard_id;
+  a.hq = desc->heads_q;
+  a.hkv = desc->heads_kv;
+  a.group = desc->heads_q / desc->heads_kv;
+  a.bm = bm;
+  a.scale = desc->softmax_scale;
+  a.scale_log2 = desc->softmax_scale * 1.44269504088896340736f;
+  a.tiles = tiles;
+  a.runs = nullptr;
+  a.num_tiles = (int32_t)num_tiles;
+  a.chunk = desc->chunk_id;
+  const int64_t q_tiles = geom.n / bm, k_tiles = geom.n / bn;
+#define HSAP_DQ_CASE(D_, BN_, W_) \
+  if (d == D_ && bn == BN_ && bm == 32 * W_) st = launch_dq<D_, BN_, W_, false, true>(a, q_tiles, s);
+  HSAP_DQ_CASE(128, 128, 8)
+  else HSAP_DQ_CASE(128, 64, 8)
+  else HSAP_DQ_CASE(128, 128, 4)
+  else HSAP_DQ_CASE(128, 64, 4)
+  else HSAP_DQ_CASE(128, 128, 2)
+  else HSAP_DQ_CASE(128, 64, 2)
+  else HSAP_DQ_CASE(64, 128, 4)
+  else HSAP_DQ_CASE(64, 64, 4)
+  else HSAP_DQ_CASE(64, 128, 2)
+  else HSAP_DQ_CASE(64, 64, 2)
+#undef HSAP_DQ_CASE
+  if (st != HSAP_OK) return st;
+  if (d == 128 && bn == 128) return launch_dkdv<128, 4, false, true>(a, k_tiles, s);
+  if (d == 128) return launch_dkdv<128, 2, false, true>(a, k_tiles, s);
+  return launch_dkdv<64, 2, false, true>(a, k_tiles, s);
+}
+
 }  // namespace hsap
 
 using namespace hsap;
 
 extern "C" hsap_status hsap_partial_attn_bwd(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                             const void* d_o, const float* lse, const float* delta,
+                                             const int32_t* doc_start, const hsap_tile* tiles, int64_t num_tiles,
+                                             float* dq_acc, float* dk_acc, float* dv_acc, void* hip_stream) {
+  clear_error();
+  return backward_tile_list(desc, q, k, v, d_o, lse, delta, doc_start, tiles, num_tiles, dq_acc, dk_acc, dv_acc,
+                            (hipStream_t)hip_stream);
+}
+
+extern "C" hsap_status hsap_partial_attn_bwd_runs(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
                                              const void* d_o, const float* lse, const float* delta,
                                              const int32_t* doc_start, const hsap_tile* tiles_k,
                                              const hsap_run* runs_k, int64_t num_runs_k, const hsap_tile* tiles_q,

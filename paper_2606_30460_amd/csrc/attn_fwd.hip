@@ -57,6 +57,7 @@ struct FwdArgs {
   const float* k_scale;  // fp8 scores: dequantisation scale per (chunk, K/V head) [P, Hkv]
   const int32_t* cu;     // when set: cumulative document lengths [num_docs + 1], used instead of doc_start
   int32_t num_docs;
+  int32_t num_tiles;     // runs == NULL: one chunk's tiles sorted by q_tile; workgroup t runs q-tile t
   Geom geom;
   int32_t shard;
   int32_t hq;
@@ -128,9 +129,10 @@ __device__ __forceinline__ float fp8_step_scale(float sl) { return fmaxf(sl, 1.1
 
 // FP8: Q and K are e4m3 codes (scores S = (Q8 K8^T) * q_scale[h] * k_scale[chunk, g]
 // from the 32x32x64 fp8 MFMA, a K row held as 128 bytes), V and the rest as in bf16.
-template <int D, int BN, int WAVES, bool FUSED, bool FP8 = false>
+template <int D, int BN, int WAVES, bool FUSED, bool FP8 = false, bool LIST = false>
 __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   static_assert(!FP8 || D == 128, "fp8 scores need head_dim 128");
+  static_assert(!LIST || (!FUSED && !FP8), "the tile-list mode is the bf16 partial forward's");
   using KT = std::conditional_t<FP8, uint8_t, __bf16>;    // K element
   using K16 = std::conditional_t<FP8, uint4, bf16x8>;     // 16 bytes of K
   constexpr int KB = 64;                     // keys per step
@@ -154,7 +156,8 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int run_idx = blockIdx.x / a.hq;  // runs are longest first: long work starts first
   const int h = blockIdx.x - run_idx * a.hq;
-  const hsap_run run = a.runs[run_idx];
+  // LIST: the tile-list mode of the partial forward, this workgroup's q-tile found in one chunk's list
+  const hsap_run run = LIST ? q_tile_run(a.tiles, a.num_tiles, run_idx, lane) : a.runs[run_idx];
   const int slot = run.slot;  // partial-output slot of this run (partial forward)
   // FUSED, or a partial run marked final (its q-tile's only part): write the final output
   const bool final_out = FUSED || (slot == kFinalSlot && a.o_out != nullptr);
@@ -434,9 +437,10 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 // ---------------------------------------------------------------------------
 // FP8: Q and K are e4m3 codes (scores from the 32x32x64 fp8 MFMA times q_scale[h] *
 // k_scale[chunk, g]); K tiles are [64][128 bytes], swizzled over their 8 chunks per row.
-template <int BN, int WAVES, bool FUSED, bool FP8 = false>
+template <int BN, int WAVES, bool FUSED, bool FP8 = false, bool LIST = false>
 __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   static_assert(WAVES == 4 || WAVES == 8, "four or eight waves");
+  static_assert(!LIST || (!FUSED && !FP8), "the tile-list mode is the bf16 partial forward's");
   using KT = std::conditional_t<FP8, uint8_t, __bf16>;  // K element
   constexpr int D = 128, KB = 64, SUBS = BN / KB, CPR = D / 8, TILE = KB * D;
   constexpr int KCPR = D * (int)sizeof(KT) / 16;        // 16-byte chunks per K row
@@ -456,7 +460,8 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int run_idx = blockIdx.x / a.hq;
   const int h = blockIdx.x - run_idx * a.hq;
-  const hsap_run run = a.runs[run_idx];
+  // LIST: the tile-list mode of the partial forward, this workgroup's q-tile found in one chunk's list
+  const hsap_run run = LIST ? q_tile_run(a.tiles, a.num_tiles, run_idx, lane) : a.runs[run_idx];
   const int slot = run.slot;
   const bool final_out = FUSED || (slot == kFinalSlot && a.o_out != nullptr);
   if (!final_out && (slot < 0 || slot >= a.num_slots)) return;
@@ -755,6 +760,15 @@ template <int BN, int WAVES, bool FUSED, bool FP8 = false>
 static hsap_status launch_dl(const FwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
+  if constexpr (!FUSED && !FP8) {
+    if (!a.runs) {
+      hipLaunchKernelGGL((attn_fwd_dl_kernel<BN, WAVES, false, false, true>), dim3((unsigned)blocks), dim3(64 * WAVES),
+                         0, stream, a);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
+      return HSAP_OK;
+    }
+  }
   hipLaunchKernelGGL((attn_fwd_dl_kernel<BN, WAVES, FUSED, FP8>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream,
                      a);
   const hipError_t e = hipGetLastError();
@@ -766,6 +780,15 @@ template <int D, int BN, int WAVES, bool FUSED, bool FP8 = false>
 static hsap_status launch(const FwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
   if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
+  if constexpr (!FUSED && !FP8) {
+    if (!a.runs) {
+      hipLaunchKernelGGL((attn_fwd_kernel<D, BN, WAVES, false, false, true>), dim3((unsigned)blocks), dim3(64 * WAVES),
+                         0, stream, a);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
+      return HSAP_OK;
+    }
+  }
   hipLaunchKernelGGL((attn_fwd_kernel<D, BN, WAVES, FUSED, FP8>), dim3((unsigned)blocks), dim3(64 * WAVES), 0, stream,
                      a);
   const hipError_t e = hipGetLastError();
@@ -794,7 +817,7 @@ static hsap_status forward(const hsap_attn_desc* desc, const void* q, const void
               "no forward kernel for head_dim=%d BM=%d BN=%d (BM in {64, 128}, or 256 with d = 128; BN in {64, 128})",
               d, bm, bn);
   if (num_runs == 0) return HSAP_OK;
-  if (!q || !k || !v || !(doc_start || a.cu) || !tiles || !runs)
+  if (!q || !k || !v || !(doc_start || a.cu) || (!runs && FUSED) || (runs && !tiles) || (!runs && a.num_tiles && !tiles))
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
   if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v) & 15)
     HSAP_FAIL(HSAP_ERR_INVALID_ARG, "q, k and v must be 16-byte aligned");
@@ -906,6 +929,28 @@ extern "C" hsap_status hsap_fwd_resident_workgroups(const hsap_attn_desc* desc, 
 }
 
 extern "C" hsap_status hsap_partial_attn_fwd(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
+                                             const int32_t* doc_start, const hsap_tile* tiles, int64_t num_tiles,
+                                             float* o_part, float* lse_part, void* hip_stream) {
+  clear_error();
+  Geom geom;
+  const hsap_status st = check_attn(desc, &geom);
+  if (st != HSAP_OK) return st;
+  if (desc->chunk_id < 0 || desc->chunk_id >= geom.P)
+    HSAP_FAIL(HSAP_ERR_INVALID_ARG, "chunk_id %d outside [0, %d)", desc->chunk_id, geom.P);
+  if (num_tiles < 0 || num_tiles > (int64_t(1) << 30)) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "bad num_tiles %lld", (long long)num_tiles);
+  if (!o_part || !lse_part || !doc_start) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "NULL pointer argument");
+  if ((uintptr_t)o_part & 15) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "o_part must be 16-byte aligned");
+  FwdArgs a{};
+  a.o_part = o_part;
+  a.lse_part = lse_part;
+  a.num_slots = 1;
+  a.num_tiles = (int32_t)num_tiles;
+  // one workgroup per (q-tile, head): each finds its q-tile's tiles in the list
+  return forward<false>(desc, q, k, v, doc_start, tiles, nullptr, geom.n / desc->shard.block_m, a,
+                        (hipStream_t)hip_stream);
+}
+
+extern "C" hsap_status hsap_partial_attn_fwd_runs(const hsap_attn_desc* desc, const void* q, const void* k, const void* v,
                                              const int32_t* doc_start, const hsap_tile* tiles, const hsap_run* runs,
                                              int64_t num_runs, float* o_part, float* lse_part, int32_t num_slots,
                                              void* hip_stream) {

@@ -71,6 +71,35 @@ hsap_status check_attn(const hsap_attn_desc* d, Geom* g);
 bool backward_supported(const hsap_attn_desc* d);
 
 #if defined(__HIPCC__)
+// First index i of tiles[0 .. num - 1] (sorted by q_tile) with tiles[i].q_tile >= key, for the
+// tile-list entry points (one chunk's tiles in the planner's order).  Wave-wide: each round
+// narrows the range 64-fold with one strided probe per lane, the last compares a window of at
+// most 64 entries; every probe stays inside the list (num <= 2^30).  The result is the same on
+// every lane.
+__device__ inline int32_t lower_bound_q_tile(const hsap_tile* tiles, int32_t num, int32_t key, int lane) {
+  if (num <= 0) return 0;
+  int32_t lo = 0, len = num;
+  while (len > 64) {
+    const int32_t stride = (len + 63) >> 6;
+    const int32_t idx = min(lo + lane * stride, lo + len - 1);
+    const bool below = lo + lane * stride < lo + len && tiles[idx].q_tile < key;
+    const int32_t cnt = __popcll(__builtin_amdgcn_ballot_w64(below));
+    if (cnt == 0) return lo;  // tiles[lo] is already >= key
+    const int32_t next = lo + (cnt - 1) * stride + 1;
+    len = min(lo + cnt * stride, lo + len) - next;
+    lo = next;
+  }
+  const bool below = lane < len && tiles[min(lo + lane, num - 1)].q_tile < key;
+  return lo + __popcll(__builtin_amdgcn_ballot_w64(below));
+}
+
+// The run of q-tile qt in a sorted tile list: {slot 0, qt, first, count}.
+__device__ inline hsap_run q_tile_run(const hsap_tile* tiles, int32_t num, int32_t qt, int lane) {
+  const int32_t first = lower_bound_q_tile(tiles, num, qt, lane);
+  const int32_t end = lower_bound_q_tile(tiles, num, qt + 1, lane);
+  return hsap_run{0, qt, first, end - first};
+}
+
 // Workgroups of the bf16 partial forward resident on one compute unit for the descriptor's shape
 // (the runtime's occupancy of the kernel that runs); 0 when there is none.
 int fwd_resident_per_cu(const hsap_attn_desc* d);
@@ -91,7 +120,7 @@ hsap_status lse_merge(int32_t num_parts, const float* const* o_parts, const floa
 
 // The executor's forwards.  Document starts come from the cumulative lengths cu_seqlens
 // [num_docs + 1] on the device (no per-position start array).  fused: hsap_attn_fwd_fused over
-// runs that span every chunk.  Otherwise hsap_partial_attn_fwd, where runs whose slot is
+// runs that span every chunk.  Otherwise hsap_partial_attn_fwd_runs, where runs whose slot is
 // kFinalSlot write the final bf16 O and LSE of their q-tile to o_out / lse_out (the q-tile's
 // only part: nothing to merge).
 constexpr int32_t kFinalSlot = -2;

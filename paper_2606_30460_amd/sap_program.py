@@ -173,7 +173,7 @@ class SapProgram:
                                 ob, lb = bufs["o_part"][e], bufs["lse_part"][e]
                             else:
                                 ob, lb = bufs["o_res"][e], bufs["lse_res"][e]
-                            L.partial_attn_fwd(self.descs[shard], qq, kk, vv, self.doc_start, self.tiles_dev[shard],
+                            L.partial_attn_fwd_runs(self.descs[shard], qq, kk, vv, self.doc_start, self.tiles_dev[shard],
                                                self._runs(shard, chunk, out_slot), ob, lb, stream=s, kv_chunk=chunk)
                         elif op == L.OP_MERGE:
                             parts = out_slot
@@ -317,6 +317,6 @@ class SapProgram:
             dk_t, dv_t = bufs["dk_res"][e][out_slot], bufs["dv_res"][e][out_slot]
         for t_ in (dq_t, dk_t, dv_t):
             t_.zero_()
-        L.partial_attn_bwd(self.descs[r], qq, kk, vv, dd, ll, de, self.doc_start, self.tiles_k_dev[r],
+        L.partial_attn_bwd_runs(self.descs[r], qq, kk, vv, dd, ll, de, self.doc_start, self.tiles_k_dev[r],
                            self._runs_k(r, c), self.tiles_dev[r], self._runs(r, c, c), dq_t, dk_t, dv_t,
                            stream=stream, kv_chunk=c)

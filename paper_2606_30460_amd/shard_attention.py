@@ -143,10 +143,10 @@ class ShardAttention:
         if ring_steps:
             for runs in self.runs_q_step:
                 if runs is not None:
-                    L.partial_attn_fwd(self.desc, q, k, v, self.doc_start, self.tiles_q, runs, bufs["o_part"],
+                    L.partial_attn_fwd_runs(self.desc, q, k, v, self.doc_start, self.tiles_q, runs, bufs["o_part"],
                                        bufs["lse_part"])
         else:
-            L.partial_attn_fwd(self.desc, q, k, v, self.doc_start, self.tiles_q, self.runs_q, bufs["o_part"],
+            L.partial_attn_fwd_runs(self.desc, q, k, v, self.doc_start, self.tiles_q, self.runs_q, bufs["o_part"],
                                bufs["lse_part"])
         L.lse_merge([bufs["o_part"][s] for s in self.present], [bufs["lse_part"][s] for s in self.present],
                     self.n, self.hq, self.d, bufs["o"], bufs["lse"])
@@ -171,7 +171,7 @@ class ShardAttention:
                 bufs["dv_acc"][c].zero_()
         L.attn_bwd_preprocess(fwd["o"], d_o, self.n, self.hq, self.d, bufs["delta"])
         # dQ over the one-run-per-q-tile lists (every chunk), so each q-tile has one owner
-        L.partial_attn_bwd(self.desc, q, k, v, d_o, fwd["lse"], bufs["delta"], self.doc_start, self.tiles_k,
+        L.partial_attn_bwd_runs(self.desc, q, k, v, d_o, fwd["lse"], bufs["delta"], self.doc_start, self.tiles_k,
                            self.runs_k, self.tiles_all, self.runs_all, bufs["dq_acc"], bufs["dk_acc"], bufs["dv_acc"])
         L.convert_f32_bf16(bufs["dq_acc"], bufs["dq"])
         # only chunks with tiles receive gradient; the others are zero

@@ -125,6 +125,51 @@ class Case:
         finally:
             ex.close()
 
+    def run_tile_list(self, backward: Optional[bool] = None) -> Dict[str, np.ndarray]:
+        """The shard through the boundary's tile-list calls, ring step by ring step: hsap_plan, then
+        per chunk c hsap_partial_attn_fwd on the step's tiles (one chunk's K/V passed alone) into
+        its own partial, hsap_lse_merge of the partials of the chunks with tiles; with the backward,
+        hsap_attn_bwd_preprocess and per chunk hsap_partial_attn_bwd accumulating dQ and that
+        chunk's dK/dV.  Partials and gradients are pre-filled with NaN / zero."""
+        bwd = self.backward if backward is None else backward
+        s = L.shard_desc(self.N, self.P, self.layout, self.shard, self.bm, self.bn)
+        dev = torch.device("cuda")
+        p = L.plan(self.cu, s)
+        offs = p["step_offsets"]
+        n = self.N // self.P
+        q = to_sharded(s, self.q.to(dev))[self.shard].contiguous()
+        k, v = to_sharded(s, self.k.to(dev)), to_sharded(s, self.v.to(dev))
+        doc_start = torch.empty(self.N, dtype=torch.int32, device=dev)
+        L.doc_start(torch.from_numpy(self.cu).to(dev), self.N, doc_start)
+        o_part = torch.full((self.P, n, self.hq, self.d), float("nan"), dtype=torch.float32, device=dev)
+        lse_part = torch.full((self.P, self.hq, n), float("nan"), dtype=torch.float32, device=dev)
+        chunks, lists = [], {}
+        for step in range(self.P):
+            c = (self.shard - step) % self.P
+            chunks.append(c)
+            lists[c] = torch.from_numpy(np.ascontiguousarray(p["tiles"][offs[step]:offs[step + 1]]).reshape(-1)).to(dev)
+            desc = L.attn_desc(s, self.hq, self.hkv, self.d, 1.0 / float(np.sqrt(self.d)), chunk_id=c)
+            L.partial_attn_fwd(desc, q, k[c], v[c], doc_start, lists[c], o_part[c], lse_part[c])
+        present = [c for c in sorted(chunks) if lists[c].numel()]
+        o = torch.empty(n, self.hq, self.d, dtype=torch.bfloat16, device=dev)
+        lse = torch.empty(self.hq, n, dtype=torch.float32, device=dev)
+        L.lse_merge([o_part[c] for c in present], [lse_part[c] for c in present], n, self.hq, self.d, o, lse)
+        out = {"chunks": chunks, "o_part": o_part.cpu().numpy(), "lse_part": lse_part.cpu().numpy(),
+               "o": o.float().cpu().numpy(), "lse": lse.cpu().numpy(), "tiles": p["tiles"], "step_offsets": offs}
+        if bwd:
+            d_o = to_sharded(s, self.do.to(dev))[self.shard].contiguous()
+            delta = torch.empty(self.hq, n, dtype=torch.float32, device=dev)
+            L.attn_bwd_preprocess(o, d_o, n, self.hq, self.d, delta)
+            dq = torch.zeros(n, self.hq, self.d, dtype=torch.float32, device=dev)
+            dk = torch.zeros(self.P, n, self.hkv, self.d, dtype=torch.float32, device=dev)
+            dv = torch.zeros_like(dk)
+            for c in chunks:        # ring order: dQ accumulates over the chunks, dK/dV per chunk
+                desc = L.attn_desc(s, self.hq, self.hkv, self.d, 1.0 / float(np.sqrt(self.d)), chunk_id=c)
+                L.partial_attn_bwd(desc, q, k[c], v[c], d_o, lse, delta, doc_start, lists[c], dq, dk[c], dv[c])
+            out.update(dq=dq.cpu().numpy(), dk=dk.cpu().numpy(), dv=dv.cpu().numpy())
+        torch.cuda.synchronize()
+        return out
+
     # --------------------------------------------------------------- oracle
     def run_oracle(self, rows=None, kv_heads=None, backward=None) -> Dict:
         """The fp64 oracle on this case (backward when the case has one, unless ``backward`` says
@@ -227,6 +272,23 @@ def compare_forward(gpu: Dict, ref: Dict, rows=None) -> Dict[str, float]:
         report["lse_fused"] = max_abs(gpu["lse_fused"][:, sl], ref["lse"])
         assert report["o_fused"] <= O_ATOL, report
         assert report["lse_fused"] <= LSE_ATOL, report
+    return report
+
+
+def compare_tile_list(gpu: Dict, ref: Dict) -> Dict[str, float]:
+    """Per-chunk partials of the tile-list calls and their merge against the oracle (asserts the bars;
+    the -inf rows of every chunk's partial must be the oracle's exactly, and none may be NaN)."""
+    report = {}
+    for step, c in enumerate(ref["chunks"]):
+        lse_g, lse_r = gpu["lse_part"][c], ref["lse_parts"][step]
+        assert not np.isnan(lse_g).any(), "LSE rows of chunk %d not written" % c
+        assert np.array_equal(np.isneginf(lse_g), np.isneginf(lse_r)), "-inf rows differ in chunk %d" % c
+        fin = ~np.isneginf(lse_r)
+        report["lse_part_%d" % c] = max_abs(lse_g[fin], lse_r[fin])
+        report["o_part_%d" % c] = max_abs(gpu["o_part"][c][fin.T], ref["o_parts"][step][fin.T])
+        assert report["lse_part_%d" % c] <= LSE_ATOL and report["o_part_%d" % c] <= O_ATOL, report
+    report["o"], report["lse"] = max_abs(gpu["o"], ref["o"]), max_abs(gpu["lse"], ref["lse"])
+    assert report["o"] <= O_ATOL and report["lse"] <= LSE_ATOL, report
     return report
 
 

@@ -38,7 +38,8 @@ def test_status_strings():
 
 def test_struct_layouts():
     assert ctypes.sizeof(L.ShardDesc) == 32
-    assert ctypes.sizeof(L.AttnDesc) == 48
+    assert ctypes.sizeof(L.AttnDesc) == 56
+    assert L.AttnDesc.chunk_id.offset == 32 and L.AttnDesc.heads_q.offset == 36
 
 
 def _status(fn, *args):
@@ -124,8 +125,39 @@ def test_forward_validates_before_launch(over, code):
     lib = L.lib()
     d = _attn_desc(**over)
     fake = ctypes.c_void_p(4096)     # never dereferenced: validation fails first
-    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
+    st = lib.hsap_partial_attn_fwd_runs(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
     assert st == code, lib.hsap_last_error().decode()
+
+
+def test_tile_list_entry_points_validate_before_launch():
+    # the boundary's tile-list forms: chunk_id, the list length and the outputs are checked first
+    lib = L.lib()
+    fake = ctypes.c_void_p(4096)
+    for over, code in [(dict(chunk_id=2), L.HSAP_ERR_INVALID_ARG), (dict(chunk_id=-1), L.HSAP_ERR_INVALID_ARG),
+                       (dict(head_dim=96), L.HSAP_ERR_UNSUPPORTED), (dict(block_n=32), L.HSAP_ERR_UNSUPPORTED)]:
+        d = _attn_desc(**over)
+        d.chunk_id = over.get("chunk_id", 1)
+        st = lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, 3, fake, fake, None)
+        assert st == code, (over, lib.hsap_last_error().decode())
+        st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, 3, fake, fake,
+                                       fake, None)
+        assert st == code, (over, lib.hsap_last_error().decode())
+    d = _attn_desc()
+    d.chunk_id = 1
+    assert lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, -1, fake, fake, None) == \
+        L.HSAP_ERR_INVALID_ARG
+    assert lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, None, 3, fake, fake, None) == \
+        L.HSAP_ERR_INVALID_ARG                                   # no list
+    assert lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, 3, None, fake, None) == \
+        L.HSAP_ERR_INVALID_ARG                                   # no output
+    assert lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, 0, fake, fake,
+                                     fake, None) == L.HSAP_OK    # an empty list adds nothing
+    # the dK/dV kernel gathers at most 2048 q-tiles per k-tile in LDS
+    big = _attn_desc(total_tokens=2 * 2049 * 64, block_m=64, block_n=64)
+    big.chunk_id = 0
+    st = lib.hsap_partial_attn_bwd(ctypes.byref(big), fake, fake, fake, fake, fake, fake, fake, fake, 3, fake, fake,
+                                   fake, None)
+    assert st == L.HSAP_ERR_UNSUPPORTED and "2048" in lib.hsap_last_error().decode()
 
 
 def test_forward_rejects_256_row_tiles_beyond_packed_descriptors():
@@ -135,7 +167,7 @@ def test_forward_rejects_256_row_tiles_beyond_packed_descriptors():
     lib = L.lib()
     fake = ctypes.c_void_p(4096)
     d = _attn_desc(block_m=256, block_n=128, sp_degree=257, total_tokens=257 * 256)
-    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
+    st = lib.hsap_partial_attn_fwd_runs(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
     assert st == L.HSAP_ERR_UNSUPPORTED, lib.hsap_last_error().decode()
     assert "256" in lib.hsap_last_error().decode()
 
@@ -144,14 +176,14 @@ def test_forward_rejects_null_and_misaligned():
     lib = L.lib()
     d = _attn_desc()
     fake = ctypes.c_void_p(4096)
-    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), None, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
+    st = lib.hsap_partial_attn_fwd_runs(ctypes.byref(d), None, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
     assert st == L.HSAP_ERR_INVALID_ARG
     odd = ctypes.c_void_p(4098)
-    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), odd, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
+    st = lib.hsap_partial_attn_fwd_runs(ctypes.byref(d), odd, fake, fake, fake, fake, fake, 1, fake, fake, 1, None)
     assert st == L.HSAP_ERR_INVALID_ARG
-    st = lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 0, None)
+    st = lib.hsap_partial_attn_fwd_runs(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 1, fake, fake, 0, None)
     assert st == L.HSAP_ERR_INVALID_ARG
-    assert lib.hsap_partial_attn_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 0, fake, fake, 1, None) == 0
+    assert lib.hsap_partial_attn_fwd_runs(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 0, fake, fake, 1, None) == 0
 
 
 def test_fused_forward_validates_before_launch():
@@ -187,15 +219,15 @@ def test_backward_validates_before_launch():
     lib = L.lib()
     fake = ctypes.c_void_p(4096)
     d = _attn_desc(block_m=32, total_tokens=64 * 2, block_n=32)
-    st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
+    st = lib.hsap_partial_attn_bwd_runs(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
                                    fake, 1, fake, fake, fake, None)
     assert st == L.HSAP_ERR_UNSUPPORTED
     d = _attn_desc(head_dim=64, block_n=128)
-    st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
+    st = lib.hsap_partial_attn_bwd_runs(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
                                    fake, 1, fake, fake, fake, None)
     assert st == L.HSAP_ERR_UNSUPPORTED
     d = _attn_desc()
-    st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, None, None, 1, fake,
+    st = lib.hsap_partial_attn_bwd_runs(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, None, None, 1, fake,
                                    fake, 1, fake, fake, fake, None)
     assert st == L.HSAP_ERR_INVALID_ARG
 
@@ -206,7 +238,7 @@ def test_backward_rejects_dq_beyond_packed_descriptors():
     lib = L.lib()
     fake = ctypes.c_void_p(4096)
     d = _attn_desc(sp_degree=260, total_tokens=260 * 128)
-    for fn in (lib.hsap_partial_attn_bwd, lib.hsap_attn_bwd_bf16):
+    for fn in (lib.hsap_partial_attn_bwd_runs, lib.hsap_attn_bwd_bf16):
         st = fn(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 0, fake, fake, 1, fake, fake,
                 fake, None)
         assert st == L.HSAP_ERR_UNSUPPORTED, lib.hsap_last_error().decode()
@@ -218,7 +250,7 @@ def test_backward_shapes_of_256_row_tiles():
     lib = L.lib()
     fake = ctypes.c_void_p(4096)
     d = _attn_desc(block_m=256, head_dim=64, block_n=64, total_tokens=2048)
-    st = lib.hsap_partial_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
+    st = lib.hsap_partial_attn_bwd_runs(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, fake, 1, fake,
                                    fake, 1, fake, fake, fake, None)
     assert st == L.HSAP_ERR_UNSUPPORTED
 

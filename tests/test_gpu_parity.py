@@ -252,7 +252,7 @@ def test_backward_ring_steps_accumulate():
     for chunk in sa.chunks:
         sel = runs_q[runs_q[:, 0] == chunk]
         if len(sel):
-            L.partial_attn_bwd(sa.desc, q, k, v, d_o, fwd["lse"], bwd["delta"], sa.doc_start, None, None, tq,
+            L.partial_attn_bwd_runs(sa.desc, q, k, v, d_o, fwd["lse"], bwd["delta"], sa.doc_start, None, None, tq,
                                torch.from_numpy(np.ascontiguousarray(sel).reshape(-1)).to(dev), bwd["dq_acc"],
                                bwd["dk_acc"], bwd["dv_acc"])
     torch.cuda.synchronize()
@@ -261,3 +261,36 @@ def test_backward_ring_steps_accumulate():
     _say(rep)
     assert rep["dq_vs_onepass"] <= 1e-5 and rep["dq_vs_oracle"] <= 3e-2, rep
 
+
+
+# ---------------------------------------------------------------------------
+# the boundary's tile-list calls (hsap_partial_attn_fwd / _bwd on one chunk's tiles)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case", SMALL_BWD + [SMALL[2], SMALL[4]])
+def test_tile_list_entry_points(case):
+    """hsap_partial_attn_fwd / hsap_partial_attn_bwd called once per ring step with that chunk's
+    tiles from hsap_plan (K/V of the chunk passed alone): each partial, the merge and the gradients
+    against the oracle; the forward partials equal the run-based entry point's bit for bit (the
+    same kernel over the same tiles per q-tile)."""
+    from paper_2606_30460_amd import _lib as L
+    from _harness import compare_tile_list
+    N, P, layout, hq, hkv, d, bm, bn, mean = case
+    rng = np.random.default_rng(N + 11 * P + hq)
+    cu = _rand_cu(rng, N, mean)
+    bwd = (d == 128 or bn == 64) and (bm <= 128 or d == 128)
+    for r in sorted({0, P - 1}):
+        _say("tile lists", case, "shard", r)
+        c = Case(cu, N, P, layout, r, hq, hkv, d, bm, bn, seed=30 + r, backward=bwd)
+        got = c.run_tile_list()
+        ref = c.run_oracle()
+        rep = compare_tile_list(got, ref["fwd"] if bwd else ref)
+        runs = c.run_gpu(max_run_tiles=0)
+        for step, ch in enumerate(got["chunks"]):
+            if got["step_offsets"][step + 1] > got["step_offsets"][step]:
+                fin = ~np.isneginf(runs["lse_part"][ch])
+                assert np.array_equal(got["lse_part"][ch], runs["lse_part"][ch])
+                assert np.array_equal(got["o_part"][ch][fin.T], runs["o_part"][ch][fin.T])
+        if bwd:
+            rep.update(compare_backward(got, ref))
+        _say({k: round(v, 6) for k, v in rep.items() if not k.startswith(("o_part", "lse_part"))})

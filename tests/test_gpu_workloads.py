@@ -130,3 +130,20 @@ def test_workload_backward_long_documents(name):
                dv=rel_max(ex["dv"][:, :, kv], ref["dv"]))
     _say(name, {k: round(v, 6) for k, v in rep.items()}, ex["info"])
     assert max(rep["dq"], rep["dk"], rep["dv"]) <= GRAD_RTOL, rep
+
+
+@pytest.mark.parametrize("name", ["c2", "c5", "c5m"])
+def test_workload_tile_list_entry_points(name):
+    """The boundary's tile-list calls (hsap_partial_attn_fwd / _bwd once per ring step on that chunk's
+    tiles from hsap_plan) on the 32768-token workloads, every row: each chunk's partial, the merge and,
+    for the forward + backward workloads, the gradients against the oracle."""
+    from _harness import compare_tile_list
+    w = make_workload(name)
+    c = Case.from_workload(w)
+    _say("workload", name, "tile-list calls, shard", c.shard)
+    got = c.run_tile_list()
+    ref = c.run_oracle()
+    rep = compare_tile_list(got, ref["fwd"] if c.backward else ref)
+    if c.backward:
+        rep.update(compare_backward(got, ref))
+    _say(name, {k: round(v, 6) for k, v in rep.items() if not k.startswith(("o_part", "lse_part"))})
