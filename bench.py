@@ -445,15 +445,16 @@ def fwd_kernel_name(res) -> str:
     direct-to-LDS for head_dim 128 with 128- or 256-row q-tiles, register-staged otherwise."""
     d, bm, bn = res["head_dim"], res["block_m"], res["block_n"]
     if d == 128 and bm in (128, 256):
-        return "attn_fwd_dl_kernel<%d, %d, false, false>" % (bn, bm // 32)
-    return "attn_fwd_kernel<%d, %d, %d, false, false>" % (d, bn, bm // 32)
+        return "attn_fwd_dl_kernel<%d, %d, false, false, false>" % (bn, bm // 32)
+    return "attn_fwd_kernel<%d, %d, %d, false, false, false>" % (d, bn, bm // 32)
 
 
 def bwd_kernel_names(res) -> list:
     """The two backward kernels the library dispatches for a workload's shapes (bf16 gradients)."""
     d, bm, bn = res["head_dim"], res["block_m"], res["block_n"]
-    return ["attn_bwd_dkdv_kernel<%d, %d, true>" % (d, bn // 32),
-            "attn_bwd_dq_kernel<%d, %d, %d, true>" % (d, bn, bm // 32)]
+    dkdv = ("attn_bwd_dkdv_split_kernel<true>" if d == 128 and bn == 128
+            else "attn_bwd_dkdv_kernel<%d, %d, true, false>" % (d, bn // 32))
+    return [dkdv, "attn_bwd_dq_kernel<%d, %d, %d, true, false>" % (d, bn, bm // 32)]
 
 
 def measured_traffic(workload: str):

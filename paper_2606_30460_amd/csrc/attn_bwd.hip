@@ -344,6 +344,261 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// dK/dV kernel with split roles (head_dim 128, BN = 128): eight waves, two per
+// key block of 32 keys.  Wave kb (0..3) is the block's S wave: it holds the
+// block's K rows as MFMA B operands and its dV accumulators; wave 4 + kb is
+// the dP wave: V rows and dK accumulators.  Per 64-row q sub-tile, in two
+// phases separated by a barrier:
+//   phase 1  S wave:  S = Q K^T, P = exp2(S * scale*log2e - LSE*log2e) on
+//                     allowed pairs; P (fp32) to LDS for its partner
+//            dP wave: dP = dO V^T
+//   phase 2  S wave:  dV += P^T dO             (dO read transposed)
+//            dP wave: P from LDS, dS = P (dP - delta), dK += dS^T Q
+//                     (Q read transposed)
+// Each wave issues 32 MFMAs per sub-tile, half of the one-wave-per-block
+// kernel's 64, and holds half its state (K or V, dK or dV), so two waves fit
+// on a SIMD: one wave's exponentials (or dS arithmetic) run while the other
+// wave's products occupy the matrix core.  S and dP are formed once.
+// Wave w and wave w + 4 share a SIMD (waves are placed round-robin).
+// ---------------------------------------------------------------------------
+template <bool BF16OUT>
+__global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) {
+  constexpr int D = 128, WAVES = 8, KB = 4;  // KB key blocks of 32: BN = 128
+  constexpr int NT = 64 * WAVES;
+  constexpr int SUB = 64;
+  constexpr int CPR = D / 8;
+  constexpr int MB = D / 32;
+  constexpr int PER_T = SUB * CPR / NT;       // 16-byte chunks of Q (and dO) per thread per sub-tile
+  static_assert((SUB * CPR) % NT == 0, "sub-tile must split evenly over the threads");
+  constexpr float LOG2E = 1.44269504088896340736f;
+  __shared__ __attribute__((aligned(16))) __bf16 Qs[2][SUB * D];
+  __shared__ __attribute__((aligned(16))) __bf16 dOs[2][SUB * D];
+  __shared__ __attribute__((aligned(16))) float lse_s[2][SUB];
+  __shared__ __attribute__((aligned(16))) float delta_s[2][SUB];
+  __shared__ __attribute__((aligned(16))) int32_t start_s[2][SUB];
+  // P hand-off, per key block and 32-query block: lane l's 16 values as four 16-byte pieces c at
+  // [c][l] (consecutive lanes at consecutive 16 bytes: no bank conflict)
+  __shared__ __attribute__((aligned(16))) f32x4 Px[KB][SUB / 32][4][64];
+
+  const int tid = threadIdx.x;
+  const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
+  const bool s_wave = w < KB;               // wave-uniform role
+  const int kb = s_wave ? w : w - KB;       // key block
+  const int run_idx = blockIdx.x / a.hkv;
+  const int g = blockIdx.x - run_idx * a.hkv;
+  const hsap_run run = a.runs[run_idx];
+  const int c = a.tiles[run.first].chunk;  // k-major runs are never empty
+  const int count = run.count;
+  const int64_t n = a.geom.n;
+  const int64_t krow0 = (int64_t)run.tile * (32 * KB);
+  const int32_t gk = (int32_t)global_pos(a.geom, c, krow0 + 32 * kb + l32);  // this lane's key position
+  const int64_t kvrow = (int64_t)c * n + krow0;
+
+  // row reads (row 32 qb + l32, chunk 2 kk + hi) and transpose reads of the swizzled tiles, as in
+  // the one-wave-per-block kernel
+  const int tr_row = 4 * hi + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int rowoff[D / 16], troff[MB][2];
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) rowoff[kk] = swz<CPR>(l32, 16 * kk + 8 * hi);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int k = 0; k < 2; ++k) troff[mb][k] = swz<CPR>(8 * k + tr_row, 32 * mb + tr_col) - 8 * k * D;
+
+  // this lane's key row of K (S wave) or V (dP wave) as MFMA B operands
+  bf16x8 kv[D / 16];
+  {
+    const __bf16* src = s_wave ? a.k : a.v;
+    const int64_t off = ((kvrow + 32 * kb + l32) * a.hkv + g) * D + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) kv[kk] = *(const bf16x8*)(src + off + 16 * kk);
+  }
+  f32x16 acc[MB];  // dV (S wave) or dK (dP wave)
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x16{};
+
+  const int nsub = a.bm / SUB;
+  const int per_head = count * nsub;
+  const int total = a.group * per_head;
+  uint32_t win0 = 0u, win1 = 0u;
+  int win_lo = 0, win_hi = -1;
+  auto load_window = [&](int v) {
+    const int i = 64 * v + lane;
+    uint32_t p = 0;
+    if (i < count) {
+      const hsap_tile t = a.tiles[run.first + i];
+      p = (uint32_t)t.q_tile | ((uint32_t)t.kind << 31);
+    }
+    if (v & 1) win1 = p;
+    else win0 = p;
+  };
+  auto ensure_window = [&](int v) {
+    if (v >= win_lo && v <= win_hi) return;
+    load_window(v);
+    if (v == win_hi + 1 && v - 1 >= win_lo) win_lo = v - 1;
+    else win_lo = v;
+    win_hi = v;
+  };
+  auto head_of = [&](int it) { return g * a.group + it / per_head; };
+  auto tile_of = [&](int it) -> uint32_t {
+    const int idx = (it % per_head) / nsub;
+    return __builtin_amdgcn_readlane(((idx >> 6) & 1) ? win1 : win0, idx & 63);
+  };
+  auto q0_of = [&](uint32_t t, int it) {
+    return (int64_t)(t & 0x7FFFFFFFu) * a.bm + ((it % per_head) % nsub) * SUB;
+  };
+  ensure_window(0);
+
+  int32_t soff[PER_T], loff[PER_T];
+#pragma unroll
+  for (int i = 0; i < PER_T; ++i) {
+    const int idx = tid + i * NT, row = idx / CPR, cc = idx % CPR;
+    soff[i] = row * a.hq * D + cc * 8;
+    loff[i] = swz<CPR>(row, cc * 8);
+  }
+  bf16x8 qreg[PER_T], oreg[PER_T];
+  float lreg = 0.f, dreg = 0.f;
+  int32_t sreg = 0;
+  auto load_sub = [&](int it) {
+    const int h = head_of(it);
+    ensure_window(((it % per_head) / nsub) >> 6);
+    const uint32_t t = tile_of(it);
+    const int64_t q0 = q0_of(t, it);
+    const int64_t base = (q0 * a.hq + h) * D;
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      qreg[i] = *(const bf16x8*)(a.q + base + soff[i]);
+      oreg[i] = *(const bf16x8*)(a.d_o + base + soff[i]);
+    }
+    if (tid < SUB) {
+      lreg = a.lse[(int64_t)h * n + q0 + tid];
+      dreg = a.delta[(int64_t)h * n + q0 + tid];
+      sreg = a.doc_start[global_pos(a.geom, a.shard, q0) + tid];
+    }
+  };
+  auto store_sub = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PER_T; ++i) {
+      *(bf16x8*)(&Qs[buf][loff[i]]) = qreg[i];
+      *(bf16x8*)(&dOs[buf][loff[i]]) = oreg[i];
+    }
+    if (tid < SUB) {
+      lse_s[buf][tid] = lreg == -__builtin_inff() ? __builtin_inff() : lreg * LOG2E;  // no key: P = 0
+      delta_s[buf][tid] = dreg;
+      start_s[buf][tid] = sreg;
+    }
+  };
+
+  load_sub(0);
+  store_sub(0);
+  __syncthreads();
+
+  for (int it = 0; it < total; ++it) {
+    const int buf = it & 1;
+    const uint32_t tile = tile_of(it);
+    const int64_t q0 = q0_of(tile, it);
+    const int32_t gq0 = (int32_t)global_pos(a.geom, a.shard, q0);
+    const bool masked = (tile >> 31) != 0;
+    if (it + 1 < total) load_sub(it + 1);
+    // the S wave reads Q rows and dO transposed, the dP wave dO rows and Q transposed
+    const __bf16* R = s_wave ? Qs[buf] : dOs[buf];
+    const __bf16* T = s_wave ? dOs[buf] : Qs[buf];
+
+    // phase 1: S (S wave) or dP (dP wave) for both 32-query blocks
+    f32x16 sp[SUB / 32];
+#pragma unroll
+    for (int qb = 0; qb < SUB / 32; ++qb) {
+      bf16x8 ra[D / 16];
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) ra[kk] = *(const bf16x8*)(R + 32 * qb * D + rowoff[kk]);
+      sp[qb] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) sp[qb] = mfma32(ra[kk], kv[kk], sp[qb]);
+    }
+    bf16x8 opnd[SUB / 32][2];  // phase 2's A operands: P (S wave) or dS (dP wave), bf16
+    if (s_wave) {
+      // P = exp2(S * scale*log2e - LSE*log2e) (register j = 4 grp + e holds query q4 + e,
+      // q4 = 32 qb + 8 grp + 4 hi), masked in one uniform branch; to LDS for the dP wave
+#pragma unroll
+      for (int qb = 0; qb < SUB / 32; ++qb) {
+        float p[16];
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+          const f32x4 l4 = *(const f32x4*)(&lse_s[buf][32 * qb + 8 * grp + 4 * hi]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) p[4 * grp + e] = fast_exp2(__builtin_fmaf(sp[qb][4 * grp + e], a.scale_log2, -l4[e]));
+        }
+        if (masked) {
+#pragma unroll
+          for (int grp = 0; grp < 4; ++grp) {
+            const int q4 = 32 * qb + 8 * grp + 4 * hi;
+            const i32x4 s4 = *(const i32x4*)(&start_s[buf][q4]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if ((uint32_t)(gk - s4[e]) > (uint32_t)(gq0 + q4 + e - s4[e])) p[4 * grp + e] = 0.f;
+          }
+        }
+#pragma unroll
+        for (int cq = 0; cq < 4; ++cq) Px[kb][qb][cq][lane] = f32x4{p[4 * cq], p[4 * cq + 1], p[4 * cq + 2], p[4 * cq + 3]};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) opnd[qb][j >> 3][j & 7] = (__bf16)p[j];
+      }
+    }
+    hsap_lds_barrier();  // P of every key block is in LDS
+
+    // phase 2: dV += P^T dO (S wave) or dS = P (dP - delta), dK += dS^T Q (dP wave)
+#pragma unroll
+    for (int qb = 0; qb < SUB / 32; ++qb) {
+      bf16x8 bt[2][MB];  // transposed reads of dO (S wave) or Q (dP wave), 16 queries per MFMA
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int rb = (32 * qb + 16 * half) * D;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+          bt[half][mb] = cat4(ds_read_tr16(T + rb + troff[mb][0]), ds_read_tr16(T + rb + 8 * D + troff[mb][1]));
+      }
+      if (!s_wave) {
+#pragma unroll
+        for (int cq = 0; cq < 4; ++cq) {
+          const f32x4 p4 = Px[kb][qb][cq][lane];
+          const f32x4 d4 = *(const f32x4*)(&delta_s[buf][32 * qb + 8 * cq + 4 * hi]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int j = 4 * cq + e;
+            opnd[qb][j >> 3][j & 7] = (__bf16)(p4[e] * (sp[qb][j] - d4[e]));
+          }
+        }
+      }
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma32(opnd[qb][half], bt[half][mb], acc[mb]);
+    }
+
+    if (it + 1 < total) store_sub(buf ^ 1);
+    hsap_lds_barrier();  // the next sub-tile is staged; P and this sub-tile's buffers are free
+  }
+
+  // this workgroup owns rows [krow0, krow0 + 128) of chunk c for K/V head g: the S waves write dV,
+  // the dP waves dK (scaled)
+  const float mul = s_wave ? 1.f : a.scale;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int64_t idx = ((kvrow + 32 * kb + c_row(j, hi)) * a.hkv + g) * D + 32 * mb + l32;
+      const float val = acc[mb][j] * mul;
+      if (BF16OUT) {
+        (s_wave ? a.dv16 : a.dk16)[idx] = (__bf16)val;
+      } else {
+        float* dst = s_wave ? a.dv : a.dk;
+        dst[idx] += val;
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // dQ kernel: one workgroup per (q-major run, query head), shaped like the
 // forward.  Wave w owns 32 query rows; in the transposed orientation
 // S^T = K Q^T and dP^T = V dO^T a lane holds one query, so its LSE and delta
@@ -594,6 +849,16 @@ static hsap_status launch_dkdv(const BwdArgs& a, int64_t num_runs, hipStream_t s
   return HSAP_OK;
 }
 
+template <bool BF16OUT>
+static hsap_status launch_dkdv_split(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
+  const int64_t blocks = num_runs * a.hkv;
+  if (blocks > INT32_MAX) HSAP_FAIL(HSAP_ERR_INVALID_ARG, "too many runs x heads");
+  hipLaunchKernelGGL((attn_bwd_dkdv_split_kernel<BF16OUT>), dim3((unsigned)blocks), dim3(512), 0, stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) HSAP_FAIL(HSAP_ERR_HIP, "attn_bwd_dkdv_split launch: %s", hipGetErrorString(e));
+  return HSAP_OK;
+}
+
 template <int D, int BN, int WAVES, bool BF16OUT, bool LIST = false>
 static hsap_status launch_dq(const BwdArgs& a, int64_t num_runs, hipStream_t stream) {
   const int64_t blocks = num_runs * a.hq;
@@ -703,7 +968,7 @@ static hsap_status backward(const hsap_attn_desc* desc, const void* q, const voi
   if (num_runs_k > 0) {
     a.tiles = tiles_k;
     a.runs = runs_k;
-    if (d == 128 && bn == 128) st = launch_dkdv<128, 4, BF16OUT>(a, num_runs_k, s);
+    if (d == 128 && bn == 128) st = launch_dkdv_split<BF16OUT>(a, num_runs_k, s);
     else if (d == 128) st = launch_dkdv<128, 2, BF16OUT>(a, num_runs_k, s);
     else st = launch_dkdv<64, 2, BF16OUT>(a, num_runs_k, s);
     if (st != HSAP_OK) return st;
