@@ -419,8 +419,7 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x16{};
 
   const int nsub = a.bm / SUB;
-  const int per_head = count * nsub;
-  const int total = a.group * per_head;
+  const int total = a.group * count * nsub;
   uint32_t win0 = 0u, win1 = 0u;
   int win_lo = 0, win_hi = -1;
   auto load_window = [&](int v) {
@@ -440,14 +439,25 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
     else win_lo = v;
     win_hi = v;
   };
-  auto head_of = [&](int it) { return g * a.group + it / per_head; };
-  auto tile_of = [&](int it) -> uint32_t {
-    const int idx = (it % per_head) / nsub;
-    return __builtin_amdgcn_readlane(((idx >> 6) & 1) ? win1 : win0, idx & 63);
+  // Sub-tile position as counters (no division in the loop): query head h, tile index idx in the
+  // run, 64-row slice sb of the tile; the next sub-tile's counters advance one step at a time.
+  struct Pos {
+    int h, idx, sb;
   };
-  auto q0_of = [&](uint32_t t, int it) {
-    return (int64_t)(t & 0x7FFFFFFFu) * a.bm + ((it % per_head) % nsub) * SUB;
+  auto advance = [&](Pos p) {
+    if (++p.sb == nsub) {
+      p.sb = 0;
+      if (++p.idx == count) {
+        p.idx = 0;
+        ++p.h;
+      }
+    }
+    return p;
   };
+  auto tile_at = [&](const Pos& p) -> uint32_t {
+    return __builtin_amdgcn_readlane(((p.idx >> 6) & 1) ? win1 : win0, p.idx & 63);
+  };
+  auto q0_at = [&](uint32_t t, const Pos& p) { return (int64_t)(t & 0x7FFFFFFFu) * a.bm + p.sb * SUB; };
   ensure_window(0);
 
   int32_t soff[PER_T], loff[PER_T];
@@ -460,11 +470,11 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   bf16x8 qreg[PER_T], oreg[PER_T];
   float lreg = 0.f, dreg = 0.f;
   int32_t sreg = 0;
-  auto load_sub = [&](int it) {
-    const int h = head_of(it);
-    ensure_window(((it % per_head) / nsub) >> 6);
-    const uint32_t t = tile_of(it);
-    const int64_t q0 = q0_of(t, it);
+  auto load_sub = [&](const Pos& ps) {
+    const int h = g * a.group + ps.h;
+    ensure_window(ps.idx >> 6);
+    const uint32_t t = tile_at(ps);
+    const int64_t q0 = q0_at(t, ps);
     const int64_t base = (q0 * a.hq + h) * D;
 #pragma unroll
     for (int i = 0; i < PER_T; ++i) {
@@ -490,17 +500,19 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
     }
   };
 
-  load_sub(0);
+  Pos pos{0, 0, 0};
+  load_sub(pos);
   store_sub(0);
   __syncthreads();
 
   for (int it = 0; it < total; ++it) {
     const int buf = it & 1;
-    const uint32_t tile = tile_of(it);
-    const int64_t q0 = q0_of(tile, it);
+    const Pos nxt = advance(pos);
+    const uint32_t tile = tile_at(pos);
+    const int64_t q0 = q0_at(tile, pos);
     const int32_t gq0 = (int32_t)global_pos(a.geom, a.shard, q0);
     const bool masked = (tile >> 31) != 0;
-    if (it + 1 < total) load_sub(it + 1);
+    if (it + 1 < total) load_sub(nxt);
     // the S wave reads Q rows and dO transposed, the dP wave dO rows and Q transposed
     const __bf16* R = s_wave ? Qs[buf] : dOs[buf];
     const __bf16* T = s_wave ? dOs[buf] : Qs[buf];
@@ -578,6 +590,7 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
 
     if (it + 1 < total) store_sub(buf ^ 1);
     hsap_lds_barrier();  // the next sub-tile is staged; P and this sub-tile's buffers are free
+    pos = nxt;
   }
 
   // this workgroup owns rows [krow0, krow0 + 128) of chunk c for K/V head g: the S waves write dV,
