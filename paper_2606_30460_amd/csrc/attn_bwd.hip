@@ -355,6 +355,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
 //   phase 2  S wave:  dV += P^T dO             (dO read transposed)
 //            dP wave: P from LDS, dS = P (dP - delta), dK += dS^T Q
 //                     (Q read transposed)
+// The Q and dO rows of the next sub-tile go from global memory straight into
+// LDS (global_load_lds) while the current one is processed.
 // Each wave issues 32 MFMAs per sub-tile, half of the one-wave-per-block
 // kernel's 64, and holds half its state (K or V, dK or dV), so two waves fit
 // on a SIMD: one wave's exponentials (or dS arithmetic) run while the other
@@ -368,8 +370,9 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   constexpr int SUB = 64;
   constexpr int CPR = D / 8;
   constexpr int MB = D / 32;
-  constexpr int PER_T = SUB * CPR / NT;       // 16-byte chunks of Q (and dO) per thread per sub-tile
-  static_assert((SUB * CPR) % NT == 0, "sub-tile must split evenly over the threads");
+  constexpr int WCH = SUB * CPR / WAVES;       // 16-byte chunks of a Q (or dO) sub-tile a wave moves
+  constexpr int U = WCH / 64;                   // transfer instructions per wave per sub-tile and tensor
+  static_assert(WCH % 64 == 0, "a wave moves whole instructions of a sub-tile");
   constexpr float LOG2E = 1.44269504088896340736f;
   __shared__ __attribute__((aligned(16))) __bf16 Qs[2][SUB * D];
   __shared__ __attribute__((aligned(16))) __bf16 dOs[2][SUB * D];
@@ -379,6 +382,7 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   // P hand-off, per key block and 32-query block: lane l's 16 values as four 16-byte pieces c at
   // [c][l] (consecutive lanes at consecutive 16 bytes: no bank conflict)
   __shared__ __attribute__((aligned(16))) f32x4 Px[KB][SUB / 32][4][64];
+  typedef __attribute__((address_space(3))) void* lds_void;
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
@@ -460,27 +464,34 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   auto q0_at = [&](uint32_t t, const Pos& p) { return (int64_t)(t & 0x7FFFFFFFu) * a.bm + p.sb * SUB; };
   ensure_window(0);
 
-  int32_t soff[PER_T], loff[PER_T];
+  // Q and dO sub-tiles by direct-to-LDS transfers: instruction u of wave w fills chunk positions
+  // p = WCH w + 64 u + lane of the swizzled tile; the lane's source is the chunk the swizzle places
+  // there, a 32-bit byte offset from the sub-tile's scalar base (Q and dO rows have the same stride)
+  uint32_t gsrc[U];
 #pragma unroll
-  for (int i = 0; i < PER_T; ++i) {
-    const int idx = tid + i * NT, row = idx / CPR, cc = idx % CPR;
-    soff[i] = row * a.hq * D + cc * 8;
-    loff[i] = swz<CPR>(row, cc * 8);
+  for (int u = 0; u < U; ++u) {
+    const int p = WCH * w + 64 * u + lane, row = p / CPR;
+    gsrc[u] = (uint32_t)((row * a.hq * D + swz_chunk<CPR>(row, p % CPR) * 8) * 2);
   }
-  bf16x8 qreg[PER_T], oreg[PER_T];
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  auto stage = [&](const __bf16* src, __bf16* dst) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(lds_void)dst + (uint32_t)(WCH * wu * 16);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(gsrc[u]), "s"(src), "{m0}"(lds + 64 * 16 * u));
+  };
   float lreg = 0.f, dreg = 0.f;
   int32_t sreg = 0;
-  auto load_sub = [&](const Pos& ps) {
+  // the sub-tile's Q and dO into buffer buf (transfers), its LSE, delta and document starts into
+  // registers of the first 64 threads (written to LDS by store_sub)
+  auto load_sub = [&](const Pos& ps, int buf) {
     const int h = g * a.group + ps.h;
     ensure_window(ps.idx >> 6);
     const uint32_t t = tile_at(ps);
     const int64_t q0 = q0_at(t, ps);
     const int64_t base = (q0 * a.hq + h) * D;
-#pragma unroll
-    for (int i = 0; i < PER_T; ++i) {
-      qreg[i] = *(const bf16x8*)(a.q + base + soff[i]);
-      oreg[i] = *(const bf16x8*)(a.d_o + base + soff[i]);
-    }
+    stage(a.q + base, Qs[buf]);
+    stage(a.d_o + base, dOs[buf]);
     if (tid < SUB) {
       lreg = a.lse[(int64_t)h * n + q0 + tid];
       dreg = a.delta[(int64_t)h * n + q0 + tid];
@@ -488,11 +499,6 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
     }
   };
   auto store_sub = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < PER_T; ++i) {
-      *(bf16x8*)(&Qs[buf][loff[i]]) = qreg[i];
-      *(bf16x8*)(&dOs[buf][loff[i]]) = oreg[i];
-    }
     if (tid < SUB) {
       lse_s[buf][tid] = lreg == -__builtin_inff() ? __builtin_inff() : lreg * LOG2E;  // no key: P = 0
       delta_s[buf][tid] = dreg;
@@ -501,9 +507,15 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   };
 
   Pos pos{0, 0, 0};
-  load_sub(pos);
+  load_sub(pos, 0);
   store_sub(0);
-  __syncthreads();
+  // The compiler does not see the waits inside asm statements: without a use of the K (or V) rows
+  // here it would wait for their loads at their first use inside the loop, in every iteration,
+  // and since the counter also counts the transfers, each iteration would wait for the next
+  // sub-tile before its first product.
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) asm volatile("" ::"v"(kv[kk]));
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   for (int it = 0; it < total; ++it) {
     const int buf = it & 1;
@@ -512,7 +524,7 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
     const int64_t q0 = q0_at(tile, pos);
     const int32_t gq0 = (int32_t)global_pos(a.geom, a.shard, q0);
     const bool masked = (tile >> 31) != 0;
-    if (it + 1 < total) load_sub(nxt);
+    if (it + 1 < total) load_sub(nxt, buf ^ 1);  // buffer buf ^ 1 was last read before the previous barrier
     // the S wave reads Q rows and dO transposed, the dP wave dO rows and Q transposed
     const __bf16* R = s_wave ? Qs[buf] : dOs[buf];
     const __bf16* T = s_wave ? dOs[buf] : Qs[buf];
@@ -589,7 +601,8 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
     }
 
     if (it + 1 < total) store_sub(buf ^ 1);
-    hsap_lds_barrier();  // the next sub-tile is staged; P and this sub-tile's buffers are free
+    // the next sub-tile has landed and is staged; P and this sub-tile's buffers are free
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     pos = nxt;
   }
 
