@@ -17,9 +17,11 @@ Bars: O max-abs <= 2e-2, LSE max-abs <= 1e-3, the set of -inf rows of every
 partial identical, gradients max|g - ref| / max|ref| <= 3e-2; the executor's bf16
 gradients equal the entry points' fp32 gradients rounded to bf16, bit for bit.
 
-For the 131072- and 262144-token workloads the backward (256-row q-tiles) is
-compared with the oracle on two K/V heads (with their query heads) and on every
-row; the other heads are held to the entry-point path bit for bit.
+For the 131072- and 262144-token workloads the backward is compared with the
+oracle on two K/V heads (with their query heads) and on every row, with the
+workloads' 128-row q-tiles and again with 256-row q-tiles (the eight-wave
+forward and dQ kernels); the other heads are held to the entry-point path bit
+for bit.
 """
 import sys
 import time
@@ -80,12 +82,13 @@ def test_workload_forward_every_row(name):
     _say(name, "entry points", {k: round(v, 6) for k, v in rep.items() if not k.startswith(("o_part", "lse_part"))})
 
 
-def _backward_case(name):
+def _backward_case(name, block_m=None):
     w = make_workload(name)
     c = Case.from_workload(w)
-    if not c.backward:      # a forward workload run forward + backward
+    bm = w.block_m if block_m is None else block_m
+    if not c.backward or bm != w.block_m:  # a forward workload run forward + backward, or other q-tiles
         c = Case(w.cu_seqlens, w.total_tokens, w.sp_degree, w.layout, c.shard, w.heads_q, w.heads_kv, w.head_dim,
-                 w.block_m, w.block_n, w.seed, backward=True)
+                 bm, w.block_n, w.seed, backward=True)
     return w, c
 
 
@@ -110,26 +113,32 @@ def test_workload_backward_every_row(name):
 
 @pytest.mark.parametrize("name", ["c3", "c4"])
 def test_workload_backward_long_documents(name):
-    """The 256-row q-tile plans of the long-document workloads, forward + backward from one executor."""
-    w, c = _backward_case(name)
+    """The long-document workloads forward + backward from one executor, with their own q-tiles (128
+    rows) and with 256-row q-tiles; the oracle (independent of the tiling) is computed once."""
+    w = make_workload(name)
     kv = [0, w.heads_kv - 1]
-    hs = c.q_heads(kv)
-    _say("workload", name, "fwd+bwd, shard", c.shard, "oracle on K/V heads", kv)
-    ex = c.run_executor()
-    _no_nan(ex, ("o", "lse", "dq", "dk", "dv"))
-    gpu = c.run_gpu()
-    # every head: the executor's bf16 gradients are the entry points' fp32 ones rounded
-    assert np.array_equal(ex["dq"], gpu["dq_bf16"])
-    assert np.array_equal(ex["dk"], _bf16(gpu["dk"])) and np.array_equal(ex["dv"], _bf16(gpu["dv"]))
-    del gpu
-    t0 = time.perf_counter()
-    ref = c.run_oracle(kv_heads=kv)
-    _say("oracle %.1f s" % (time.perf_counter() - t0))
-    rep = _executor_forward_report(ex, ref["fwd"], heads=hs)
-    rep.update(dq=rel_max(ex["dq"][:, hs], ref["dq"]), dk=rel_max(ex["dk"][:, :, kv], ref["dk"]),
-               dv=rel_max(ex["dv"][:, :, kv], ref["dv"]))
-    _say(name, {k: round(v, 6) for k, v in rep.items()}, ex["info"])
-    assert max(rep["dq"], rep["dk"], rep["dv"]) <= GRAD_RTOL, rep
+    ref = None
+    for bm in (w.block_m, 256):
+        _, c = _backward_case(name, block_m=bm)
+        hs = c.q_heads(kv)
+        _say("workload", name, "fwd+bwd, BM", bm, "shard", c.shard, "oracle on K/V heads", kv)
+        ex = c.run_executor()
+        _no_nan(ex, ("o", "lse", "dq", "dk", "dv"))
+        gpu = c.run_gpu()
+        # every head: the executor's bf16 gradients are the entry points' fp32 ones rounded
+        assert np.array_equal(ex["dq"], gpu["dq_bf16"])
+        assert np.array_equal(ex["dk"], _bf16(gpu["dk"])) and np.array_equal(ex["dv"], _bf16(gpu["dv"]))
+        del gpu
+        if ref is None:
+            t0 = time.perf_counter()
+            ref = c.run_oracle(kv_heads=kv)
+            _say("oracle %.1f s" % (time.perf_counter() - t0))
+        rep = _executor_forward_report(ex, ref["fwd"], heads=hs)
+        rep.update(dq=rel_max(ex["dq"][:, hs], ref["dq"]), dk=rel_max(ex["dk"][:, :, kv], ref["dk"]),
+                   dv=rel_max(ex["dv"][:, :, kv], ref["dv"]))
+        _say(name, "BM", bm, {k: round(v, 6) for k, v in rep.items()}, ex["info"])
+        assert max(rep["dq"], rep["dk"], rep["dv"]) <= GRAD_RTOL, rep
+        del ex
 
 
 @pytest.mark.parametrize("name", ["c2", "c5", "c5m"])

@@ -210,13 +210,13 @@ def _c2(seed: int) -> Workload:
 def _c3(seed: int) -> Workload:
     return Workload("c3_n128k_mixed_gqa32x8_d128_sp16_zigzag", 131072,
                     doc_lengths_mixed(131072, 0.1, (64, 512), (8192, 65536), seed), 32, 8, 128,
-                    16, "zigzag", None, 256, 128, False, seed)
+                    16, "zigzag", None, 128, 128, False, seed)
 
 
 def _c4(seed: int) -> Workload:
     return Workload("c4_n256k_pareto_h8of32_d128_ring8", 262144,
                     doc_lengths_pareto(262144, 1.2, 32, 131072, seed), 8, 8, 128,
-                    8, "contiguous", None, 256, 128, False, seed)
+                    8, "contiguous", None, 128, 128, False, seed)
 
 
 def _c5(seed: int) -> Workload:
