@@ -154,8 +154,8 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
-  const int run_idx = blockIdx.x / a.hq;  // runs are longest first: long work starts first
-  const int h = blockIdx.x - run_idx * a.hq;
+  int run_idx, h;  // runs are longest first: long work starts first
+  run_and_head(blockIdx.x, a.hq, a.hkv, run_idx, h);
   // LIST: the tile-list mode of the partial forward, this workgroup's q-tile found in one chunk's list
   const hsap_run run = LIST ? q_tile_run(a.tiles, a.num_tiles, run_idx, lane) : a.runs[run_idx];
   const int slot = run.slot;  // partial-output slot of this run (partial forward)
@@ -458,8 +458,8 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
-  const int run_idx = blockIdx.x / a.hq;
-  const int h = blockIdx.x - run_idx * a.hq;
+  int run_idx, h;
+  run_and_head(blockIdx.x, a.hq, a.hkv, run_idx, h);
   // LIST: the tile-list mode of the partial forward, this workgroup's q-tile found in one chunk's list
   const hsap_run run = LIST ? q_tile_run(a.tiles, a.num_tiles, run_idx, lane) : a.runs[run_idx];
   const int slot = run.slot;

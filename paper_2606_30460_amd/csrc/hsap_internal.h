@@ -93,6 +93,27 @@ __device__ inline int32_t lower_bound_q_tile(const hsap_tile* tiles, int32_t num
   return lo + __popcll(__builtin_amdgcn_ballot_w64(below));
 }
 
+// Workgroup bid of a (run, query head) grid -> its run and query head.  Workgroups are dispatched
+// to the eight XCDs round-robin (workgroup i on XCD i % 8), and each XCD has its own L2.  When the
+// K/V heads split evenly over the XCDs, the query heads that read one K/V head are placed on one
+// XCD (K/V head g on XCD g % 8), so the K/V tiles they share are fetched into one L2 instead of
+// `group` of them.  Runs keep their order (longest first) on every XCD.  Without grouped heads
+// (hq == hkv) this is the plain run-major order, head fastest.
+__device__ inline void run_and_head(int bid, int hq, int hkv, int& run, int& h) {
+  if (hkv % 8 == 0 && hq != hkv) {
+    const int per = hq >> 3;  // query heads per XCD
+    const int group = hq / hkv;
+    const int x = bid & 7, y = bid >> 3;
+    run = y / per;
+    const int lh = y - run * per;  // the XCD's lh-th query head: K/V head 8 j + x, member i
+    const int j = lh / group, i = lh - j * group;
+    h = (8 * j + x) * group + i;
+  } else {
+    run = bid / hq;
+    h = bid - run * hq;
+  }
+}
+
 // The run of q-tile qt in a sorted tile list: {slot 0, qt, first, count}.
 __device__ inline hsap_run q_tile_run(const hsap_tile* tiles, int32_t num, int32_t qt, int lane) {
   const int32_t first = lower_bound_q_tile(tiles, num, qt, lane);
