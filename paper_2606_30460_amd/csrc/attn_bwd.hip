@@ -347,16 +347,16 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attn_bwd_dkdv_kernel(BwdArgs a)
 // dK/dV kernel with split roles (head_dim 128, BN = 128): eight waves, two per
 // key block of 32 keys.  Wave kb (0..3) is the block's S wave: it holds the
 // block's K rows as MFMA B operands and its dV accumulators; wave 4 + kb is
-// the dP wave: V rows and dK accumulators.  Per 64-row q sub-tile, in two
-// phases separated by a barrier:
-//   phase 1  S wave:  S = Q K^T, P = exp2(S * scale*log2e - LSE*log2e) on
-//                     allowed pairs; P (fp32) to LDS for its partner
-//            dP wave: dP = dO V^T
-//   phase 2  S wave:  dV += P^T dO             (dO read transposed)
-//            dP wave: P from LDS, dS = P (dP - delta), dK += dS^T Q
-//                     (Q read transposed)
-// The Q and dO rows of the next sub-tile go from global memory straight into
-// LDS (global_load_lds) while the current one is processed.
+// the dP wave: V rows and dK accumulators.  Per 64-row q sub-tile:
+//   scores    S wave:  S = Q K^T, P = exp2(S * scale*log2e - LSE*log2e) on
+//                      allowed pairs; P (fp16) to LDS for its partner
+//             dP wave: dP = dO V^T
+//   products  S wave:  dV += P^T dO             (dO read transposed)
+//             dP wave: P from LDS, dS = P (dP - delta), dK += dS^T Q
+//                      (Q read transposed)
+// software-pipelined by one sub-tile: iteration t runs the products of t and
+// the scores of t + 1, with one barrier, while the Q and dO rows of t + 2 go
+// from global memory straight into LDS (global_load_lds).
 // Each wave issues 32 MFMAs per sub-tile, half of the one-wave-per-block
 // kernel's 64, and holds half its state (K or V, dK or dV), so two waves fit
 // on a SIMD: one wave's exponentials (or dS arithmetic) run while the other
@@ -374,14 +374,16 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   constexpr int U = WCH / 64;                   // transfer instructions per wave per sub-tile and tensor
   static_assert(WCH % 64 == 0, "a wave moves whole instructions of a sub-tile");
   constexpr float LOG2E = 1.44269504088896340736f;
-  __shared__ __attribute__((aligned(16))) __bf16 Qs[2][SUB * D];
-  __shared__ __attribute__((aligned(16))) __bf16 dOs[2][SUB * D];
-  __shared__ __attribute__((aligned(16))) float lse_s[2][SUB];
-  __shared__ __attribute__((aligned(16))) float delta_s[2][SUB];
-  __shared__ __attribute__((aligned(16))) int32_t start_s[2][SUB];
-  // P hand-off, per key block and 32-query block: lane l's 16 values as four 16-byte pieces c at
-  // [c][l] (consecutive lanes at consecutive 16 bytes: no bank conflict)
-  __shared__ __attribute__((aligned(16))) f32x4 Px[KB][SUB / 32][4][64];
+  // a ring of three sub-tiles: t (gradient products), t + 1 (scores), t + 2 (in flight)
+  __shared__ __attribute__((aligned(16))) __bf16 Qs[3][SUB * D];
+  __shared__ __attribute__((aligned(16))) __bf16 dOs[3][SUB * D];
+  __shared__ __attribute__((aligned(16))) float lse_s[3][SUB];
+  __shared__ __attribute__((aligned(16))) float delta_s[3][SUB];
+  __shared__ __attribute__((aligned(16))) int32_t start_s[3][SUB];
+  // P hand-off in fp16 (two buffers: P of sub-tile t + 1 is written while the dP wave reads P of
+  // t), per key block and 32-query block: lane l's 16 values as two 16-byte pieces at [half][l]
+  // (consecutive lanes at consecutive 16 bytes: no bank conflict)
+  __shared__ __attribute__((aligned(16))) h16x8 Px[2][KB][SUB / 32][2][64];
   typedef __attribute__((address_space(3))) void* lds_void;
 
   const int tid = threadIdx.x;
@@ -506,31 +508,14 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
     }
   };
 
-  Pos pos{0, 0, 0};
-  load_sub(pos, 0);
-  store_sub(0);
-  // The compiler does not see the waits inside asm statements: without a use of the K (or V) rows
-  // here it would wait for their loads at their first use inside the loop, in every iteration,
-  // and since the counter also counts the transfers, each iteration would wait for the next
-  // sub-tile before its first product.
-#pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) asm volatile("" ::"v"(kv[kk]));
-  asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-
-  for (int it = 0; it < total; ++it) {
-    const int buf = it & 1;
-    const Pos nxt = advance(pos);
-    const uint32_t tile = tile_at(pos);
-    const int64_t q0 = q0_at(tile, pos);
-    const int32_t gq0 = (int32_t)global_pos(a.geom, a.shard, q0);
-    const bool masked = (tile >> 31) != 0;
-    if (it + 1 < total) load_sub(nxt, buf ^ 1);  // buffer buf ^ 1 was last read before the previous barrier
-    // the S wave reads Q rows and dO transposed, the dP wave dO rows and Q transposed
-    const __bf16* R = s_wave ? Qs[buf] : dOs[buf];
-    const __bf16* T = s_wave ? dOs[buf] : Qs[buf];
-
-    // phase 1: S (S wave) or dP (dP wave) for both 32-query blocks
-    f32x16 sp[SUB / 32];
+  // Scores of a sub-tile from its rows (buffer rb): S = Q K^T (S wave) or dP = dO V^T (dP wave)
+  // into sp; the S wave turns them into P (register j = 4 grp + e holds query q4 + e,
+  // q4 = 32 qb + 8 grp + 4 hi; P = exp2(S * scale*log2e - LSE*log2e), masked in one uniform
+  // branch), kept in bf16 as its own next A operand and handed to the dP wave in fp16.
+  f32x16 sp[SUB / 32];
+  bf16x8 opnd[SUB / 32][2];  // A operands of the gradient products: P (S wave) or dS (dP wave)
+  auto scores = [&](int rb, int pbuf, bool masked, int32_t gq0) {
+    const __bf16* R = s_wave ? Qs[rb] : dOs[rb];
 #pragma unroll
     for (int qb = 0; qb < SUB / 32; ++qb) {
       bf16x8 ra[D / 16];
@@ -540,16 +525,13 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) sp[qb] = mfma32(ra[kk], kv[kk], sp[qb]);
     }
-    bf16x8 opnd[SUB / 32][2];  // phase 2's A operands: P (S wave) or dS (dP wave), bf16
     if (s_wave) {
-      // P = exp2(S * scale*log2e - LSE*log2e) (register j = 4 grp + e holds query q4 + e,
-      // q4 = 32 qb + 8 grp + 4 hi), masked in one uniform branch; to LDS for the dP wave
 #pragma unroll
       for (int qb = 0; qb < SUB / 32; ++qb) {
         float p[16];
 #pragma unroll
         for (int grp = 0; grp < 4; ++grp) {
-          const f32x4 l4 = *(const f32x4*)(&lse_s[buf][32 * qb + 8 * grp + 4 * hi]);
+          const f32x4 l4 = *(const f32x4*)(&lse_s[rb][32 * qb + 8 * grp + 4 * hi]);
 #pragma unroll
           for (int e = 0; e < 4; ++e) p[4 * grp + e] = fast_exp2(__builtin_fmaf(sp[qb][4 * grp + e], a.scale_log2, -l4[e]));
         }
@@ -557,24 +539,35 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
 #pragma unroll
           for (int grp = 0; grp < 4; ++grp) {
             const int q4 = 32 * qb + 8 * grp + 4 * hi;
-            const i32x4 s4 = *(const i32x4*)(&start_s[buf][q4]);
+            const i32x4 s4 = *(const i32x4*)(&start_s[rb][q4]);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
               if ((uint32_t)(gk - s4[e]) > (uint32_t)(gq0 + q4 + e - s4[e])) p[4 * grp + e] = 0.f;
           }
         }
 #pragma unroll
-        for (int cq = 0; cq < 4; ++cq) Px[kb][qb][cq][lane] = f32x4{p[4 * cq], p[4 * cq + 1], p[4 * cq + 2], p[4 * cq + 3]};
+        for (int half = 0; half < 2; ++half) {
+          h16x8 ph;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const auto pk = __builtin_amdgcn_cvt_pkrtz(p[8 * half + 2 * i], p[8 * half + 2 * i + 1]);
+            ph[2 * i] = pk[0];
+            ph[2 * i + 1] = pk[1];
+          }
+          Px[pbuf][kb][qb][half][lane] = ph;
+        }
 #pragma unroll
         for (int j = 0; j < 16; ++j) opnd[qb][j >> 3][j & 7] = (__bf16)p[j];
       }
     }
-    hsap_lds_barrier();  // P of every key block is in LDS
-
-    // phase 2: dV += P^T dO (S wave) or dS = P (dP - delta), dK += dS^T Q (dP wave)
+  };
+  // Gradient products of a sub-tile (buffer tb): dV += P^T dO (S wave, dO read transposed) or
+  // dS = P (dP - delta), dK += dS^T Q (dP wave, P from the hand-off, Q read transposed)
+  auto products = [&](int tb, int pbuf) {
+    const __bf16* T = s_wave ? dOs[tb] : Qs[tb];
 #pragma unroll
     for (int qb = 0; qb < SUB / 32; ++qb) {
-      bf16x8 bt[2][MB];  // transposed reads of dO (S wave) or Q (dP wave), 16 queries per MFMA
+      bf16x8 bt[2][MB];  // 16 queries per MFMA
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         const int rb = (32 * qb + 16 * half) * D;
@@ -583,14 +576,14 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
           bt[half][mb] = cat4(ds_read_tr16(T + rb + troff[mb][0]), ds_read_tr16(T + rb + 8 * D + troff[mb][1]));
       }
       if (!s_wave) {
+        const h16x8 ph[2] = {Px[pbuf][kb][qb][0][lane], Px[pbuf][kb][qb][1][lane]};
 #pragma unroll
         for (int cq = 0; cq < 4; ++cq) {
-          const f32x4 p4 = Px[kb][qb][cq][lane];
-          const f32x4 d4 = *(const f32x4*)(&delta_s[buf][32 * qb + 8 * cq + 4 * hi]);
+          const f32x4 d4 = *(const f32x4*)(&delta_s[tb][32 * qb + 8 * cq + 4 * hi]);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int j = 4 * cq + e;
-            opnd[qb][j >> 3][j & 7] = (__bf16)(p4[e] * (sp[qb][j] - d4[e]));
+            opnd[qb][j >> 3][j & 7] = (__bf16)((float)ph[j >> 3][j & 7] * (sp[qb][j] - d4[e]));
           }
         }
       }
@@ -599,11 +592,54 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma32(opnd[qb][half], bt[half][mb], acc[mb]);
     }
+  };
+  auto sub_mask = [&](const Pos& p, bool& masked, int32_t& gq0) {
+    const uint32_t t = tile_at(p);
+    masked = (t >> 31) != 0;
+    gq0 = (int32_t)global_pos(a.geom, a.shard, q0_at(t, p));
+  };
 
-    if (it + 1 < total) store_sub(buf ^ 1);
-    // the next sub-tile has landed and is staged; P and this sub-tile's buffers are free
+  // prologue: sub-tiles 0 and 1 staged, the scores of sub-tile 0
+  Pos cur{0, 0, 0};
+  Pos nx1 = advance(cur);
+  bool m0;
+  int32_t g0;
+  sub_mask(cur, m0, g0);
+  load_sub(cur, 0);
+  store_sub(0);
+  if (total > 1) {
+    load_sub(nx1, 1);
+    store_sub(1);
+  }
+  // The compiler does not see the waits inside asm statements: without a use of the K (or V) rows
+  // here it would wait for their loads at their first use inside the loop, in every iteration,
+  // and since the counter also counts the transfers, each iteration would wait for the next
+  // sub-tiles before its first product.
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) asm volatile("" ::"v"(kv[kk]));
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  scores(0, 0, m0, g0);
+  hsap_lds_barrier();  // P of sub-tile 0 is in LDS
+
+  // Iteration t: the gradient products of sub-tile t, then the scores of sub-tile t + 1, while
+  // sub-tile t + 2 is moved into the third buffer; one barrier.  Both waves of a SIMD start with
+  // independent work (the S wave's products on P it holds, the dP wave's dS arithmetic) and the S
+  // wave's exponentials follow its score products while the dP wave's products run.
+  int b0 = 0;  // t % 3
+  for (int t = 0; t < total; ++t) {
+    const int b1 = b0 == 2 ? 0 : b0 + 1, b2 = b1 == 2 ? 0 : b1 + 1;
+    const Pos nx2 = advance(nx1);
+    bool m1 = false;
+    int32_t g1 = 0;
+    if (t + 1 < total) sub_mask(nx1, m1, g1);  // before the window of t + 2 may replace it
+    if (t + 2 < total) load_sub(nx2, b2);       // buffer b2 was last read before the previous barrier
+    products(b0, t & 1);
+    if (t + 1 < total) scores(b1, (t + 1) & 1, m1, g1);
+    if (t + 2 < total) store_sub(b2);
+    // sub-tile t + 2 has landed and is staged; P of t + 1 is in LDS; buffer b0 is free
     asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    pos = nxt;
+    nx1 = nx2;
+    b0 = b1;
   }
 
   // this workgroup owns rows [krow0, krow0 + 128) of chunk c for K/V head g: the S waves write dV,
