@@ -710,15 +710,15 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
         }
     }
     // K(s + 2) and V(s + 1) must have landed before the next step.  Three slots: they were
-    // issued one step ago, and this step's own transfers (U instructions each) stay in flight.
-    // Two slots: they are this step's transfers.
+    // issued one step ago, and this step's own transfers (UK instructions for K, U for V) stay in
+    // flight.  Two slots: they are this step's transfers.
     if constexpr (NSLOT == 3) {
-      static_assert(U == 2, "the waits below count two instructions per tile");
-      if (ldk && ldv) asm volatile("s_waitcnt vmcnt(4)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      else if (ldk || ldv) asm volatile("s_waitcnt vmcnt(2)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      else asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      if (ldk && ldv) vm_wait_barrier<UK + U>();
+      else if (ldk) vm_wait_barrier<UK>();
+      else if (ldv) vm_wait_barrier<U>();
+      else vm_wait_barrier<0>();
     } else {
-      asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      vm_wait_barrier<0>();
     }
     sk = s1;
   };

@@ -66,6 +66,15 @@ __device__ __forceinline__ void hsap_lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Wait until at most N of this wave's vector-memory operations are in flight (they complete in
+// issue order) and all its LDS operations are done, then the workgroup barrier.  Used by the
+// direct-to-LDS rings: the transfers a step may leave in flight are its own, the youngest.
+template <int N>
+__device__ __forceinline__ void vm_wait_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a six-bit count");
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
 // Unpadded LDS tiles of CPR 16-byte chunks per row (CPR = 16: 128 bf16 per
 // row; CPR = 8: 64 bf16) store chunk c of row r at chunk c ^ f(r).  f is
 // chosen so that both access patterns of the attention kernels hit 16
