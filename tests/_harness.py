@@ -189,13 +189,17 @@ class Case:
 
 
 def _oracle_workers() -> int:
-    return max(1, len(os.sched_getaffinity(0)) // 2)
+    return max(1, len(os.sched_getaffinity(0)))
 
 
 def oracle_by_kv_heads(q, k, v, do, cu, N, P, layout, shard, kv_heads, rows=None) -> Dict:
     """oracle.shard_forward (do is None) or oracle.shard_backward for the given K/V heads and the
-    query heads that read them, one K/V head per task on a pool of host threads with two BLAS
-    threads each; results are concatenated along the head axes in the order of ``kv_heads``."""
+    query heads that read them, one K/V head per task on a pool of host threads, each calling a
+    single-threaded BLAS; results are concatenated along the head axes in the order of ``kv_heads``.
+
+    The BLAS runs single-threaded because its own thread pool is shared by every caller thread:
+    OpenBLAS documents that a program which is itself multi-threaded must set it to one thread,
+    since concurrent calls into its threaded kernels conflict."""
     hq, hkv = q.shape[1], k.shape[1]
     group = hq // hkv
 
@@ -207,7 +211,7 @@ def oracle_by_kv_heads(q, k, v, do, cu, N, P, layout, shard, kv_heads, rows=None
             raise ValueError("the backward is computed over every row")
         return oracle.shard_backward(q[:, hs], k[:, g:g + 1], v[:, g:g + 1], do[:, hs], cu, N, P, layout, shard)
 
-    with threadpool_limits(limits=2):
+    with threadpool_limits(limits=1):
         with concurrent.futures.ThreadPoolExecutor(min(_oracle_workers(), len(kv_heads))) as pool:
             parts = list(pool.map(one, kv_heads))
 
