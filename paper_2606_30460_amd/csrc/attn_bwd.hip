@@ -6,19 +6,24 @@
 // forward and backward.  Two kernels share the work, so that neither needs
 // atomics per k-tile:
 //
-// dK/dV kernel: one workgroup per (k-major run, K/V head).  A run is one
-// (chunk, k-tile) with the q-tiles listed against it.  The workgroup has
-// WAVES waves; wave w owns 32 keys (BN = 32 * WAVES) and keeps their K and V
-// rows (as MFMA B operands) and their dK, dV accumulators in registers for
-// the whole run, looping over the query heads of its K/V head group and over
-// the listed q-tiles in sub-tiles of 64 rows.  Per block of 32 queries:
+// dK/dV kernels: one workgroup per (k-major run, K/V head).  A run is one
+// (chunk, k-tile) with the q-tiles listed against it; the workgroup keeps the
+// k-tile's K and V rows (as MFMA B operands) and its dK, dV accumulators in
+// registers for the whole run, looping over the query heads of its K/V head
+// group and over the listed q-tiles in sub-tiles of 64 rows.  Per sub-tile:
 //   S  = Q K^T, dP = dO V^T           (lane = key, registers = queries)
 //   P  = exp2(S * scale*log2e - LSE*log2e) on allowed pairs, dS = P (dP - delta)
 //   dV += P^T dO, dK += dS^T Q        (A operands from registers; dO and Q
 //                                      read transposed from LDS)
-// Q and dO sub-tiles are double buffered in LDS (swizzled, see mfma.h) with
-// the next sub-tile's rows loading into registers while the current one
-// computes.  Each (chunk, k-tile, K/V head) block of dK/dV has one owner.
+// For head_dim 128 with 128-key tiles (every benchmark workload) the split
+// kernel gives each 32-key block to two waves on one SIMD, one forming S, P
+// and dV, the other dP, dS and dK (P handed over through LDS); otherwise one
+// wave owns 32 keys and does all four products.  Q and dO sub-tiles sit in
+// XOR-swizzled LDS tiles (mfma.h).  Each (chunk, k-tile, K/V head) block of
+// dK/dV has one owner.
+//
+// dQ kernel: one workgroup per (q-major run, query head), shaped like the
+// forward; it forms S and dP again for its own pairs (described below).
 //
 #include <type_traits>
 
