@@ -2,12 +2,13 @@
 
 Each workload runs twice on the GPU on the same seeded inputs:
 
-* through the step executor exactly as the benchmark times it (one hsap_executor
-  with the benchmark's options: host plan and one upload, document starts found in
-  cu_seqlens, the partial forward with final-slot writes of single-part q-tiles,
-  the merge of the listed q-tiles, the fused forward, the two-stage form of the
-  forward, and for the forward+backward workloads the backward with delta folded
-  into the dQ kernel and bf16 gradients);
+* through the step executor as the benchmark times it (host plan and one upload,
+  document starts found in cu_seqlens, the partial forward with final-slot writes
+  of single-part q-tiles, the merge of the listed q-tiles, the two-stage form of
+  the forward, and for the forward+backward workloads the backward with delta
+  folded into the dQ kernel and bf16 gradients), plus the fused forward from the
+  same plan (the benchmark times it with an executor of its own; its lists are
+  the same);
 * through the entry points one by one (per-position document starts, every
   partial slot kept, fp32 gradient accumulators), whose partials are compared
   chunk by chunk.
