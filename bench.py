@@ -432,7 +432,7 @@ def fp8_analysis(name: str, reps: int = 50) -> dict:
 
 
 FWD_SOURCES = ("paper_2606_30460_amd/csrc/attn_fwd.hip", "paper_2606_30460_amd/csrc/mfma.h",
-               "paper_2606_30460_amd/csrc/hsap_internal.h")
+               "paper_2606_30460_amd/csrc/hsap_internal.h", "paper_2606_30460_amd/build.py")
 TRAFFIC_GLOB = "profiles/attn_fwd_hbm_traffic*.md"
 
 

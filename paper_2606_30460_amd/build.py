@@ -31,6 +31,10 @@ HIP_FLAGS = [
     "-Wall", "-Wno-unused-function",
 ]
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall"]
+# Per-source additions.  The forward kernels never see a NaN (finite bf16 inputs; masked scores are
+# -inf, which stays honoured): without NaN semantics the compiler drops the canonicalising maxes
+# around the row maximum (5 VALU instructions per 64-key step; c4 forward +0.6-0.8 % on one box).
+EXTRA_FLAGS = {"attn_fwd.hip": ["-fno-honor-nans"]}
 
 
 def _hipcc() -> str:
@@ -43,7 +47,7 @@ def _hipcc() -> str:
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
     if src.endswith(".hip"):
-        cmd = [_hipcc(), *HIP_FLAGS, "-c", src, "-o", obj]
+        cmd = [_hipcc(), *HIP_FLAGS, *EXTRA_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     else:
         cmd = [shutil.which("g++") or "g++", *CXX_FLAGS, "-I/opt/rocm/include", "-c", src, "-o", obj]
     proc = subprocess.run(cmd, capture_output=True, text=True)
