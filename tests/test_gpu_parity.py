@@ -47,6 +47,10 @@ SMALL = [
     (3072, 3, "contiguous", 6, 3, 64, 128, 64, 3000),
     (4096, 2, "zigzag", 4, 2, 128, 256, 128, 700),
     (4096, 4, "contiguous", 2, 2, 128, 256, 64, 300),
+    # K/V heads a multiple of 8 with grouped query heads: the query heads of one K/V head are
+    # placed on one XCD (groups of 2 and 8)
+    (2048, 2, "zigzag", 16, 8, 128, 128, 128, 400),
+    (2048, 2, "contiguous", 64, 8, 128, 128, 64, 250),
 ]
 
 
@@ -210,6 +214,8 @@ SMALL_BWD = [
     # 256-row q-tiles (eight-wave dQ kernel, four 64-row sub-tiles per tile in dK/dV), GQA
     (4096, 2, "zigzag", 4, 2, 128, 256, 128, 700),
     (8192, 4, "contiguous", 8, 2, 128, 256, 64, 40),
+    # K/V heads a multiple of 8 with grouped query heads (the dQ kernel's XCD placement)
+    (2048, 2, "contiguous", 16, 8, 128, 128, 128, 300),
 ]
 
 
