@@ -434,6 +434,16 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_kernel(FwdArgs a) {
 // V one, so a transfer has one step.  Each wave moves 1024 / WAVES of a tile's
 // 1024 16-byte chunks, 64 per instruction; a lane's source chunk is the one
 // the swizzle places at its destination.
+//
+// Order of a step: the step's transfers; the mask (MASKED tiles only), the
+// row maximum and the rare rescale of O; then one straight-line block with
+// the exponentials and PV of this step and the score products of the next,
+// so that a wave's own vector work fills the shadow of its matrix products
+// (scheduling-group barriers ask for that interleave).  The wave raises its
+// priority for the block, so the SIMD's other wave (another workgroup) runs
+// its transfers and row maximum meanwhile.  Every step forms the next
+// step's scores; the last step's read a slot that no transfer is writing and
+// are dropped.
 // ---------------------------------------------------------------------------
 // FP8: Q and K are e4m3 codes (scores from the 32x32x64 fp8 MFMA times q_scale[h] *
 // k_scale[chunk, g]); K tiles are [64][128 bytes], swizzled over their 8 chunks per row.
@@ -631,9 +641,27 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
   const uint32_t span = (uint32_t)(gq - qstart);
 
   int sk = 0;  // s % NSLOT
-  // one 64-key step (softmax and PV of step s from `sc`, scores of step s + 1 into `sn`), run twice
-  // per loop iteration with the score arrays swapped
-  // (`par` is s % 2 as a compile-time constant: with two slots every slot index is one)
+  // Instruction order asked of the compiler for the block of a step (bf16 scores): four K-operand
+  // reads ahead, then per score MFMA one LDS read and four vector instructions (the exponentials,
+  // sums and conversions of this step), then per PV MFMA two V^T reads and three vector ones.
+  auto block_order = []() __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x406, 4, 0);  // VALU, SALU, transcendental
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x406, 3, 0);
+    }
+  };
+  // one 64-key step: softmax and PV of step s from `sc`, scores of step s + 1 into `sn` (run twice
+  // per loop iteration with the score arrays swapped; `par` is s % 2 as a compile-time constant:
+  // with two slots every slot index is one)
   auto step = [&](int s, auto par, f32x16 (&sc)[KB / 32], f32x16 (&sn)[KB / 32]) __attribute__((always_inline)) {
     constexpr int PAR = decltype(par)::value;
     // the window of tile (s + NSLOT) / SUBS is needed now (rare vector load: every 64 tiles)
@@ -648,7 +676,6 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
     const bool ldk = s + NSLOT < total, ldv = s + NSLOT - 1 < total;
     if (ldk) stage_k(kbase + step_off(tile_at(s + NSLOT), s + NSLOT), Ks[s0]);
     if (ldv) stage(a.v + step_off(tile_at(s + NSLOT - 1), s + NSLOT - 1), Vs[sv]);
-    if (s + 1 < total) scores(Ks[s1], sn);
 
     // Masked tile: a step whose keys no query of the wave may see is skipped (all its
     // probabilities would be 0: the running max, sum and O stay as they are), and one whose keys
@@ -669,6 +696,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
             if ((uint32_t)(rel0 + (32 * nb + c_row(j, 0))) > span) sc[nb][j] = NEG_INF;
       }
     }
+    float m_use = 0.f;
     if (live) {
       float mx = sc[0][0];
 #pragma unroll
@@ -683,17 +711,35 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
         for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
         m_run = m_new;
       }
-      const float m_use = m_run == NEG_INF ? 0.f : m_run;
+      m_use = m_run == NEG_INF ? 0.f : m_run;
+    }
+
+    if (live) {
+      // the block: exponentials of this step (each 32-key half followed in the source by that
+      // half's next-step score products, so nothing common is left to hoist above the branch),
+      // then PV of this step
+      __builtin_amdgcn_s_setprio(1);
       float rs = 0.f;
       bf16x8 pb[KB / 32][2];
 #pragma unroll
-      for (int nb = 0; nb < KB / 32; ++nb)
+      for (int nb = 0; nb < KB / 32; ++nb) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const float p = fast_exp2(__builtin_fmaf(sc[nb][j], sl, -m_use));
           rs += p;
           pb[nb][j >> 3][j & 7] = (__bf16)p;
         }
+        if constexpr (FP8) {
+          if (nb == 0) scores(Ks[s1], sn);
+        } else {
+          bf16x8 kf[D / 16];
+#pragma unroll
+          for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(const bf16x8*)(Ks[s1] + 32 * nb * D + rowoff[kk]);
+          sn[nb] = f32x16{};
+#pragma unroll
+          for (int kk = 0; kk < D / 16; ++kk) sn[nb] = mfma32(kf[kk], qf[kk], sn[nb]);
+        }
+      }
       l_run += rs;
 
       const __bf16* V = Vs[s0];
@@ -708,6 +754,10 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_fwd_dl_kernel(FwdArgs a) {
             o[mb] = mfma32(av, pb[nb][half], o[mb]);
           }
         }
+      if constexpr (!FP8) block_order();
+      __builtin_amdgcn_s_setprio(0);
+    } else {
+      scores(Ks[s1], sn);
     }
     // K(s + 2) and V(s + 1) must have landed before the next step.  Three slots: they were
     // issued one step ago, and this step's own transfers (UK instructions for K, U for V) stay in
