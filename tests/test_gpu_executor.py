@@ -88,6 +88,44 @@ def test_executor_matches_oracle_and_entry_points(case):
                 assert np.array_equal(ex["dq"], gpu["dq_bf16"])
 
 
+# many (run, head) items, several times the GPU's resident workgroups, through the executor's
+# partial and fused forwards and through the entry points
+MANY_ITEMS = [
+    # N, P, layout, hq, hkv, d, bm, bn, mean doc length
+    (8192, 2, "contiguous", 32, 32, 128, 128, 128, 300),
+    # K/V heads a multiple of 8: a group's query heads placed on one XCD
+    (16384, 4, "zigzag", 32, 8, 128, 128, 128, 500),
+    # documents of 1..7 tokens: masked tiles throughout, runs of a single tile, chunks that no
+    # query reaches
+    (8192, 2, "contiguous", 32, 16, 128, 128, 128, 4),
+    # one document: runs of up to 32 tiles (two windows), split into pieces by the planner
+    (8192, 2, "contiguous", 32, 32, 128, 128, 128, 8192),
+]
+
+
+@pytest.mark.parametrize("case", MANY_ITEMS)
+def test_executor_many_items(case):
+    N, P, layout, hq, hkv, d, bm, bn, mean = case
+    cu = _cu(np.random.default_rng(N + P + hkv), N, mean)
+    r = P - 1
+    c = Case(cu, N, P, layout, r, hq, hkv, d, bm, bn, seed=40 + r, backward=False)
+    ref = c.run_oracle()
+    for split in (-1, 0):
+        _say("executor, many items", case, "shard", r, "split", split)
+        ex = c.run_executor(max_run_tiles=split)
+        info = ex["info"]
+        assert info["num_runs_q"] * hq > 512 and info["num_runs_all"] * hq > 512, info
+        rep = {"o": max_abs(ex["o"], ref["o"]), "lse": max_abs(ex["lse"], ref["lse"]),
+               "o_fused": max_abs(ex["o_fused"], ref["o"]), "lse_fused": max_abs(ex["lse_fused"], ref["lse"])}
+        _say(rep, info)
+        assert rep["o"] <= O_ATOL and rep["o_fused"] <= O_ATOL, rep
+        assert rep["lse"] <= LSE_ATOL and rep["lse_fused"] <= LSE_ATOL, rep
+        assert np.array_equal(ex["o_staged"], ex["o"]) and np.array_equal(ex["lse_staged"], ex["lse"])
+        gpu = c.run_gpu(max_run_tiles=info["split_length"])
+        assert np.array_equal(ex["o"], gpu["o"]) and np.array_equal(ex["lse"], gpu["lse"])
+        assert np.array_equal(ex["o_fused"], gpu["o_fused"]) and np.array_equal(ex["lse_fused"], gpu["lse_fused"])
+
+
 def test_executor_replans_other_batches():
     """One executor, three batches in a row (the second needs more partials than the
     first, so the partial workspace grows), then the first batch again: every result
