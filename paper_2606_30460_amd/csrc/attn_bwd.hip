@@ -383,7 +383,7 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   __shared__ __attribute__((aligned(16))) __bf16 Qs[3][SUB * D];
   __shared__ __attribute__((aligned(16))) __bf16 dOs[3][SUB * D];
   __shared__ __attribute__((aligned(16))) float lse_s[3][SUB];
-  __shared__ __attribute__((aligned(16))) float delta_s[3][SUB];
+  __shared__ __attribute__((aligned(16))) float ndelta_s[3][SUB];  // -delta
   __shared__ __attribute__((aligned(16))) int32_t start_s[3][SUB];
   // P hand-off in fp16 (two buffers: P of sub-tile t + 1 is written while the dP wave reads P of
   // t), per key block and 32-query block: lane l's 16 values as two 16-byte pieces at [half][l]
@@ -508,7 +508,7 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
   auto store_sub = [&](int buf) {
     if (tid < SUB) {
       lse_s[buf][tid] = lreg == -__builtin_inff() ? __builtin_inff() : lreg * LOG2E;  // no key: P = 0
-      delta_s[buf][tid] = dreg;
+      ndelta_s[buf][tid] = -dreg;
       start_s[buf][tid] = sreg;
     }
   };
@@ -526,9 +526,24 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
       bf16x8 ra[D / 16];
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) ra[kk] = *(const bf16x8*)(R + 32 * qb * D + rowoff[kk]);
-      sp[qb] = f32x16{};
+      if (s_wave) {
+        sp[qb] = f32x16{};
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) sp[qb] = mfma32(ra[kk], kv[kk], sp[qb]);
+        for (int kk = 0; kk < D / 16; ++kk) sp[qb] = mfma32(ra[kk], kv[kk], sp[qb]);
+      } else {
+        // the products accumulate onto -delta of each query (register j = 4 cq + e), so the
+        // chain ends with dP - delta and dS takes one multiply per element
+        f32x16 init;
+#pragma unroll
+        for (int cq = 0; cq < 4; ++cq) {
+          const f32x4 d4 = *(const f32x4*)(&ndelta_s[rb][32 * qb + 8 * cq + 4 * hi]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) init[4 * cq + e] = d4[e];
+        }
+        sp[qb] = init;
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) sp[qb] = mfma32(ra[kk], kv[kk], sp[qb]);
+      }
     }
     if (s_wave) {
 #pragma unroll
@@ -581,16 +596,11 @@ __global__ __launch_bounds__(512, 2) void attn_bwd_dkdv_split_kernel(BwdArgs a) 
           bt[half][mb] = cat4(ds_read_tr16(T + rb + troff[mb][0]), ds_read_tr16(T + rb + 8 * D + troff[mb][1]));
       }
       if (!s_wave) {
+        // dS = P (dP - delta): one mixed-precision multiply per element (fp16 P, fp32 dP - delta)
         const h16x8 ph[2] = {Px[pbuf][kb][qb][0][lane], Px[pbuf][kb][qb][1][lane]};
 #pragma unroll
-        for (int cq = 0; cq < 4; ++cq) {
-          const f32x4 d4 = *(const f32x4*)(&delta_s[tb][32 * qb + 8 * cq + 4 * hi]);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int j = 4 * cq + e;
-            opnd[qb][j >> 3][j & 7] = (__bf16)((float)ph[j >> 3][j & 7] * (sp[qb][j] - d4[e]));
-          }
-        }
+        for (int j = 0; j < 16; ++j)
+          opnd[qb][j >> 3][j & 7] = (__bf16)__builtin_fmaf((float)ph[j >> 3][j & 7], sp[qb][j], 0.f);
       }
 #pragma unroll
       for (int half = 0; half < 2; ++half)
@@ -746,6 +756,9 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
       dlt = a.delta[(int64_t)h * n + qrow];
     }
   }
+  f32x16 ndlt;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) ndlt[j] = -dlt;
   const int tr_row = 4 * hi + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   int rowoff[D / 16], troff[MB][2];
@@ -850,7 +863,8 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
     if (live) {
 #pragma unroll
       for (int nb = 0; nb < KB / 32; ++nb) {
-        f32x16 st{}, dpt{};
+        // dP^T accumulates onto -delta (ndlt), so the chain ends with dP^T - delta
+        f32x16 st{}, dpt = ndlt;
 #pragma unroll
         for (int kk = 0; kk < D / 16; ++kk) {
           st = mfma32(*(const bf16x8*)(K + 32 * nb * D + rowoff[kk]), qf[kk], st);
@@ -866,7 +880,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_bwd_dq_kernel(BwdArgs a) {
         }
         bf16x8 sb[2];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) sb[j >> 3][j & 7] = (__bf16)(p[j] * (dpt[j] - dlt));
+        for (int j = 0; j < 16; ++j) sb[j >> 3][j & 7] = (__bf16)(p[j] * dpt[j]);
         // dQ^T += K^T dS^T, 16 keys per MFMA
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
